@@ -1,0 +1,332 @@
+"""CPU oracle for the OPTIMA weight-update hot path.
+
+TEST INFRASTRUCTURE ONLY. Nothing in the product path may import, call or link
+this module: only the tests, the smoke check and the benchmark's CPU-baseline
+leg use it. It is a plain, slow, fp64 NumPy restatement of what the method
+computes, written from the paper (OPTIMA, arXiv 2512.13886); it shares no code,
+constants or helpers with the HIP library.
+
+What each function follows
+--------------------------
+hessian          Section 3.4 "Hessian calculation": H = sum over calibration
+                 sequences y_i of y_i^T y_i (the incremental form of Y^T Y).
+damp             Not in the paper (it only states H = X^T X is PSD, Eq. (6)).
+                 Reading: H + lambda I with lambda = rel * trace(H) / d, which
+                 makes every column QP strictly convex (unique optimum).
+power_iteration  Step size of the first-order solver (Section 3.3 names rAPDHG
+                 but prints no step rule). Reading: Rayleigh quotient of the
+                 power iteration started from a given vector.
+objective        Eq. (4)/(6): f_j = dw_j^T H dw_j with dw_j = w_j - w0_j.
+closed_form      Eq. (10)-(11): the unconstrained QP over the kept set I has
+                 Q = H_II, c = -2 H_IS w_S, so dw_I = H_II^{-1} H_IS w_S and
+                 w_I = w0_I + H_II^{-1} H_IS w0_S, w_S = 0 (Cholesky of H_II).
+kkt_solve        Eq. (6) solved through its KKT system (stationarity plus the
+                 equality constraints of Eq. (5)) with a dense LU solve; used on
+                 tiny d only, as an independent check of closed_form.
+rapdhg           Section 3.3 / 3.4: the batched restarted accelerated
+                 primal-dual hybrid gradient solve of Eq. (6), with the pruned
+                 entries fixed through equal lower and upper bounds (Section 3.4
+                 "Equality constraints"). The paper only cites the algorithm, so
+                 the iteration below is this module's reading of it for a QP
+                 whose only constraints are bounds (the dual block is empty):
+                   alpha_k = 2/(k+2), eta_k = (k+1)/(2L), L = 2 lambda_max (1+delta)
+                   x_md = (1-alpha) x_ag + alpha x
+                   g    = 2 H (x_md - w0)              (gradient of Eq. (6))
+                   x    = sel(mask, x - eta g, 0)       (projection on the bounds)
+                   x_ag = (1-alpha) x_ag + alpha x
+                 Every `check_every` iterations (and at the last one) the
+                 iterate x and the average x_ag are scored by
+                   r_d = ||g_K||_2, gap = |z^T g|, KKT = sqrt(r_d^2 + gap^2)
+                 and the lower-KKT one is the candidate (ties: x_ag). A column
+                 terminates when r_d <= eps_abs + eps_rel ||2 H w0||_2 and
+                 gap <= eps_abs + eps_rel (|P| + |D|), P = f(cand),
+                 D = -cand^T H cand + w0^T H w0 (Appendix D tolerances). A
+                 restart to the candidate happens on sufficient decay
+                 (KKT <= 0.2 KKT_restart), on necessary decay without local
+                 progress (KKT <= 0.8 KKT_restart and KKT > KKT_previous check),
+                 or when the inner loop is long (k >= 0.36 t); it is accepted
+                 only if it does not raise the objective above the last
+                 restart point's.
+
+Parity status
+-------------
+hessian, damp, objective, closed_form, kkt_solve: pinned by brute force, exact
+rational arithmetic and closed forms in the CPU tests. power_iteration: pinned
+by LAPACK eigenvalues. rapdhg: its fixed point is pinned by closed_form and its
+iterates by the invariants (pruned entries exactly +0.0, accepted restarts never
+raise the objective, the accelerated O(1/k^2) bound without restarts); the exact
+trajectory (step schedule, restart constants) is the reading above and is
+"parity unpinned": the paper prints no trajectory to compare against.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import scipy.linalg
+
+
+# ----------------------------------------------------------------------------
+# Hessian, damping, spectral norm
+# ----------------------------------------------------------------------------
+
+def hessian(chunks) -> np.ndarray:
+    """H = sum_i y_i^T y_i over calibration sequences y_i (Section 3.4)."""
+    H = None
+    for y in chunks:
+        y = np.asarray(y, dtype=np.float64)
+        if H is None:
+            H = np.zeros((y.shape[1], y.shape[1]))
+        H += y.T @ y
+    if H is None:
+        raise ValueError("no calibration chunks")
+    return H
+
+
+def damp(H: np.ndarray, rel: float = 0.01):
+    """Return (H + lambda I, lambda) with lambda = rel * trace(H) / d."""
+    H = np.asarray(H, dtype=np.float64)
+    lam = rel * np.trace(H) / H.shape[0]
+    return H + lam * np.eye(H.shape[0]), lam
+
+
+def power_iteration(H: np.ndarray, v0: np.ndarray, max_iters: int = 1000,
+                    tol: float = 1e-6):
+    """Largest eigenvalue of symmetric PSD H by power iteration.
+
+    Iteration i computes y = H v (v of unit length), the Rayleigh quotient
+    rho_i = v^T y, and v <- y / ||y||. It stops when
+    |rho_i - rho_{i-1}| <= tol * rho_i, or after max_iters iterations.
+    Returns (rho, iterations).
+    """
+    H = np.asarray(H, dtype=np.float64)
+    v = np.asarray(v0, dtype=np.float64)
+    v = v / np.linalg.norm(v)
+    rho_prev = None
+    rho = 0.0
+    for it in range(1, max_iters + 1):
+        y = H @ v
+        rho = float(v @ y)
+        ny = np.linalg.norm(y)
+        if ny == 0.0:
+            return 0.0, it
+        v = y / ny
+        if rho_prev is not None and abs(rho - rho_prev) <= tol * abs(rho):
+            return rho, it
+        rho_prev = rho
+    return rho, max_iters
+
+
+# ----------------------------------------------------------------------------
+# The column QPs: objective, closed form, KKT
+# ----------------------------------------------------------------------------
+
+def objective(H: np.ndarray, W0: np.ndarray, W: np.ndarray) -> np.ndarray:
+    """f_j = (w_j - w0_j)^T H (w_j - w0_j) for every row j (Eq. (4))."""
+    D = np.asarray(W, dtype=np.float64) - np.asarray(W0, dtype=np.float64)
+    return np.einsum("ij,ij->i", D @ np.asarray(H, dtype=np.float64), D)
+
+
+def closed_form(H: np.ndarray, W0: np.ndarray, mask: np.ndarray) -> np.ndarray:
+    """Unique optimum of every column QP (Eq. (10)-(11)), via Cholesky of H_II."""
+    H = np.asarray(H, dtype=np.float64)
+    W0 = np.asarray(W0, dtype=np.float64)
+    keep = np.asarray(mask) != 0
+    W = np.zeros_like(W0)
+    for j in range(W0.shape[0]):
+        I = np.flatnonzero(keep[j])
+        S = np.flatnonzero(~keep[j])
+        if I.size == 0:
+            continue
+        rhs = H[np.ix_(I, S)] @ W0[j, S]
+        dw = scipy.linalg.cho_solve(scipy.linalg.cho_factor(H[np.ix_(I, I)]), rhs)
+        W[j, I] = W0[j, I] + dw
+    return W
+
+
+def kkt_solve(H: np.ndarray, W0: np.ndarray, mask: np.ndarray) -> np.ndarray:
+    """Optimum of Eq. (6) from its KKT system, one dense solve per column.
+
+    Unknowns (dw, nu): stationarity 2 H dw + E_S^T nu = 0 and feasibility
+    E_S dw = -w0_S (Eq. (5)), E_S selecting the pruned entries.
+    """
+    H = np.asarray(H, dtype=np.float64)
+    W0 = np.asarray(W0, dtype=np.float64)
+    keep = np.asarray(mask) != 0
+    n, d = W0.shape
+    W = np.zeros_like(W0)
+    for j in range(n):
+        S = np.flatnonzero(~keep[j])
+        m = S.size
+        K = np.zeros((d + m, d + m))
+        K[:d, :d] = 2.0 * H
+        E = np.zeros((m, d))
+        E[np.arange(m), S] = 1.0
+        K[:d, d:] = E.T
+        K[d:, :d] = E
+        rhs = np.concatenate([np.zeros(d), -W0[j, S]])
+        sol = np.linalg.solve(K, rhs)
+        W[j] = W0[j] + sol[:d]
+        W[j, S] = 0.0  # the constraint holds exactly
+    return W
+
+
+# ----------------------------------------------------------------------------
+# rAPDHG
+# ----------------------------------------------------------------------------
+
+@dataclass
+class SolverOptions:
+    max_iters: int = 100_000
+    check_every: int = 64
+    fixed_iters: bool = False      # run exactly max_iters (checks still restart)
+    eps_rel: float = 0.01
+    eps_abs: float = 0.01
+    beta_sufficient: float = 0.2
+    beta_necessary: float = 0.8
+    beta_artificial: float = 0.36
+    step_safety: float = 1e-3      # L = 2 lambda_max (1 + step_safety)
+    restarts: bool = True
+
+
+@dataclass
+class SolveResult:
+    W: np.ndarray
+    iters: np.ndarray
+    restarts: np.ndarray
+    converged: np.ndarray
+    f_initial: np.ndarray
+    f_final: np.ndarray
+    kkt_final: np.ndarray
+    anchors: list = field(default_factory=list)  # per column: f at each accepted restart
+
+
+def _score(H, W0, keep, Z):
+    """Per-row r_d, gap, KKT, f and z^T H z of candidate rows Z."""
+    dZ = Z - W0
+    HdZ = dZ @ H                      # rows of H (z - w0); H is symmetric
+    G = 2.0 * HdZ
+    rd = np.sqrt(np.sum(np.where(keep, G, 0.0) ** 2, axis=1))
+    gap = np.abs(np.sum(Z * G, axis=1))
+    f = np.sum(dZ * HdZ, axis=1)
+    zHz = np.sum(Z * (Z @ H), axis=1)
+    return {"rd": rd, "gap": gap, "kkt": np.hypot(rd, gap), "f": f, "zHz": zHz}
+
+
+def check_decision(s_x: dict, s_a: dict, kkt_restart, kkt_prev, f_anchor, k, t,
+                   c_norm, w0Hw0, opts: SolverOptions):
+    """Candidate choice, termination test and restart test at one check.
+
+    Returns (use_x, converged, restart, s_cand). All inputs are per-column arrays.
+    """
+    use_x = s_x["kkt"] < s_a["kkt"]  # ties go to the average
+    s_c = {key: np.where(use_x, s_x[key], s_a[key]) for key in s_x}
+    P = s_c["f"]
+    D = -s_c["zHz"] + w0Hw0
+    converged = ((s_c["rd"] <= opts.eps_abs + opts.eps_rel * c_norm)
+                 & (s_c["gap"] <= opts.eps_abs + opts.eps_rel * (np.abs(P) + np.abs(D))))
+    kc = s_c["kkt"]
+    cond = ((kc <= opts.beta_sufficient * kkt_restart)
+            | ((kc <= opts.beta_necessary * kkt_restart) & (kc > kkt_prev))
+            | (k >= opts.beta_artificial * t))
+    restart = cond & (s_c["f"] <= f_anchor) if opts.restarts else np.zeros_like(cond)
+    return use_x, converged, restart, s_c
+
+
+def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
+           opts: SolverOptions | None = None, observer=None) -> SolveResult:
+    """Solve all column QPs of Eq. (6) side by side (one row of W0 per QP).
+
+    `observer(t, x, x_ag)`, if given, sees the iterates after every iteration
+    (before that iteration's check); it must not modify them.
+    """
+    opts = opts or SolverOptions()
+    H = np.asarray(H, dtype=np.float64)
+    W0 = np.asarray(W0, dtype=np.float64)
+    keep = np.asarray(mask) != 0
+    n, d = W0.shape
+    L = 2.0 * float(lambda_max) * (1.0 + opts.step_safety)
+
+    def sel(V):
+        return np.where(keep, V, 0.0)
+
+    x = sel(W0)
+    xa = x.copy()
+    Hw0 = W0 @ H
+    c_norm = np.linalg.norm(2.0 * Hw0, axis=1)
+    w0Hw0 = np.sum(W0 * Hw0, axis=1)
+
+    k = np.zeros(n, dtype=np.int64)
+    done = np.zeros(n, dtype=bool)
+    out = {"W": np.zeros_like(W0), "iters": np.zeros(n, dtype=np.int64),
+           "restarts": np.zeros(n, dtype=np.int64),
+           "converged": np.zeros(n, dtype=bool), "f_final": np.zeros(n),
+           "kkt_final": np.zeros(n)}
+    anchors = [[] for _ in range(n)]
+
+    s0 = _score(H, W0, keep, x)
+    f_initial = s0["f"].copy()
+    kkt_restart = s0["kkt"].copy()
+    kkt_prev = s0["kkt"].copy()
+    f_anchor = s0["f"].copy()
+
+    def finish(rows, Z, s, t, conv):
+        out["W"][rows] = Z[rows]
+        out["iters"][rows] = t
+        out["converged"][rows] = conv[rows]
+        out["f_final"][rows] = s["f"][rows]
+        out["kkt_final"][rows] = s["kkt"][rows]
+        done[rows] = True
+
+    # Termination test at the start point (all-kept or all-pruned columns).
+    P0, D0 = s0["f"], -s0["zHz"] + w0Hw0
+    conv0 = ((s0["rd"] <= opts.eps_abs + opts.eps_rel * c_norm)
+             & (s0["gap"] <= opts.eps_abs + opts.eps_rel * (np.abs(P0) + np.abs(D0))))
+    if opts.max_iters <= 0:
+        finish(np.ones(n, dtype=bool), x, s0, 0, conv0)
+    elif not opts.fixed_iters:
+        finish(conv0, x, s0, 0, conv0)
+
+    t = 0
+    while t < opts.max_iters and not done.all():
+        act = ~done
+        alpha = (2.0 / (k + 2.0))[:, None]
+        eta = ((k + 1.0) / (2.0 * L))[:, None]
+        x_md = (1.0 - alpha) * xa + alpha * x
+        g = 2.0 * ((x_md - W0) @ H)
+        x_new = sel(x - eta * g)
+        xa_new = (1.0 - alpha) * xa + alpha * x_new
+        x[act] = x_new[act]
+        xa[act] = xa_new[act]
+        k[act] += 1
+        t += 1
+        if observer is not None:
+            observer(t, x, xa)
+        if t % opts.check_every and t != opts.max_iters:
+            continue
+        s_x = _score(H, W0, keep, x)
+        s_a = _score(H, W0, keep, xa)
+        use_x, conv, restart, s_c = check_decision(
+            s_x, s_a, kkt_restart, kkt_prev, f_anchor, k, t, c_norm, w0Hw0, opts)
+        cand = np.where(use_x[:, None], x, xa)
+        if not opts.fixed_iters:
+            stop = act & conv
+            finish(stop, cand, s_c, t, conv)
+            act = act & ~stop
+        acc = act & restart
+        x[acc] = cand[acc]
+        xa[acc] = cand[acc]
+        k[acc] = 0
+        kkt_restart[acc] = s_c["kkt"][acc]
+        f_anchor[acc] = s_c["f"][acc]
+        out["restarts"][acc] += 1
+        for j in np.flatnonzero(acc):
+            anchors[j].append(float(s_c["f"][j]))
+        kkt_prev[act] = s_c["kkt"][act]
+        if t == opts.max_iters:
+            finish(act, cand, s_c, t, conv)
+
+    return SolveResult(W=out["W"], iters=out["iters"], restarts=out["restarts"],
+                       converged=out["converged"], f_initial=f_initial,
+                       f_final=out["f_final"], kkt_final=out["kkt_final"],
+                       anchors=anchors)

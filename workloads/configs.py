@@ -1,0 +1,84 @@
+"""Layer configurations for the synthetic workloads.
+
+Each configuration describes one pruned linear layer: the calibration token
+matrix X (n_tok x d, streamed in sequences of `chunk` tokens, as in the
+incremental Hessian of Section 3.4), the dense weight W0 (n_cols x d, one QP per
+row, i.e. per output column of the paper's d_in x d_out weight, Eq. (3)), and
+the mask recipe. The shapes and value distributions stand in for the paper's
+128 x 2048-token C4 calibration set (Appendix D, Table 8); no C4 data is used.
+
+This module holds no arithmetic of the method: it only names sizes and seeds.
+"""
+from dataclasses import dataclass, field, replace
+
+
+@dataclass(frozen=True)
+class LayerConfig:
+    name: str
+    cfg_id: int            # first word of every seed sequence of this layer
+    d: int                 # d_in: QP dimension and Hessian side
+    n_cols: int            # d_out: number of column QPs
+    n_tok: int             # calibration tokens (sequences x sequence length)
+    chunk: int             # tokens per calibration sequence
+    x_dtype: str           # "f32" or "bf16": storage type of X
+    w_dtype: str           # "f32" or "bf16": storage type of W0 (values only)
+    w_std: float           # W0 ~ N(0, w_std^2)
+    x_recipe: str          # "ar1" | "lognormal" | "student_t_outliers" | "silu_gated"
+    mask_kind: str         # "unstructured" | "2:4"
+    sparsity: float        # fraction pruned per column (unstructured)
+    rel_damp: float = 0.01  # lambda = rel_damp * mean(diag(X^T X))
+    n_outliers: int = 8
+    outlier_scale: float = 50.0
+    t_dof: int = 4
+    tensor_offset: int = 0  # added to tensor ids (block matrices use 10*k)
+
+    @property
+    def n_chunks(self) -> int:
+        return (self.n_tok + self.chunk - 1) // self.chunk
+
+    def with_tokens(self, n_tok: int) -> "LayerConfig":
+        """Same layer with fewer (or more) calibration tokens."""
+        return replace(self, n_tok=n_tok)
+
+    def with_cols(self, n_cols: int) -> "LayerConfig":
+        return replace(self, n_cols=n_cols)
+
+
+# Tensor ids inside a layer's seed sequence [cfg_id, tensor_id, index].
+TENSOR_X = 0
+TENSOR_W0 = 1
+TENSOR_OUTLIERS = 2
+TENSOR_SCALES = 3
+TENSOR_V0 = 4          # start vector of the power iteration
+TENSOR_GATE = 5        # second factor of the SiLU-gated activations
+
+TINY = LayerConfig(
+    name="tiny", cfg_id=0, d=128, n_cols=64, n_tok=512, chunk=512,
+    x_dtype="f32", w_dtype="f32", w_std=0.02, x_recipe="ar1",
+    mask_kind="unstructured", sparsity=0.5)
+
+GPT2_FC = LayerConfig(
+    name="gpt2_fc", cfg_id=1, d=768, n_cols=3072, n_tok=128 * 2048, chunk=2048,
+    x_dtype="bf16", w_dtype="bf16", w_std=0.02, x_recipe="lognormal",
+    mask_kind="unstructured", sparsity=0.5)
+
+Q_PROJ = LayerConfig(
+    name="q_proj", cfg_id=2, d=4096, n_cols=4096, n_tok=128 * 2048, chunk=2048,
+    x_dtype="bf16", w_dtype="bf16", w_std=0.015, x_recipe="student_t_outliers",
+    mask_kind="2:4", sparsity=0.5)
+
+DOWN_PROJ = LayerConfig(
+    name="down_proj", cfg_id=3, d=14336, n_cols=4096, n_tok=128 * 2048, chunk=2048,
+    x_dtype="bf16", w_dtype="bf16", w_std=0.015, x_recipe="silu_gated",
+    mask_kind="unstructured", sparsity=0.6)
+
+CONFIGS = {c.name: c for c in (TINY, GPT2_FC, Q_PROJ, DOWN_PROJ)}
+
+
+@dataclass(frozen=True)
+class SolverSettings:
+    """Solver budgets used with the configurations (Appendix D, Table 8)."""
+    paper_eps: float = 0.01        # relative and absolute tolerance
+    paper_max_iters: int = 100_000
+    check_every: int = 64
+    tiny_fixed_iters: int = 1000
