@@ -1,0 +1,191 @@
+/*
+ * optima.h -- C ABI of the OPTIMA weight-update hot path on AMD MI355X (gfx950).
+ *
+ * OPTIMA (arXiv 2512.13886) rewrites the layer-wise weight reconstruction that
+ * follows mask selection as one quadratic program per output column (Eq. (3)-(6)):
+ *
+ *     minimise  (w_j - w0_j)^T H (w_j - w0_j)   subject to  w_j[i] = 0 for every
+ *     pruned entry i (mask[j][i] == 0),
+ *
+ * with one Hessian H = X^T X shared by all columns of the layer. The library
+ * computes H from calibration tokens, damps it, estimates its spectral norm and
+ * solves all column QPs together with a batched restarted accelerated
+ * primal-dual hybrid gradient (rAPDHG) method (Section 3.3-3.4, Algorithm 1).
+ *
+ * Conventions shared by every call
+ *   - Matrices are row-major. The weight and mask are stored [n_cols][d]: row j
+ *     holds the QP of output column j (the PyTorch Linear layout; the paper
+ *     writes W as d_in x d_out, Eq. (3)).
+ *   - Mask bytes: 1 keeps the weight, 0 prunes it (Eq. (1)).
+ *   - Every pointer argument is a device pointer owned by the caller unless
+ *     stated otherwise; the library keeps no pointer after a call returns and
+ *     allocates no device memory. Work buffers come from the caller through a
+ *     `ws` argument sized by the matching *_workspace_bytes query.
+ *   - All calls are ordered on `stream` (NULL = the default stream).
+ *   - Errors are returned before any kernel is launched when they come from
+ *     argument validation. HIP failures map to OPTIMA_E_HIP.
+ */
+#ifndef OPTIMA_H
+#define OPTIMA_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int optima_status;
+
+#define OPTIMA_OK 0
+#define OPTIMA_E_INVAL (-1)       /* NULL pointer, bad size, misaligned or aliased buffer */
+#define OPTIMA_E_HIP (-2)         /* a HIP runtime call or kernel launch failed */
+#define OPTIMA_E_NONFINITE (-3)   /* NaN or Inf in H, W0 or the spectral norm */
+#define OPTIMA_E_WORKSPACE (-4)   /* ws NULL or smaller than the size query returned */
+#define OPTIMA_E_UNSUPPORTED (-5) /* unsupported dtype, or the device is not gfx950 */
+
+#define OPTIMA_DTYPE_F32 0
+#define OPTIMA_DTYPE_BF16 1
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* optima_status_string(optima_status status);
+
+/* Library ABI version (increments on any signature change). */
+int optima_abi_version(void);
+
+/* ---------------------------------------------------------------------------
+ * Hessian accumulation -- Section 3.4 "Hessian calculation", Algorithm 1.
+ *
+ * H[d][d] (fp32) = (accumulate ? H : 0) + X^T X, where X[n_tok][d] holds n_tok
+ * calibration tokens (one or many 2048-token sequences; the paper sums
+ * y_i^T y_i sequence by sequence, which gives the same matrix as stacking).
+ * X is fp32 (dtype OPTIMA_DTYPE_F32) or bf16 (OPTIMA_DTYPE_BF16); products are
+ * formed exactly and summed in fp32. Both triangles of H are written and the
+ * result is exactly symmetric; with accumulate = 1 the lower triangle of the
+ * incoming H is read and taken as the whole matrix. n_tok = 0 leaves H as it is
+ * (accumulate = 1) or zeroes it. X must be 16-byte aligned; H may alias nothing
+ * else. ws must hold optima_hessian_workspace_bytes(n_tok, d, dtype) bytes
+ * (token-slab transpose buffer and split-K partial sums).
+ * ------------------------------------------------------------------------- */
+size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype);
+optima_status optima_hessian_accumulate(const void* X, int dtype, int64_t n_tok,
+                                        int64_t d, float* H, int accumulate,
+                                        void* ws, size_t ws_bytes,
+                                        hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Damping. The paper's H = X^T X is only positive semi-definite (Eq. (6));
+ * this call adds lambda * I with lambda = rel_damp * trace(H) / d, which makes
+ * every column QP strictly convex so its optimum (Eq. (10)-(11)) is unique.
+ * The trace is summed in fp64 on the device. lambda_out (device, one float,
+ * required) receives lambda; if the trace is not finite, H is left unchanged
+ * and lambda_out receives NaN (the solve then reports OPTIMA_E_NONFINITE).
+ * ------------------------------------------------------------------------- */
+optima_status optima_hessian_damp(float* H, int64_t d, float rel_damp,
+                                  float* lambda_out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Spectral norm of H for the solver's step size (Section 3.3: the first-order
+ * method's bottleneck is products with H; its step needs ||Q|| = 2 lambda_max).
+ * Power iteration from the caller's start vector v0[d] (device, not modified):
+ * iteration i forms y = H v with v of unit length, rho_i = v^T y and
+ * v <- y / ||y||, stopping once |rho_i - rho_{i-1}| <= tol * rho_i or after
+ * max_iters iterations. lambda_max (device, one float) receives the last rho;
+ * iters (device int32, may be NULL) the iteration count. H must be symmetric
+ * and 16-byte aligned. Blocking: the call synchronises `stream` a few times to
+ * test convergence. ws: optima_spectral_norm_workspace_bytes(d) bytes.
+ * ------------------------------------------------------------------------- */
+size_t optima_spectral_norm_workspace_bytes(int64_t d);
+optima_status optima_spectral_norm(const float* H, int64_t d, const float* v0,
+                                   int max_iters, float tol, void* ws,
+                                   size_t ws_bytes, float* lambda_max,
+                                   int32_t* iters, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Batched column-QP solve -- Eq. (6), Algorithm 1, Section 3.3-3.4.
+ *
+ * For every row j < n_cols of W0 (fp32 values) and mask (uint8), writes
+ *   W_out[j] = argmin (w - W0[j])^T H (w - W0[j])  s.t. w[i] = +0.0 where
+ *              mask[j][i] == 0,
+ * reached with the batched rAPDHG iteration. The pruned entries are fixed
+ * through equal lower and upper bounds (Section 3.4), i.e. the projection
+ * keeps them at exactly +0.0 (bit pattern 0). Per column j, with
+ * alpha_k = 2/(k+2), eta_k = (k+1)/(2L), L = 2 lambda_max (1 + step_safety):
+ *   x_md = (1-alpha) x_ag + alpha x;  g = 2 H (x_md - w0);
+ *   x = sel(mask, x - eta g, +0);     x_ag = (1-alpha) x_ag + alpha x,
+ * starting from x = x_ag = sel(mask, w0, +0). Every check_every iterations
+ * (and at max_iters) x and x_ag are scored by r_d = ||g restricted to kept
+ * entries||, gap = |z^T g|, KKT = sqrt(r_d^2 + gap^2); the lower-KKT one is the
+ * candidate (ties: x_ag). A column terminates (unless fixed_iters) when
+ * r_d <= eps_abs + eps_rel ||2 H w0|| and gap <= eps_abs + eps_rel (|P| + |D|)
+ * with P = f(cand), D = w0^T H w0 - cand^T H cand (Appendix D tolerances). It
+ * restarts to the candidate on KKT decay by beta_sufficient, on decay by
+ * beta_necessary without progress since the last check, or when the iterations
+ * since the last restart reach beta_artificial times the total; a restart is
+ * accepted only if it does not raise the objective above the previous restart
+ * point's. Columns are fully independent: the result for a column does not
+ * depend on the others in the batch (Algorithm 1 batching).
+ *
+ * H: [d][d] fp32, symmetric, 16-byte aligned. lambda_max: device float (from
+ * optima_spectral_norm or the caller). W_out: [n_cols][d] fp32, must not
+ * overlap W0. stats (host struct of device arrays, may be NULL; each array may
+ * be NULL): per column iterations run, accepted restarts, convergence flag,
+ * objective at the start point sel(mask, w0, 0), objective and KKT of W_out
+ * (computed on the device from the maintained products). info (host, may be
+ * NULL) receives run totals. ws: optima_qp_workspace_bytes(d, n_cols) bytes.
+ * Blocking: the call synchronises `stream` once per check to learn how many
+ * columns are still active. Non-convergence is not an error; it is reported
+ * per column. Returns OPTIMA_E_NONFINITE if H or W0 holds NaN/Inf or
+ * lambda_max is not a positive finite number.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int64_t max_iters;      /* >= 0; the paper uses 100000 (Table 8) */
+  int32_t check_every;    /* >= 1; default 64 */
+  int32_t fixed_iters;    /* 1: run exactly max_iters, checks only restart */
+  float eps_rel;          /* default 0.01 (Table 8) */
+  float eps_abs;          /* default 0.01 (Table 8) */
+  float beta_sufficient;  /* default 0.2 */
+  float beta_necessary;   /* default 0.8 */
+  float beta_artificial;  /* default 0.36 */
+  float step_safety;      /* default 1e-3 */
+  int32_t restarts;       /* 0 disables restarts; default 1 */
+  int32_t reserved;       /* must be 0 */
+} optima_solver_opts;
+
+typedef struct {
+  int32_t* iters;
+  int32_t* restarts;
+  uint8_t* converged;
+  float* f_initial;
+  float* f_final;
+  float* kkt_final;
+} optima_solve_stats;
+
+typedef struct {
+  int64_t iterations;         /* iterations run by the longest-running column */
+  int64_t gemm_calls;         /* H-product launches (including the two at setup) */
+  int64_t row_products;       /* sum over those launches of the columns multiplied */
+  int64_t checks;             /* check passes */
+  int64_t timed_launches;     /* H-product launches between checks (the iteration loop) */
+  int64_t timed_row_products; /* columns multiplied by those launches */
+  double timed_product_ms;    /* their device time, from HIP events recorded on `stream`
+                                 around each run of back-to-back product launches */
+} optima_solve_info;
+
+void optima_solver_opts_default(optima_solver_opts* opts);
+size_t optima_qp_workspace_bytes(int64_t d, int64_t n_cols);
+optima_status optima_qp_solve_batched(const float* H, int64_t d,
+                                      const float* lambda_max, const float* W0,
+                                      const uint8_t* mask, int64_t n_cols,
+                                      const optima_solver_opts* opts, void* ws,
+                                      size_t ws_bytes, float* W_out,
+                                      const optima_solve_stats* stats,
+                                      optima_solve_info* info,
+                                      hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OPTIMA_H */

@@ -1,0 +1,244 @@
+"""ctypes binding of liboptima.so: argument marshalling only.
+
+Every function has the name of the C entry point it wraps, takes torch tensors
+(device memory) and passes their data pointers and the current HIP stream
+through. No computation of the method happens here. The library must exist:
+importing this module without it raises, there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, fields
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liboptima.so")
+
+OPTIMA_OK = 0
+OPTIMA_E_INVAL = -1
+OPTIMA_E_HIP = -2
+OPTIMA_E_NONFINITE = -3
+OPTIMA_E_WORKSPACE = -4
+OPTIMA_E_UNSUPPORTED = -5
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+
+
+class OptimaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(
+        f"{_LIB_PATH} is missing: build it with `python -m paper_2512_13886_amd.build`")
+_lib = ctypes.CDLL(_LIB_PATH)
+
+_i64, _i32, _sz, _vp, _f32 = ctypes.c_int64, ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_float
+
+
+class _Opts(ctypes.Structure):
+    _fields_ = [("max_iters", ctypes.c_int64), ("check_every", ctypes.c_int32),
+                ("fixed_iters", ctypes.c_int32), ("eps_rel", ctypes.c_float),
+                ("eps_abs", ctypes.c_float), ("beta_sufficient", ctypes.c_float),
+                ("beta_necessary", ctypes.c_float), ("beta_artificial", ctypes.c_float),
+                ("step_safety", ctypes.c_float), ("restarts", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+class _Stats(ctypes.Structure):
+    _fields_ = [("iters", _vp), ("restarts", _vp), ("converged", _vp),
+                ("f_initial", _vp), ("f_final", _vp), ("kkt_final", _vp)]
+
+
+class _Info(ctypes.Structure):
+    _fields_ = [("iterations", ctypes.c_int64), ("gemm_calls", ctypes.c_int64),
+                ("row_products", ctypes.c_int64), ("checks", ctypes.c_int64),
+                ("timed_launches", ctypes.c_int64), ("timed_row_products", ctypes.c_int64),
+                ("timed_product_ms", ctypes.c_double)]
+
+
+def _sig(name, res, args):
+    f = getattr(_lib, name)
+    f.restype = res
+    f.argtypes = args
+    return f
+
+
+_status_string = _sig("optima_status_string", ctypes.c_char_p, [_i32])
+_abi_version = _sig("optima_abi_version", _i32, [])
+_hess_ws = _sig("optima_hessian_workspace_bytes", _sz, [_i64, _i64, _i32])
+_hess_acc = _sig("optima_hessian_accumulate", _i32,
+                 [_vp, _i32, _i64, _i64, _vp, _i32, _vp, _sz, _vp])
+_damp = _sig("optima_hessian_damp", _i32, [_vp, _i64, _f32, _vp, _vp])
+_spec_ws = _sig("optima_spectral_norm_workspace_bytes", _sz, [_i64])
+_spec = _sig("optima_spectral_norm", _i32,
+             [_vp, _i64, _vp, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
+_opts_default = _sig("optima_solver_opts_default", None, [ctypes.POINTER(_Opts)])
+_qp_ws = _sig("optima_qp_workspace_bytes", _sz, [_i64, _i64])
+_qp_solve = _sig("optima_qp_solve_batched", _i32,
+                 [_vp, _i64, _vp, _vp, _vp, _i64, ctypes.POINTER(_Opts), _vp, _sz, _vp,
+                  ctypes.POINTER(_Stats), ctypes.POINTER(_Info), _vp])
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def optima_status_string(status: int) -> str:
+    return _status_string(int(status)).decode()
+
+
+def optima_abi_version() -> int:
+    return int(_abi_version())
+
+
+def _check(status: int):
+    if status != OPTIMA_OK:
+        raise OptimaError(status, optima_status_string(status))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need_cuda(name, t, dtype=None):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _workspace(nbytes: int, ws, device):
+    if ws is not None:
+        _need_cuda("ws", ws)
+        return ws, ws.numel() * ws.element_size()
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device), int(nbytes)
+
+
+@dataclass
+class SolverOpts:
+    """Mirror of optima_solver_opts; defaults come from the library."""
+    max_iters: int = 0
+    check_every: int = 0
+    fixed_iters: int = 0
+    eps_rel: float = 0.0
+    eps_abs: float = 0.0
+    beta_sufficient: float = 0.0
+    beta_necessary: float = 0.0
+    beta_artificial: float = 0.0
+    step_safety: float = 0.0
+    restarts: int = 0
+    reserved: int = 0
+
+    @classmethod
+    def default(cls, **overrides) -> "SolverOpts":
+        c = _Opts()
+        _opts_default(ctypes.byref(c))
+        o = cls(**{f.name: getattr(c, f.name) for f in fields(cls)})
+        for k, v in overrides.items():
+            if not hasattr(o, k):
+                raise AttributeError(k)
+            setattr(o, k, v)
+        return o
+
+    def _c(self) -> _Opts:
+        return _Opts(**{f.name: getattr(self, f.name) for f in fields(self)})
+
+
+def optima_hessian_workspace_bytes(n_tok: int, d: int, dtype: int) -> int:
+    return int(_hess_ws(n_tok, d, dtype))
+
+
+def optima_hessian_accumulate(X: torch.Tensor, H: torch.Tensor, accumulate: bool = False,
+                              ws: torch.Tensor | None = None, stream=None) -> None:
+    """H (+)= X^T X for X [n_tok, d] (float32 or bfloat16), H [d, d] float32."""
+    _need_cuda("X", X)
+    _need_cuda("H", H, torch.float32)
+    if X.dim() != 2 or H.shape != (X.shape[1], X.shape[1]):
+        raise ValueError("X must be [n_tok, d] and H [d, d]")
+    dtype = {torch.float32: DTYPE_F32, torch.bfloat16: DTYPE_BF16}.get(X.dtype)
+    if dtype is None:
+        raise ValueError("X must be float32 or bfloat16")
+    n_tok, d = X.shape
+    ws, nbytes = _workspace(optima_hessian_workspace_bytes(n_tok, d, dtype), ws, X.device)
+    _check(_hess_acc(_ptr(X), dtype, n_tok, d, _ptr(H), int(bool(accumulate)), _ptr(ws),
+                     nbytes, _stream(stream)))
+
+
+def optima_hessian_damp(H: torch.Tensor, rel_damp: float, lambda_out: torch.Tensor,
+                        stream=None) -> None:
+    _need_cuda("H", H, torch.float32)
+    _need_cuda("lambda_out", lambda_out, torch.float32)
+    _check(_damp(_ptr(H), H.shape[0], float(rel_damp), _ptr(lambda_out), _stream(stream)))
+
+
+def optima_spectral_norm_workspace_bytes(d: int) -> int:
+    return int(_spec_ws(d))
+
+
+def optima_spectral_norm(H: torch.Tensor, v0: torch.Tensor, lambda_max: torch.Tensor,
+                         max_iters: int = 1000, tol: float = 1e-6,
+                         ws: torch.Tensor | None = None, iters: torch.Tensor | None = None,
+                         stream=None) -> None:
+    _need_cuda("H", H, torch.float32)
+    _need_cuda("v0", v0, torch.float32)
+    _need_cuda("lambda_max", lambda_max, torch.float32)
+    if iters is not None:
+        _need_cuda("iters", iters, torch.int32)
+    d = H.shape[0]
+    ws, nbytes = _workspace(optima_spectral_norm_workspace_bytes(d), ws, H.device)
+    _check(_spec(_ptr(H), d, _ptr(v0), int(max_iters), float(tol), _ptr(ws), nbytes,
+                 _ptr(lambda_max), _ptr(iters), _stream(stream)))
+
+
+def optima_qp_workspace_bytes(d: int, n_cols: int) -> int:
+    return int(_qp_ws(d, n_cols))
+
+
+def optima_qp_solve_batched(H: torch.Tensor, lambda_max: torch.Tensor, W0: torch.Tensor,
+                            mask: torch.Tensor, W_out: torch.Tensor,
+                            opts: SolverOpts | None = None, ws: torch.Tensor | None = None,
+                            stats: dict | None = None, stream=None) -> dict:
+    """Solves every row QP of W0 under `mask`; returns the run totals.
+
+    stats: optional dict of device tensors with keys among iters (int32),
+    restarts (int32), converged (uint8), f_initial, f_final, kkt_final (float32).
+    """
+    _need_cuda("H", H, torch.float32)
+    _need_cuda("lambda_max", lambda_max, torch.float32)
+    _need_cuda("W0", W0, torch.float32)
+    _need_cuda("mask", mask, torch.uint8)
+    _need_cuda("W_out", W_out, torch.float32)
+    n_cols, d = W0.shape
+    if H.shape != (d, d) or mask.shape != W0.shape or W_out.shape != W0.shape:
+        raise ValueError("shape mismatch between H, W0, mask and W_out")
+    opts = opts or SolverOpts.default()
+    ws, nbytes = _workspace(optima_qp_workspace_bytes(d, n_cols), ws, W0.device)
+    st = _Stats()
+    kinds = {"iters": torch.int32, "restarts": torch.int32, "converged": torch.uint8,
+             "f_initial": torch.float32, "f_final": torch.float32, "kkt_final": torch.float32}
+    for key, t in (stats or {}).items():
+        if key not in kinds:
+            raise KeyError(key)
+        _need_cuda(key, t, kinds[key])
+        if t.numel() != n_cols:
+            raise ValueError(f"stats[{key}] must have n_cols entries")
+        setattr(st, key, t.data_ptr())
+    info = _Info()
+    c_opts = opts._c()
+    _check(_qp_solve(_ptr(H), d, _ptr(lambda_max), _ptr(W0), _ptr(mask), n_cols,
+                     ctypes.byref(c_opts), _ptr(ws), nbytes, _ptr(W_out), ctypes.byref(st),
+                     ctypes.byref(info), _stream(stream)))
+    return {f[0]: getattr(info, f[0]) for f in _Info._fields_}

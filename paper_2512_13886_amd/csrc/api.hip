@@ -1,0 +1,138 @@
+// extern "C" entry points of liboptima.so: argument validation, then the
+// launch sequences in hessian.hip, spectral.hip and solver.hip.
+#include "common.h"
+
+namespace optima {
+size_t hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype);
+optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_t d, float* H,
+                                 int accumulate, void* ws, hipStream_t s);
+optima_status hessian_damp(float* H, int64_t d, float rel, float* lambda_out, hipStream_t s);
+size_t spectral_norm_workspace_bytes(int64_t d);
+optima_status spectral_norm(const float* H, int64_t d, const float* v0, int max_iters, float tol,
+                            void* ws, float* lambda_max, int32_t* iters, hipStream_t s);
+size_t qp_workspace_bytes(int64_t d, int64_t n_cols);
+optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const float* W0,
+                       const uint8_t* mask, int64_t n_cols, const optima_solver_opts& o, void* ws,
+                       float* W_out, const optima_solve_stats& stats, optima_solve_info* info,
+                       hipStream_t s);
+}  // namespace optima
+
+namespace {
+// Sizes are kept within 32-bit tile and row indices.
+constexpr int64_t kMaxDim = int64_t(1) << 20;
+constexpr int64_t kMaxCols = int64_t(1) << 24;
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+}  // namespace
+
+extern "C" {
+
+const char* optima_status_string(optima_status status) {
+  switch (status) {
+    case OPTIMA_OK: return "OPTIMA_OK";
+    case OPTIMA_E_INVAL: return "OPTIMA_E_INVAL: invalid argument";
+    case OPTIMA_E_HIP: return "OPTIMA_E_HIP: HIP runtime error";
+    case OPTIMA_E_NONFINITE: return "OPTIMA_E_NONFINITE: NaN or Inf in the input";
+    case OPTIMA_E_WORKSPACE: return "OPTIMA_E_WORKSPACE: workspace missing or too small";
+    case OPTIMA_E_UNSUPPORTED: return "OPTIMA_E_UNSUPPORTED: unsupported dtype or device";
+    default: return "OPTIMA: unknown status";
+  }
+}
+
+int optima_abi_version(void) { return 1; }
+
+size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
+  if (n_tok < 0 || d < 1 || d > kMaxDim) return 0;
+  if (dtype != OPTIMA_DTYPE_F32 && dtype != OPTIMA_DTYPE_BF16) return 0;
+  return optima::hessian_workspace_bytes(n_tok, d, dtype);
+}
+
+optima_status optima_hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_t d,
+                                        float* H, int accumulate, void* ws, size_t ws_bytes,
+                                        hipStream_t stream) {
+  if (dtype != OPTIMA_DTYPE_F32 && dtype != OPTIMA_DTYPE_BF16) return OPTIMA_E_UNSUPPORTED;
+  if (!H || n_tok < 0 || d < 1 || d > kMaxDim) return OPTIMA_E_INVAL;
+  if (n_tok > 0 && !X) return OPTIMA_E_INVAL;
+  const size_t esz = dtype == OPTIMA_DTYPE_BF16 ? 2 : 4;
+  if (X && (reinterpret_cast<uintptr_t>(X) % esz)) return OPTIMA_E_INVAL;
+  if (X && overlaps(X, size_t(n_tok) * size_t(d) * esz, H, size_t(d) * size_t(d) * 4))
+    return OPTIMA_E_INVAL;
+  if (n_tok > 0) {
+    const size_t need = optima::hessian_workspace_bytes(n_tok, d, dtype);
+    if (!ws || ws_bytes < need) return OPTIMA_E_WORKSPACE;
+  }
+  return optima::hessian_accumulate(X, dtype, n_tok, d, H, accumulate ? 1 : 0, ws, stream);
+}
+
+optima_status optima_hessian_damp(float* H, int64_t d, float rel_damp, float* lambda_out,
+                                  hipStream_t stream) {
+  if (!H || !lambda_out || d < 1 || d > kMaxDim) return OPTIMA_E_INVAL;
+  if (!(rel_damp >= 0.f)) return OPTIMA_E_INVAL;
+  return optima::hessian_damp(H, d, rel_damp, lambda_out, stream);
+}
+
+size_t optima_spectral_norm_workspace_bytes(int64_t d) {
+  if (d < 1 || d > kMaxDim) return 0;
+  return optima::spectral_norm_workspace_bytes(d);
+}
+
+optima_status optima_spectral_norm(const float* H, int64_t d, const float* v0, int max_iters,
+                                   float tol, void* ws, size_t ws_bytes, float* lambda_max,
+                                   int32_t* iters, hipStream_t stream) {
+  if (!H || !v0 || !lambda_max || d < 1 || d > kMaxDim || max_iters < 1 || !(tol >= 0.f))
+    return OPTIMA_E_INVAL;
+  if (!ws || ws_bytes < optima::spectral_norm_workspace_bytes(d)) return OPTIMA_E_WORKSPACE;
+  return optima::spectral_norm(H, d, v0, max_iters, tol, ws, lambda_max, iters, stream);
+}
+
+void optima_solver_opts_default(optima_solver_opts* o) {
+  if (!o) return;
+  o->max_iters = 100000;
+  o->check_every = 64;
+  o->fixed_iters = 0;
+  o->eps_rel = 0.01f;
+  o->eps_abs = 0.01f;
+  o->beta_sufficient = 0.2f;
+  o->beta_necessary = 0.8f;
+  o->beta_artificial = 0.36f;
+  o->step_safety = 1e-3f;
+  o->restarts = 1;
+  o->reserved = 0;
+}
+
+size_t optima_qp_workspace_bytes(int64_t d, int64_t n_cols) {
+  if (d < 1 || d > kMaxDim || n_cols < 0 || n_cols > kMaxCols) return 0;
+  return optima::qp_workspace_bytes(d, n_cols);
+}
+
+optima_status optima_qp_solve_batched(const float* H, int64_t d, const float* lambda_max,
+                                      const float* W0, const uint8_t* mask, int64_t n_cols,
+                                      const optima_solver_opts* opts, void* ws, size_t ws_bytes,
+                                      float* W_out, const optima_solve_stats* stats,
+                                      optima_solve_info* info, hipStream_t stream) {
+  if (!opts || d < 1 || d > kMaxDim || n_cols < 0 || n_cols > kMaxCols) return OPTIMA_E_INVAL;
+  if (info) *info = optima_solve_info{};
+  if (n_cols == 0) return OPTIMA_OK;
+  if (!H || !lambda_max || !W0 || !mask || !W_out) return OPTIMA_E_INVAL;
+  if (!optima::aligned16(H) || (reinterpret_cast<uintptr_t>(W0) & 3) ||
+      (reinterpret_cast<uintptr_t>(W_out) & 3))
+    return OPTIMA_E_INVAL;
+  const size_t wbytes = size_t(n_cols) * size_t(d) * sizeof(float);
+  if (overlaps(W0, wbytes, W_out, wbytes) || overlaps(H, size_t(d) * d * 4, W_out, wbytes) ||
+      overlaps(mask, size_t(n_cols) * d, W_out, wbytes))
+    return OPTIMA_E_INVAL;
+  const optima_solver_opts& o = *opts;
+  if (o.max_iters < 0 || o.check_every < 1 || o.reserved != 0) return OPTIMA_E_INVAL;
+  if (!(o.eps_rel >= 0.f) || !(o.eps_abs >= 0.f) || !(o.step_safety >= 0.f) ||
+      !(o.beta_sufficient >= 0.f) || !(o.beta_necessary >= 0.f) || !(o.beta_artificial >= 0.f))
+    return OPTIMA_E_INVAL;
+  if (!ws || ws_bytes < optima::qp_workspace_bytes(d, n_cols)) return OPTIMA_E_WORKSPACE;
+  optima_solve_stats st{};
+  if (stats) st = *stats;
+  return optima::qp_solve(H, d, lambda_max, W0, mask, n_cols, o, ws, W_out, st, info, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,714 @@
+// Batched column-QP solve (Eq. (6)) by restarted accelerated PDHG on gfx950.
+//
+// Per column j the state is x (two ping-pong buffers: the H-product reads one
+// while the fused update writes the other), the average x_ag, and the
+// maintained products Hx = H x, Hx_ag = H x_ag, Hw0 = H w0. All are fp32
+// [n_cols][dp] with dp = d rounded up to the 128-wide tile; padding entries
+// are zero and stay zero (they behave as pruned). With the products kept,
+// one iteration needs a single product with H:
+//   update   g = 2((1-a) Hx_ag + a Hx - Hw0), x' = sel(m, x - eta g, 0),
+//            x_ag' = (1-a) x_ag + a x'
+//   product  Hx' = H x', Hx_ag' = (1-a) Hx_ag + a Hx'
+// (H x_md = (1-a) Hx_ag + a Hx by linearity, so the gradient needs no second
+// product). The product kernel runs the next iteration's update in its
+// epilogue, element by element, so between checks each iteration is one
+// launch. Columns that terminate leave the active list; the products then run
+// over the active rows only.
+#include "common.h"
+#include "gemm_core.h"
+
+namespace optima {
+namespace {
+
+enum GemmMode { kPlain = 0, kPlain2 = 1, kStore = 2, kFused = 3 };
+
+struct ProductArgs {
+  const float* A;      // rows of the multiplied vectors, pitch dp
+  const float* B;      // H, [dp][dp] (pitch dp)
+  const int* rows;     // active list (row r of the launch is column rows[r]); NULL = identity
+  int n_rows;
+  int dp;
+  int d;
+  float* out1;         // kPlain/kPlain2: destination; kStore: Hx
+  float* out2;         // kPlain2: second destination
+  float* HA;           // Hx_ag (kStore, kFused)
+  const float* HW0;    // kFused
+  const float* Xin;    // kFused: x of the current iteration (same as A)
+  float* Xout;         // kFused: x of the next iteration
+  float* XA;           // kFused: x_ag
+  const uint8_t* mask; // [n_cols][d]
+  const int* kbase;    // iterations since restart, per column, at the last check
+  int s;               // iterations since the last check before this product
+  const float* Lp;     // step constant L
+};
+
+struct RowCoef {
+  float alpha, alpha1, eta1;
+};
+
+template <int MODE>
+__device__ inline RowCoef row_coef(const ProductArgs& p, int j, float L) {
+  RowCoef c{0.f, 0.f, 0.f};
+  if (MODE == kFused || MODE == kStore) {
+    const float k = float(p.kbase[j] + p.s);
+    c.alpha = 2.f / (k + 2.f);
+    c.alpha1 = 2.f / (k + 3.f);
+    c.eta1 = (k + 2.f) / (2.f * L);
+  }
+  return c;
+}
+
+// Consumes y = (H x)[j][n] for column j.
+template <int MODE>
+__device__ inline void epilogue_elem(const ProductArgs& p, int j, int n, float y, const RowCoef& c) {
+  const size_t o = size_t(j) * p.dp + n;
+  if (MODE == kPlain) {
+    p.out1[o] = y;
+  } else if (MODE == kPlain2) {
+    p.out1[o] = y;
+    p.out2[o] = y;
+  } else if (MODE == kStore) {
+    p.HA[o] = (1.f - c.alpha) * p.HA[o] + c.alpha * y;
+    p.out1[o] = y;
+  } else {  // kFused: finish this iteration's products, run the next update
+    const float ha = (1.f - c.alpha) * p.HA[o] + c.alpha * y;
+    const float g = 2.f * ((1.f - c.alpha1) * ha + c.alpha1 * y - p.HW0[o]);
+    const bool keep = n < p.d && p.mask[size_t(j) * p.d + n] != 0;
+    const float xn = keep ? p.Xin[o] - c.eta1 * g : 0.f;
+    p.XA[o] = (1.f - c.alpha1) * p.XA[o] + c.alpha1 * xn;
+    p.HA[o] = ha;
+    p.Xout[o] = xn;
+  }
+}
+
+// The products of `splits` contiguous K ranges of one output tile; with
+// splits == 1 the tile is finished in place, otherwise each range writes its
+// partial sum to part[split][launch row][n] and k_split_epilogue adds them.
+template <int MODE>
+__global__ void __launch_bounds__(kThreads) k_product(ProductArgs p, int splits, float* part) {
+  __shared__ __attribute__((aligned(16))) char lds[kGemmLdsBytes];
+  const int tiles_m = (p.n_rows + kTile - 1) / kTile;
+  const int tiles_n = p.dp / kTile;
+  const int n_tiles = tiles_m * tiles_n;
+  const int lin = blockIdx.x % n_tiles;
+  const int sp = blockIdx.x / n_tiles;
+  int tm, tn;
+  tile_of_block(lin, n_tiles, tiles_m, tiles_n, &tm, &tn);
+  const int m0 = tm * kTile, n0 = tn * kTile;
+  const int stages = p.dp * 4 / kStageRowBytes;
+  const int s0 = int(int64_t(stages) * sp / splits);
+  const int s1 = int(int64_t(stages) * (sp + 1) / splits);
+
+  const char* a_src[4];
+  const char* b_src[4];
+  const int seg = threadIdx.x & 7, rq = threadIdx.x >> 3;
+  const size_t k_off = size_t(s0) * kStageRowBytes + seg * 16;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    int r = m0 + rq + 32 * i;
+    r = r < p.n_rows ? r : p.n_rows - 1;
+    const int j = p.rows ? p.rows[r] : r;
+    a_src[i] = reinterpret_cast<const char*>(p.A + size_t(j) * p.dp) + k_off;
+    b_src[i] = reinterpret_cast<const char*>(p.B + size_t(n0 + rq + 32 * i) * p.dp) + k_off;
+  }
+  f4 acc[4][4];
+  gemm_tile_mainloop<float>(acc, a_src, b_src, s1 - s0, lds);
+
+  if (splits > 1) {
+    float* P = part + size_t(sp) * size_t(tiles_m) * kTile * size_t(p.dp);
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = m0 + acc_row(mi, e);
+        if (r >= p.n_rows) continue;
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) P[size_t(r) * p.dp + n0 + acc_col(ni)] = acc[mi][ni][e];
+      }
+    return;
+  }
+  const float L = (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f;
+#pragma unroll
+  for (int mi = 0; mi < 4; ++mi) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = m0 + acc_row(mi, e);
+      if (r >= p.n_rows) continue;
+      const int j = p.rows ? p.rows[r] : r;
+      const RowCoef c = row_coef<MODE>(p, j, L);
+#pragma unroll
+      for (int ni = 0; ni < 4; ++ni) epilogue_elem<MODE>(p, j, n0 + acc_col(ni), acc[mi][ni][e], c);
+    }
+  }
+}
+
+// Sums the split partials in split order and applies the product epilogue.
+template <int MODE>
+__global__ void __launch_bounds__(kThreads) k_split_epilogue(ProductArgs p, int splits,
+                                                             const float* part) {
+  const int r = blockIdx.x;
+  if (r >= p.n_rows) return;
+  const int j = p.rows ? p.rows[r] : r;
+  const int tiles_m = (p.n_rows + kTile - 1) / kTile;
+  const size_t split_stride = size_t(tiles_m) * kTile * size_t(p.dp);
+  const RowCoef c = row_coef<MODE>(p, j, (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f);
+  for (int n = blockIdx.y * kThreads + threadIdx.x; n < p.dp; n += gridDim.y * kThreads) {
+    const float* q = part + size_t(r) * p.dp + n;
+    float y = q[0];
+    for (int sp = 1; sp < splits; ++sp) y += q[sp * split_stride];
+    epilogue_elem<MODE>(p, j, n, y, c);
+  }
+}
+
+// Iteration update from the stored products (first iteration after a check).
+__global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows, int dp, int d,
+                                                     const float* X, float* Xout, float* XA,
+                                                     const float* HX, const float* HA,
+                                                     const float* HW0, const uint8_t* mask,
+                                                     const int* kbase, const float* Lp) {
+  const int r = blockIdx.x;
+  if (r >= n_rows) return;
+  const int j = rows ? rows[r] : r;
+  const float k = float(kbase[j]);
+  const float alpha = 2.f / (k + 2.f);
+  const float eta = (k + 1.f) / (2.f * *Lp);
+  const size_t base = size_t(j) * dp;
+  for (int n = blockIdx.y * kThreads + threadIdx.x; n < dp; n += gridDim.y * kThreads) {
+    const size_t o = base + n;
+    const float g = 2.f * ((1.f - alpha) * HA[o] + alpha * HX[o] - HW0[o]);
+    const bool keep = n < d && mask[size_t(j) * d + n] != 0;
+    const float xn = keep ? X[o] - eta * g : 0.f;
+    XA[o] = (1.f - alpha) * XA[o] + alpha * xn;
+    Xout[o] = xn;
+  }
+}
+
+// Copies W0 into padded rows and forms the start point x = x_ag = sel(m, w0, 0).
+__global__ void __launch_bounds__(kThreads) k_prep(const float* W0, const uint8_t* mask, int n_cols,
+                                                   int d, int dp, float* W0P, float* X, float* XA,
+                                                   int* flags) {
+  const int j = blockIdx.x;
+  const size_t base = size_t(j) * dp;
+  bool bad = false;
+  for (int n = blockIdx.y * kThreads + threadIdx.x; n < dp; n += gridDim.y * kThreads) {
+    float w = 0.f;
+    bool keep = false;
+    if (n < d) {
+      w = W0[size_t(j) * d + n];
+      keep = mask[size_t(j) * d + n] != 0;
+      bad |= !isfinite(w);
+    }
+    W0P[base + n] = w;
+    const float x = keep ? w : 0.f;
+    X[base + n] = x;
+    XA[base + n] = x;
+  }
+  if (bad) atomicOr(flags, 1);
+}
+
+// Zero-padded copy of H (used when d is not a multiple of the tile) with a
+// finiteness scan; with hp == nullptr it only scans.
+__global__ void __launch_bounds__(kThreads) k_scan_pad_h(const float* H, int d, int dp, float* hp,
+                                                         int* flags) {
+  bool bad = false;
+  const size_t total = size_t(dp) * dp;
+  const size_t stride = size_t(gridDim.x) * kThreads;
+  for (size_t e = size_t(blockIdx.x) * kThreads + threadIdx.x; e < total; e += stride) {
+    const int i = int(e / dp), jj = int(e % dp);
+    float v = 0.f;
+    if (i < d && jj < d) {
+      v = H[size_t(i) * d + jj];
+      bad |= !isfinite(v);
+    }
+    if (hp) hp[e] = v;
+  }
+  if (bad) atomicOr(flags, 1);
+}
+
+__global__ void k_step_constant(const float* lambda_max, float step_safety, float* Lp, int* flags) {
+  const float lm = *lambda_max;
+  if (!(lm > 0.f) || !isfinite(lm)) {
+    atomicOr(flags, 2);
+    *Lp = 1.f;
+    return;
+  }
+  *Lp = float(2.0 * double(lm) * (1.0 + double(step_safety)));
+}
+
+struct ColState {
+  int* kbase;         // iterations since restart as of the last check
+  int* restarts;
+  int* done;
+  double* kkt_restart;
+  double* kkt_prev;
+  double* f_anchor;
+  double* c_norm;     // ||2 H w0||_2
+  double* w0hw0;      // w0^T H w0
+};
+
+struct CheckArgs {
+  const int* rows;
+  int n_rows;
+  int dp, d;
+  float* X;            // current x
+  float* XA;
+  float* HX;
+  float* HA;
+  const float* HW0;
+  const float* W0;     // [n_cols][d]
+  const uint8_t* mask;
+  ColState st;
+  int n_block;         // iterations run since the last check
+  int64_t t;           // total iterations run
+  int initial;         // first check at the start point
+  int final_check;     // t == max_iters
+  optima_solver_opts o;
+  float* W_out;
+  optima_solve_stats stats;
+};
+
+// One workgroup per active column: scores x and x_ag, picks the candidate,
+// then terminates the column or applies an accepted restart.
+__global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
+  __shared__ double red[kThreads / 64];
+  __shared__ int decision;  // bit 0: terminate, bit 1: restart, bit 2: candidate is x
+  const int r = blockIdx.x;
+  if (r >= a.n_rows) return;
+  const int j = a.rows ? a.rows[r] : r;
+  const size_t base = size_t(j) * a.dp;
+
+  double rdx = 0, gpx = 0, fx = 0, qx = 0, rda = 0, gpa = 0, fa = 0, qa = 0, cn = 0, wq = 0;
+  for (int n = threadIdx.x; n < a.d; n += kThreads) {
+    const size_t o = base + n;
+    const double hw = a.HW0[o];
+    const double w0 = a.W0[size_t(j) * a.d + n];
+    const bool keep = a.mask[size_t(j) * a.d + n] != 0;
+    const double x = a.X[o], hx = a.HX[o];
+    const double gx = 2.0 * (hx - hw);
+    rdx += keep ? gx * gx : 0.0;
+    gpx += x * gx;
+    fx += (x - w0) * (hx - hw);
+    qx += x * hx;
+    if (a.initial) {
+      cn += 4.0 * hw * hw;
+      wq += w0 * hw;
+    } else {
+      const double xa = a.XA[o], ha = a.HA[o];
+      const double ga = 2.0 * (ha - hw);
+      rda += keep ? ga * ga : 0.0;
+      gpa += xa * ga;
+      fa += (xa - w0) * (ha - hw);
+      qa += xa * ha;
+    }
+  }
+  rdx = block_sum(rdx, red);
+  gpx = block_sum(gpx, red);
+  fx = block_sum(fx, red);
+  qx = block_sum(qx, red);
+  if (a.initial) {
+    cn = block_sum(cn, red);
+    wq = block_sum(wq, red);
+  } else {
+    rda = block_sum(rda, red);
+    gpa = block_sum(gpa, red);
+    fa = block_sum(fa, red);
+    qa = block_sum(qa, red);
+  }
+
+  if (threadIdx.x == 0) {
+    const optima_solver_opts& o = a.o;
+    const ColState& st = a.st;
+    double c_norm, w0hw0;
+    if (a.initial) {
+      c_norm = sqrt(cn);
+      w0hw0 = wq;
+      st.c_norm[j] = c_norm;
+      st.w0hw0[j] = w0hw0;
+    } else {
+      c_norm = st.c_norm[j];
+      w0hw0 = st.w0hw0[j];
+    }
+    const double rd_x = sqrt(rdx), gap_x = fabs(gpx), kkt_x = sqrt(rd_x * rd_x + gap_x * gap_x);
+    double rd_c = rd_x, gap_c = gap_x, kkt_c = kkt_x, f_c = fx, q_c = qx;
+    bool cand_x = true;
+    if (!a.initial) {
+      const double rd_a = sqrt(rda), gap_a = fabs(gpa), kkt_a = sqrt(rd_a * rd_a + gap_a * gap_a);
+      cand_x = kkt_x < kkt_a;  // ties go to the average
+      if (!cand_x) {
+        rd_c = rd_a;
+        gap_c = gap_a;
+        kkt_c = kkt_a;
+        f_c = fa;
+        q_c = qa;
+      }
+    }
+    const double P = f_c, D = -q_c + w0hw0;
+    const bool conv = rd_c <= double(o.eps_abs) + double(o.eps_rel) * c_norm &&
+                      gap_c <= double(o.eps_abs) + double(o.eps_rel) * (fabs(P) + fabs(D));
+    int dec = cand_x ? 4 : 0;
+    if (a.initial) {
+      if (a.stats.f_initial) a.stats.f_initial[j] = float(fx);
+      st.kkt_restart[j] = kkt_x;
+      st.kkt_prev[j] = kkt_x;
+      st.f_anchor[j] = fx;
+      st.kbase[j] = 0;
+      st.restarts[j] = 0;
+      if ((conv && !o.fixed_iters) || a.final_check) dec |= 1;
+    } else {
+      const bool stop = (conv && !o.fixed_iters) || a.final_check;
+      if (stop) {
+        dec |= 1;
+      } else {
+        const double k = double(st.kbase[j] + a.n_block);
+        const bool cond = kkt_c <= double(o.beta_sufficient) * st.kkt_restart[j] ||
+                          (kkt_c <= double(o.beta_necessary) * st.kkt_restart[j] &&
+                           kkt_c > st.kkt_prev[j]) ||
+                          k >= double(o.beta_artificial) * double(a.t);
+        if (o.restarts && cond && f_c <= st.f_anchor[j]) {
+          dec |= 2;
+          st.kbase[j] = 0;
+          st.kkt_restart[j] = kkt_c;
+          st.f_anchor[j] = f_c;
+          st.restarts[j] += 1;
+        } else {
+          st.kbase[j] = int(k);
+        }
+        st.kkt_prev[j] = kkt_c;
+      }
+    }
+    if (dec & 1) {
+      st.done[j] = 1;
+      if (a.stats.iters) a.stats.iters[j] = int(a.t);
+      if (a.stats.restarts) a.stats.restarts[j] = st.restarts[j];
+      if (a.stats.converged) a.stats.converged[j] = conv ? 1 : 0;
+      if (a.stats.f_final) a.stats.f_final[j] = float(f_c);
+      if (a.stats.kkt_final) a.stats.kkt_final[j] = float(kkt_c);
+    }
+    decision = dec;
+  }
+  __syncthreads();
+  const int dec = decision;
+  if (dec & 1) {
+    const float* src = (dec & 4) ? a.X : a.XA;
+    for (int n = threadIdx.x; n < a.d; n += kThreads) a.W_out[size_t(j) * a.d + n] = src[base + n];
+  } else if (dec & 2) {
+    float* xd = (dec & 4) ? a.XA : a.X;
+    float* hd = (dec & 4) ? a.HA : a.HX;
+    const float* xs = (dec & 4) ? a.X : a.XA;
+    const float* hs = (dec & 4) ? a.HX : a.HA;
+    for (int n = threadIdx.x; n < a.dp; n += kThreads) {
+      xd[base + n] = xs[base + n];
+      hd[base + n] = hs[base + n];
+    }
+  }
+}
+
+// Stable compaction of the active list: keeps the columns not yet done.
+__global__ void __launch_bounds__(1024) k_compact(const int* rows_in, int n_in, const int* done,
+                                                  int* rows_out, int* n_out) {
+  __shared__ int scan[1024];
+  __shared__ int carry;
+  if (threadIdx.x == 0) carry = 0;
+  __syncthreads();
+  for (int b = 0; b < n_in; b += 1024) {
+    const int r = b + threadIdx.x;
+    int j = 0, keep = 0;
+    if (r < n_in) {
+      j = rows_in ? rows_in[r] : r;
+      keep = done[j] ? 0 : 1;
+    }
+    scan[threadIdx.x] = keep;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+      const int v = threadIdx.x >= o ? scan[threadIdx.x - o] : 0;
+      __syncthreads();
+      scan[threadIdx.x] += v;
+      __syncthreads();
+    }
+    if (keep) rows_out[carry + scan[threadIdx.x] - 1] = j;
+    __syncthreads();
+    if (threadIdx.x == 1023) carry += scan[1023];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *n_out = carry;
+}
+
+// Split-K limits: at most kMaxSplits ranges, and at most kMaxSplitTiles
+// (tile, range) pairs, which bounds the partial-sum buffer to 128 MiB.
+constexpr int kMaxSplits = 16;
+constexpr int kMaxSplitTiles = 2048;
+
+struct Layout {
+  int64_t dp;
+  bool pad_h;
+  size_t part_elems;
+  float* part;
+  float *X0, *X1, *XA, *HX, *HA, *HW0, *Hp, *L;
+  int *rows0, *rows1, *n_active, *flags;
+  ColState st;
+};
+
+Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
+  Layout l{};
+  l.dp = round_up(d, kTile);
+  l.pad_h = (d % kTile) != 0;
+  Carver c(ws);
+  const size_t vec = size_t(n_cols) * size_t(l.dp);
+  l.X0 = c.take<float>(vec);
+  l.X1 = c.take<float>(vec);
+  l.XA = c.take<float>(vec);
+  l.HX = c.take<float>(vec);
+  l.HA = c.take<float>(vec);
+  l.HW0 = c.take<float>(vec);
+  l.Hp = l.pad_h ? c.take<float>(size_t(l.dp) * size_t(l.dp)) : nullptr;
+  l.part_elems = std::min<size_t>(size_t(kMaxSplitTiles) * kTile * kTile,
+                                  size_t(kMaxSplits) * size_t(round_up(n_cols, kTile)) * size_t(l.dp));
+  l.part = c.take<float>(l.part_elems);
+  l.rows0 = c.take<int>(n_cols);
+  l.rows1 = c.take<int>(n_cols);
+  l.st.kbase = c.take<int>(n_cols);
+  l.st.restarts = c.take<int>(n_cols);
+  l.st.done = c.take<int>(n_cols);
+  l.st.kkt_restart = c.take<double>(n_cols);
+  l.st.kkt_prev = c.take<double>(n_cols);
+  l.st.f_anchor = c.take<double>(n_cols);
+  l.st.c_norm = c.take<double>(n_cols);
+  l.st.w0hw0 = c.take<double>(n_cols);
+  l.n_active = c.take<int>(4);
+  l.flags = c.take<int>(4);
+  l.L = c.take<float>(4);
+  if (bytes) *bytes = c.bytes();
+  return l;
+}
+
+int device_cu_count() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cache[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+// Number of K ranges for a product over `tiles` output tiles: splitting pays
+// when the tiles leave CUs idle or unevenly loaded. The model counts the
+// workgroups the busiest CU runs (relative to its share of the total work),
+// rates a CU with a single workgroup at 60% (one wave per SIMD cannot hide
+// the stage barriers), and charges 3% per extra range for the partial sums.
+int choose_splits(int tiles, int stages, int tiles_m, int dp, size_t part_cap) {
+  const int n_cu = device_cu_count();
+  if (tiles >= 4 * n_cu) return 1;
+  auto cost = [&](int S) {
+    const int per_cu = int(ceil_div(int64_t(tiles) * S, n_cu));
+    const double eff = per_cu >= 2 ? 1.0 : 0.6;
+    return double(per_cu) / S / eff * (1.0 + 0.03 * (S - 1));
+  };
+  int best = 1;
+  double best_cost = cost(1);
+  for (int S = 2; S <= kMaxSplits && S <= stages; ++S) {
+    if (int64_t(tiles) * S > kMaxSplitTiles) break;
+    if (size_t(S) * size_t(tiles_m) * kTile * size_t(dp) > part_cap) break;
+    const double c = cost(S);
+    if (c < best_cost - 1e-9) {
+      best = S;
+      best_cost = c;
+    }
+  }
+  return best;
+}
+
+template <int MODE>
+optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t s) {
+  const int tiles_m = int(ceil_div(p.n_rows, kTile));
+  const int tiles_n = p.dp / kTile;
+  const int stages = p.dp * 4 / kStageRowBytes;
+  const int S = choose_splits(tiles_m * tiles_n, stages, tiles_m, p.dp, l.part_elems);
+  hipLaunchKernelGGL(k_product<MODE>, dim3(tiles_m * tiles_n * S), dim3(kThreads), 0, s, p, S,
+                     l.part);
+  OPTIMA_LAUNCH_CHECK();
+  if (S > 1) {
+    const dim3 g(unsigned(p.n_rows), unsigned(ceil_div(p.dp, 4 * kThreads)));
+    hipLaunchKernelGGL(k_split_epilogue<MODE>, g, dim3(kThreads), 0, s, p, S,
+                       static_cast<const float*>(l.part));
+    OPTIMA_LAUNCH_CHECK();
+  }
+  return OPTIMA_OK;
+}
+
+}  // namespace
+
+size_t qp_workspace_bytes(int64_t d, int64_t n_cols) {
+  size_t b = 0;
+  carve(nullptr, d, n_cols, &b);
+  return b;
+}
+
+optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const float* W0,
+                       const uint8_t* mask, int64_t n_cols, const optima_solver_opts& o,
+                       void* ws, float* W_out, const optima_solve_stats& stats,
+                       optima_solve_info* info, hipStream_t s) {
+  size_t need = 0;
+  Layout l = carve(ws, d, n_cols, &need);
+  const int dp = int(l.dp), di = int(d), nc = int(n_cols);
+  optima_solve_info inf{};
+
+  OPTIMA_HIP_TRY(hipMemsetAsync(l.flags, 0, 4 * sizeof(int), s));
+  OPTIMA_HIP_TRY(hipMemsetAsync(l.st.done, 0, size_t(nc) * sizeof(int), s));
+  const float* Hm = H;
+  {
+    const int blocks = int(std::min<int64_t>(4096, ceil_div(int64_t(dp) * dp, kThreads)));
+    hipLaunchKernelGGL(k_scan_pad_h, dim3(blocks), dim3(kThreads), 0, s, H, di, dp, l.Hp, l.flags);
+    OPTIMA_LAUNCH_CHECK();
+    if (l.pad_h) Hm = l.Hp;
+  }
+  hipLaunchKernelGGL(k_step_constant, dim3(1), dim3(1), 0, s, lambda_max, o.step_safety, l.L, l.flags);
+  OPTIMA_LAUNCH_CHECK();
+  const dim3 vec_grid(unsigned(nc), unsigned(ceil_div(dp, 4 * kThreads)));
+  // W0 padded copy goes to HX first; Hw0 = H w0, then Hx = Hx_ag = H x0.
+  hipLaunchKernelGGL(k_prep, vec_grid, dim3(kThreads), 0, s, W0, mask, nc, di, dp, l.HX, l.X0,
+                     l.XA, l.flags);
+  OPTIMA_LAUNCH_CHECK();
+  int flags = 0;
+  OPTIMA_HIP_TRY(hipMemcpyAsync(&flags, l.flags, sizeof(int), hipMemcpyDeviceToHost, s));
+  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  if (flags) return OPTIMA_E_NONFINITE;
+
+  ProductArgs p{};
+  p.B = Hm;
+  p.dp = dp;
+  p.d = di;
+  p.mask = mask;
+  p.kbase = l.st.kbase;
+  p.Lp = l.L;
+  p.rows = nullptr;
+  p.n_rows = nc;
+  p.A = l.HX;
+  p.out1 = l.HW0;
+  if (auto e = launch_product<kPlain>(p, l, s)) return e;
+  p.A = l.X0;
+  p.out1 = l.HX;
+  p.out2 = l.HA;
+  if (auto e = launch_product<kPlain2>(p, l, s)) return e;
+  inf.gemm_calls += 2;
+  inf.row_products += 2 * int64_t(nc);
+
+  CheckArgs ca{};
+  ca.dp = dp;
+  ca.d = di;
+  ca.XA = l.XA;
+  ca.HX = l.HX;
+  ca.HA = l.HA;
+  ca.HW0 = l.HW0;
+  ca.W0 = W0;
+  ca.mask = mask;
+  ca.st = l.st;
+  ca.o = o;
+  ca.W_out = W_out;
+  ca.stats = stats;
+
+  // Initial check at the start point.
+  ca.rows = nullptr;
+  ca.n_rows = nc;
+  ca.X = l.X0;
+  ca.initial = 1;
+  ca.final_check = o.max_iters == 0;
+  ca.t = 0;
+  ca.n_block = 0;
+  hipLaunchKernelGGL(k_check, dim3(nc), dim3(kThreads), 0, s, ca);
+  OPTIMA_LAUNCH_CHECK();
+  inf.checks += 1;
+  hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, (const int*)nullptr, nc, l.st.done,
+                     l.rows0, l.n_active);
+  OPTIMA_LAUNCH_CHECK();
+  int n_act = 0;
+  OPTIMA_HIP_TRY(hipMemcpyAsync(&n_act, l.n_active, sizeof(int), hipMemcpyDeviceToHost, s));
+  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+
+  // Optional timing of the iteration loop's product launches.
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  if (info) {
+    OPTIMA_HIP_TRY(hipEventCreate(&ev[0]));
+    if (hipEventCreate(&ev[1]) != hipSuccess) {
+      (void)hipEventDestroy(ev[0]);
+      return OPTIMA_E_HIP;
+    }
+  }
+  struct EventGuard {
+    hipEvent_t* e;
+    ~EventGuard() {
+      if (e[0]) (void)hipEventDestroy(e[0]);
+      if (e[1]) (void)hipEventDestroy(e[1]);
+    }
+  } guard{ev};
+
+  int* rows = l.rows0;
+  int* rows_next = l.rows1;
+  float* xbuf[2] = {l.X0, l.X1};
+  int cur = 0;
+  int64_t t = 0;
+  const int64_t ce = o.check_every;
+  while (t < o.max_iters && n_act > 0) {
+    const int64_t t_next = std::min<int64_t>((t / ce + 1) * ce, o.max_iters);
+    const int n = int(t_next - t);
+    const dim3 ug(unsigned(n_act), unsigned(ceil_div(dp, 4 * kThreads)));
+    hipLaunchKernelGGL(k_update, ug, dim3(kThreads), 0, s, rows, n_act, dp, di, xbuf[cur],
+                       xbuf[cur ^ 1], l.XA, l.HX, l.HA, l.HW0, mask, l.st.kbase, l.L);
+    OPTIMA_LAUNCH_CHECK();
+    cur ^= 1;
+    p.rows = rows;
+    p.n_rows = n_act;
+    p.HA = l.HA;
+    p.HW0 = l.HW0;
+    p.XA = l.XA;
+    if (info) OPTIMA_HIP_TRY(hipEventRecord(ev[0], s));
+    for (int i = 0; i + 1 < n; ++i) {
+      p.A = xbuf[cur];
+      p.Xin = xbuf[cur];
+      p.Xout = xbuf[cur ^ 1];
+      p.s = i;
+      if (auto e = launch_product<kFused>(p, l, s)) return e;
+      cur ^= 1;
+    }
+    p.A = xbuf[cur];
+    p.out1 = l.HX;
+    p.s = n - 1;
+    if (auto e = launch_product<kStore>(p, l, s)) return e;
+    if (info) OPTIMA_HIP_TRY(hipEventRecord(ev[1], s));
+    inf.gemm_calls += n;
+    inf.row_products += int64_t(n) * n_act;
+    inf.timed_launches += n;
+    inf.timed_row_products += int64_t(n) * n_act;
+    t = t_next;
+
+    ca.rows = rows;
+    ca.n_rows = n_act;
+    ca.X = xbuf[cur];
+    ca.initial = 0;
+    ca.final_check = t == o.max_iters;
+    ca.t = t;
+    ca.n_block = n;
+    hipLaunchKernelGGL(k_check, dim3(n_act), dim3(kThreads), 0, s, ca);
+    OPTIMA_LAUNCH_CHECK();
+    inf.checks += 1;
+    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, rows, n_act, l.st.done, rows_next,
+                       l.n_active);
+    OPTIMA_LAUNCH_CHECK();
+    std::swap(rows, rows_next);
+    OPTIMA_HIP_TRY(hipMemcpyAsync(&n_act, l.n_active, sizeof(int), hipMemcpyDeviceToHost, s));
+    OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+    if (info) {
+      float ms = 0.f;
+      OPTIMA_HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));
+      inf.timed_product_ms += ms;
+    }
+  }
+  inf.iterations = t;
+  if (info) *info = inf;
+  return OPTIMA_OK;
+}
+
+}  // namespace optima

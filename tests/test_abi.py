@@ -1,0 +1,84 @@
+"""Host-side checks of liboptima.so: it loads, exports every function that
+include/optima.h declares, and its host-only paths (status strings, defaults,
+workspace queries, argument validation that returns before any launch)
+behave as the header states. No kernel is launched here."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "optima.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(optima_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2512_13886_amd as L
+    return ctypes.CDLL(L.library_path())
+
+
+def test_header_declares_the_four_calls():
+    names = _declared_functions()
+    for n in ("optima_hessian_accumulate", "optima_hessian_damp", "optima_spectral_norm",
+              "optima_qp_solve_batched"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    missing = [n for n in _declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings_and_version():
+    import paper_2512_13886_amd as L
+    assert L.optima_abi_version() >= 1
+    assert "INVAL" in L.optima_status_string(-1)
+    assert "NONFINITE" in L.optima_status_string(-3)
+    assert "WORKSPACE" in L.optima_status_string(-4)
+    assert "unknown" in L.optima_status_string(42)
+
+
+def test_default_options_follow_table_8():
+    import paper_2512_13886_amd as L
+    o = L.SolverOpts.default()
+    assert o.max_iters == 100000 and o.check_every == 64
+    assert o.eps_rel == pytest.approx(0.01) and o.eps_abs == pytest.approx(0.01)
+    assert o.restarts == 1 and o.fixed_iters == 0
+
+
+def test_workspace_queries():
+    import paper_2512_13886_amd as L
+    a = L.optima_qp_workspace_bytes(4096, 4096)
+    assert a >= 6 * 4096 * 4096 * 4
+    assert L.optima_qp_workspace_bytes(4096, 2048) < a
+    assert L.optima_qp_workspace_bytes(100, 3) >= 128 * 128 * 4  # padded copy of H
+    assert L.optima_qp_workspace_bytes(0, 3) == 0
+    h = L.optima_hessian_workspace_bytes(262144, 4096, L.DTYPE_BF16)
+    assert h >= 4096 * 65536 * 2
+    assert L.optima_hessian_workspace_bytes(10, 4096, 7) == 0
+    assert L.optima_spectral_norm_workspace_bytes(4096) >= 2 * 4096 * 4
+
+
+def test_validation_returns_before_launch(lib):
+    i64, vp = ctypes.c_int64, ctypes.c_void_p
+    f = lib.optima_hessian_accumulate
+    f.restype = ctypes.c_int
+    f.argtypes = [vp, ctypes.c_int, i64, i64, vp, ctypes.c_int, vp, ctypes.c_size_t, vp]
+    assert f(None, 0, 10, 8, None, 0, None, 0, None) == -1          # H is NULL
+    assert f(None, 9, 10, 8, vp(256), 0, None, 0, None) == -5       # dtype
+    assert f(vp(512), 0, 10, 8, vp(1 << 20), 0, None, 0, None) == -4  # no workspace
+    q = lib.optima_qp_solve_batched
+    q.restype = ctypes.c_int
+    q.argtypes = [vp, i64, vp, vp, vp, i64, vp, vp, ctypes.c_size_t, vp, vp, vp, vp]
+    assert q(None, 8, None, None, None, 4, None, None, 0, None, None, None, None) == -1
+    g = lib.optima_spectral_norm
+    g.restype = ctypes.c_int
+    g.argtypes = [vp, i64, vp, ctypes.c_int, ctypes.c_float, vp, ctypes.c_size_t, vp, vp, vp]
+    assert g(vp(256), 8, vp(512), 0, 1e-6, None, 0, vp(1024), None, None) == -1  # max_iters
