@@ -6,12 +6,20 @@
 //
 // Work split: 256 threads = 4 waves in a 2x2 grid, each wave owning a 64x64
 // sub-tile as 4x4 blocks of 16x16 MFMA outputs (16 accumulators of 4 floats).
-// K advances in stages of 128 bytes per row (32 fp32 or 64 bf16 values):
-// every thread fetches 4 A and 4 B 16-byte vectors of the next stage into
-// registers while the waves run the MFMAs of the current stage out of LDS;
-// two LDS stage buffers need one barrier per stage. LDS rows are padded by 16
-// bytes so that the 16-byte fragment reads of 16 consecutive rows fall in
-// distinct banks.
+// K advances in stages of 128 bytes per row (32 fp32 or 64 bf16 values).
+//
+// Operands move HBM/L2 -> LDS with gfx950's direct loads
+// (global_load_lds_dwordx4): no registers are spent on prefetch and the loads
+// of stage s + 1 are issued right after the barrier that frees their buffer,
+// ahead of the LDS reads and MFMAs of stage s (enforced with scheduling
+// groups). One wave's direct load writes 1 KiB of LDS contiguously (lane l at
+// byte 16 l), i.e. 8 tile rows of 128 bytes; to keep the fragment reads free
+// of bank conflicts without padding, the 16-byte segment g of tile row r is
+// stored at physical segment g ^ (r & 7), and each lane fetches from global
+// memory the logical segment that belongs at its physical slot. The two stage
+// buffers are distinct LDS arrays and the stage loop is unrolled by two, so
+// that no LDS read shares an object with an in-flight direct load and the
+// compiler adds no wait for it.
 //
 // Fragment layout (v_mfma_f32_16x16x4_f32 and v_mfma_f32_16x16x32_bf16): lane
 // l supplies row (l % 16) of a 16-row block and the K group (l / 16). One
@@ -28,9 +36,7 @@
 namespace optima {
 
 constexpr int kStageRowBytes = 128;
-constexpr int kLdsRowBytes = kStageRowBytes + 16;
-constexpr int kStageBytes = 2 * kTile * kLdsRowBytes;  // A and B tiles
-constexpr int kGemmLdsBytes = 2 * kStageBytes;         // double buffered
+constexpr int kStageBufBytes = 2 * kTile * kStageRowBytes;  // A and B tiles, 32 KiB
 
 template <typename T>
 struct MfmaOp;
@@ -71,82 +77,111 @@ struct MfmaOp<Bf16Tag> {
   }
 };
 
-// a_src[i] / b_src[i]: byte address of this thread's 16-byte vector in load
-// row (threadIdx.x / 8 + 32 i) at the first stage; stage s adds
-// s * kStageRowBytes. All addresses must be 16-byte aligned. The prefetch
-// of stage s + 1 is unconditional (the last stage re-reads itself) so that
-// the prefetch registers never leave the register file.
+// Rows of the tile that this thread's direct loads fetch: round i (0..3)
+// covers tile row load_row(i); the byte offset of the fetched 16-byte segment
+// within the row's 128-byte stage is load_seg_bytes().
+__device__ inline int load_row(int i) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  return (i * 4 + wave) * 8 + (lane >> 3);
+}
+__device__ inline int load_seg_bytes() {
+  const int lane = threadIdx.x & 63;
+  return ((lane & 7) ^ (lane >> 3)) * 16;
+}
+
+template <typename T>
+struct StageShape;
+template <>
+struct StageShape<float> {
+  static constexpr int kMfmaPerChunk = 64;
+};
+template <>
+struct StageShape<Bf16Tag> {
+  static constexpr int kMfmaPerChunk = 16;
+};
+
+__device__ inline void issue_stage(const char* const (&a_src)[4], const char* const (&b_src)[4],
+                                   int s, char* buf) {
+  const size_t o = size_t(s) * kStageRowBytes;
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    char* d = buf + (i * 4 + wave) * 1024;
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(a_src[i] + o),
+        (__attribute__((address_space(3))) void*)d, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(b_src[i] + o),
+        (__attribute__((address_space(3))) void*)(d + kTile * kStageRowBytes), 16, 0, 0);
+  }
+}
+
+template <typename T>
+__device__ inline void compute_stage(f4 (&acc)[4][4], const char* buf) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1, g = lane >> 4;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    uint4 a[4], b[4];
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi) {
+      const int r = wm * 64 + mi * 16 + (lane & 15);
+      a[mi] = *reinterpret_cast<const uint4*>(buf + r * kStageRowBytes + (((4 * c + g) ^ (r & 7)) * 16));
+    }
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) {
+      const int r = wn * 64 + ni * 16 + (lane & 15);
+      b[ni] = *reinterpret_cast<const uint4*>(buf + kTile * kStageRowBytes + r * kStageRowBytes +
+                                             (((4 * c + g) ^ (r & 7)) * 16));
+    }
+    MfmaOp<T>::run(acc, a, b);
+  }
+  // Order within the stage: the 8 direct loads issued just before, then per
+  // chunk its 8 LDS reads and its MFMAs.
+  __builtin_amdgcn_sched_group_barrier(0x020, 8, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, StageShape<T>::kMfmaPerChunk, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, StageShape<T>::kMfmaPerChunk, 0);
+}
+
+// s_waitcnt vmcnt(0), leaving expcnt and lgkmcnt unwaited.
+__device__ inline void wait_direct_loads() { __builtin_amdgcn_s_waitcnt(0xF70); }
+
+// a_src[i] / b_src[i]: address of the 16-byte segment this thread fetches in
+// tile row load_row(i) at the first stage (row start + load_seg_bytes());
+// stage s adds s * kStageRowBytes. All addresses must be 16-byte aligned.
 template <typename T>
 __device__ inline void gemm_tile_mainloop(f4 (&acc)[4][4], const char* const (&a_src)[4],
-                                          const char* const (&b_src)[4], int n_stages,
-                                          char* lds) {
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int seg = tid & 7, rq = tid >> 3;
-
+                                          const char* const (&b_src)[4], int n_stages) {
+  __shared__ __attribute__((aligned(1024))) char lds0[kStageBufBytes];
+  __shared__ __attribute__((aligned(1024))) char lds1[kStageBufBytes];
 #pragma unroll
   for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
     for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f4{0.f, 0.f, 0.f, 0.f};
   if (n_stages <= 0) return;
 
-  const int st_off = rq * kLdsRowBytes + seg * 16;
-  const int frag_a = (wm * 64 + (lane & 15)) * kLdsRowBytes + (lane >> 4) * 16;
-  const int frag_b = kTile * kLdsRowBytes + (wn * 64 + (lane & 15)) * kLdsRowBytes + (lane >> 4) * 16;
-
-  uint4 ra0, ra1, ra2, ra3, rb0, rb1, rb2, rb3;
-#define OPTIMA_GLOAD(S)                                                        \
-  {                                                                            \
-    const size_t o_ = size_t(S) * kStageRowBytes;                              \
-    ra0 = *reinterpret_cast<const uint4*>(a_src[0] + o_);                      \
-    ra1 = *reinterpret_cast<const uint4*>(a_src[1] + o_);                      \
-    ra2 = *reinterpret_cast<const uint4*>(a_src[2] + o_);                      \
-    ra3 = *reinterpret_cast<const uint4*>(a_src[3] + o_);                      \
-    rb0 = *reinterpret_cast<const uint4*>(b_src[0] + o_);                      \
-    rb1 = *reinterpret_cast<const uint4*>(b_src[1] + o_);                      \
-    rb2 = *reinterpret_cast<const uint4*>(b_src[2] + o_);                      \
-    rb3 = *reinterpret_cast<const uint4*>(b_src[3] + o_);                      \
-  }
-#define OPTIMA_LSTORE(BUF)                                                     \
-  {                                                                            \
-    char* As_ = lds + (BUF) * kStageBytes + st_off;                            \
-    char* Bs_ = As_ + kTile * kLdsRowBytes;                                    \
-    *reinterpret_cast<uint4*>(As_ + 0 * 32 * kLdsRowBytes) = ra0;              \
-    *reinterpret_cast<uint4*>(As_ + 1 * 32 * kLdsRowBytes) = ra1;              \
-    *reinterpret_cast<uint4*>(As_ + 2 * 32 * kLdsRowBytes) = ra2;              \
-    *reinterpret_cast<uint4*>(As_ + 3 * 32 * kLdsRowBytes) = ra3;              \
-    *reinterpret_cast<uint4*>(Bs_ + 0 * 32 * kLdsRowBytes) = rb0;              \
-    *reinterpret_cast<uint4*>(Bs_ + 1 * 32 * kLdsRowBytes) = rb1;              \
-    *reinterpret_cast<uint4*>(Bs_ + 2 * 32 * kLdsRowBytes) = rb2;              \
-    *reinterpret_cast<uint4*>(Bs_ + 3 * 32 * kLdsRowBytes) = rb3;              \
-  }
-
-  OPTIMA_GLOAD(0);
-  OPTIMA_LSTORE(0);
-  __syncthreads();
-
-  for (int s = 0; s < n_stages; ++s) {
-    const int sn = s + 1 < n_stages ? s + 1 : s;
-    OPTIMA_GLOAD(sn);
-    const char* base = lds + (s & 1) * kStageBytes;
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      uint4 a[4], b[4];
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-        a[mi] = *reinterpret_cast<const uint4*>(base + frag_a + mi * 16 * kLdsRowBytes + c * 64);
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni)
-        b[ni] = *reinterpret_cast<const uint4*>(base + frag_b + ni * 16 * kLdsRowBytes + c * 64);
-      MfmaOp<T>::run(acc, a, b);
-    }
-    if (s + 1 < n_stages) OPTIMA_LSTORE((s + 1) & 1);
+  issue_stage(a_src, b_src, 0, lds0);
+  int s = 0;
+  for (; s + 1 < n_stages; s += 2) {
+    wait_direct_loads();
     __syncthreads();
+    issue_stage(a_src, b_src, s + 1, lds1);
+    compute_stage<T>(acc, lds0);
+    wait_direct_loads();
+    __syncthreads();
+    issue_stage(a_src, b_src, s + 2 < n_stages ? s + 2 : n_stages - 1, lds0);
+    compute_stage<T>(acc, lds1);
   }
-#undef OPTIMA_GLOAD
-#undef OPTIMA_LSTORE
+  if (s < n_stages) {  // odd count: the last stage is in lds0
+    wait_direct_loads();
+    __syncthreads();
+    compute_stage<T>(acc, lds0);
+  }
+  // No direct load may still be writing LDS when the workgroup moves on.
+  wait_direct_loads();
+  __syncthreads();
 }
 
 // Output coordinates of accumulator element (mi, ni, e) of this thread,

@@ -78,7 +78,6 @@ template <typename T>
 __global__ void __launch_bounds__(kThreads) k_syrk(const char* XT, int64_t pitch_bytes,
                                                    int stages, int splits, int64_t dp,
                                                    float* part, int first) {
-  __shared__ __attribute__((aligned(16))) char lds[kGemmLdsBytes];
   const int tile = blockIdx.x / splits;
   const int sp = blockIdx.x - tile * splits;
   int ti, tj;
@@ -87,15 +86,15 @@ __global__ void __launch_bounds__(kThreads) k_syrk(const char* XT, int64_t pitch
   const int s1 = int(int64_t(stages) * (sp + 1) / splits);
   const char* a_src[4];
   const char* b_src[4];
-  const int seg = threadIdx.x & 7, rq = threadIdx.x >> 3;
+  const int64_t k_off = int64_t(s0) * kStageRowBytes + load_seg_bytes();
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int64_t r = rq + 32 * i;
-    a_src[i] = XT + (int64_t(ti) * kTile + r) * pitch_bytes + int64_t(s0) * kStageRowBytes + seg * 16;
-    b_src[i] = XT + (int64_t(tj) * kTile + r) * pitch_bytes + int64_t(s0) * kStageRowBytes + seg * 16;
+    const int64_t r = load_row(i);
+    a_src[i] = XT + (int64_t(ti) * kTile + r) * pitch_bytes + k_off;
+    b_src[i] = XT + (int64_t(tj) * kTile + r) * pitch_bytes + k_off;
   }
   f4 acc[4][4];
-  gemm_tile_mainloop<T>(acc, a_src, b_src, s1 - s0, lds);
+  gemm_tile_mainloop<T>(acc, a_src, b_src, s1 - s0);
   float* P = part + size_t(sp) * size_t(dp) * size_t(dp);
 #pragma unroll
   for (int mi = 0; mi < 4; ++mi)

@@ -86,7 +86,6 @@ __device__ inline void epilogue_elem(const ProductArgs& p, int j, int n, float y
 // partial sum to part[split][launch row][n] and k_split_epilogue adds them.
 template <int MODE>
 __global__ void __launch_bounds__(kThreads) k_product(ProductArgs p, int splits, float* part) {
-  __shared__ __attribute__((aligned(16))) char lds[kGemmLdsBytes];
   const int tiles_m = (p.n_rows + kTile - 1) / kTile;
   const int tiles_n = p.dp / kTile;
   const int n_tiles = tiles_m * tiles_n;
@@ -101,18 +100,17 @@ __global__ void __launch_bounds__(kThreads) k_product(ProductArgs p, int splits,
 
   const char* a_src[4];
   const char* b_src[4];
-  const int seg = threadIdx.x & 7, rq = threadIdx.x >> 3;
-  const size_t k_off = size_t(s0) * kStageRowBytes + seg * 16;
+  const size_t k_off = size_t(s0) * kStageRowBytes + load_seg_bytes();
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    int r = m0 + rq + 32 * i;
+    int r = m0 + load_row(i);
     r = r < p.n_rows ? r : p.n_rows - 1;
     const int j = p.rows ? p.rows[r] : r;
     a_src[i] = reinterpret_cast<const char*>(p.A + size_t(j) * p.dp) + k_off;
-    b_src[i] = reinterpret_cast<const char*>(p.B + size_t(n0 + rq + 32 * i) * p.dp) + k_off;
+    b_src[i] = reinterpret_cast<const char*>(p.B + size_t(n0 + load_row(i)) * p.dp) + k_off;
   }
   f4 acc[4][4];
-  gemm_tile_mainloop<float>(acc, a_src, b_src, s1 - s0, lds);
+  gemm_tile_mainloop<float>(acc, a_src, b_src, s1 - s0);
 
   if (splits > 1) {
     float* P = part + size_t(sp) * size_t(tiles_m) * kTile * size_t(p.dp);
