@@ -97,6 +97,8 @@ def main() -> int:
     ap.add_argument("--cpu-sample-chunks", type=int, default=8)
     ap.add_argument("--fixed-iters", type=int, default=1000,
                     help="iterations of the full-batch leg that sets the roofline")
+    ap.add_argument("--precision", choices=["fp32", "bf16x3"], default="fp32",
+                    help="arithmetic of the per-iteration H-products")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="first run one 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -141,7 +143,9 @@ def main() -> int:
     qws = torch.empty(L.optima_qp_workspace_bytes(d, C), dtype=torch.uint8, device=dev)
     iters = torch.zeros(C, dtype=torch.int32, device=dev)
     conv = torch.zeros(C, dtype=torch.uint8, device=dev)
-    opts = L.SolverOpts.default()  # Table 8: tol 0.01 / 0.01, 100000 iterations
+    prec = {"fp32": L.PREC_FP32, "bf16x3": L.PREC_BF16X3}[args.precision]
+    # Table 8: tol 0.01 / 0.01, 100000 iterations
+    opts = L.SolverOpts.default(precision=prec)
     torch.cuda.synchronize()
 
     def step():
@@ -188,7 +192,7 @@ def main() -> int:
 
     # Full-batch leg: all 4096 columns for a fixed number of iterations. It
     # gives the iteration rate at B = C and the roofline of the H-product.
-    fixed = L.SolverOpts.default(max_iters=args.fixed_iters, fixed_iters=1)
+    fixed = L.SolverOpts.default(max_iters=args.fixed_iters, fixed_iters=1, precision=prec)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     finfo = L.optima_qp_solve_batched(H, lmax, W0d, Md, Wout, opts=fixed, ws=qws)

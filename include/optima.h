@@ -48,6 +48,16 @@ typedef int optima_status;
 #define OPTIMA_DTYPE_F32 0
 #define OPTIMA_DTYPE_BF16 1
 
+/* Arithmetic of the solver's per-iteration H-products (optima_solver_opts).
+ * FP32: v_mfma_f32_16x16x4_f32, fp32 products and sums.
+ * BF16X3: every fp32 operand v is split into bf16 planes hi = rne(v),
+ *   lo = rne(v - hi), and a*b is formed as hi*hi + hi*lo + lo*hi on
+ *   v_mfma_f32_16x16x32_bf16 with fp32 accumulation; the dropped terms are
+ *   below 3 * 2^-16 |a b| per product. The two setup products (H w0, H x0)
+ *   always use FP32. */
+#define OPTIMA_PREC_FP32 0
+#define OPTIMA_PREC_BF16X3 1
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* optima_status_string(optima_status status);
 
@@ -150,7 +160,7 @@ typedef struct {
   float beta_artificial;  /* default 0.36 */
   float step_safety;      /* default 1e-3 */
   int32_t restarts;       /* 0 disables restarts; default 1 */
-  int32_t reserved;       /* must be 0 */
+  int32_t precision;      /* OPTIMA_PREC_FP32 or OPTIMA_PREC_BF16X3 */
 } optima_solver_opts;
 
 typedef struct {

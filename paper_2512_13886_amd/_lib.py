@@ -23,6 +23,8 @@ OPTIMA_E_WORKSPACE = -4
 OPTIMA_E_UNSUPPORTED = -5
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
+PREC_FP32 = 0
+PREC_BF16X3 = 1
 
 
 class OptimaError(RuntimeError):
@@ -45,7 +47,7 @@ class _Opts(ctypes.Structure):
                 ("eps_abs", ctypes.c_float), ("beta_sufficient", ctypes.c_float),
                 ("beta_necessary", ctypes.c_float), ("beta_artificial", ctypes.c_float),
                 ("step_safety", ctypes.c_float), ("restarts", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("precision", ctypes.c_int32)]
 
 
 class _Stats(ctypes.Structure):
@@ -140,7 +142,7 @@ class SolverOpts:
     beta_artificial: float = 0.0
     step_safety: float = 0.0
     restarts: int = 0
-    reserved: int = 0
+    precision: int = 0
 
     @classmethod
     def default(cls, **overrides) -> "SolverOpts":

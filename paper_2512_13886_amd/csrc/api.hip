@@ -42,7 +42,7 @@ const char* optima_status_string(optima_status status) {
   }
 }
 
-int optima_abi_version(void) { return 1; }
+int optima_abi_version(void) { return 2; }
 
 size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
   if (n_tok < 0 || d < 1 || d > kMaxDim) return 0;
@@ -100,7 +100,7 @@ void optima_solver_opts_default(optima_solver_opts* o) {
   o->beta_artificial = 0.36f;
   o->step_safety = 1e-3f;
   o->restarts = 1;
-  o->reserved = 0;
+  o->precision = OPTIMA_PREC_FP32;
 }
 
 size_t optima_qp_workspace_bytes(int64_t d, int64_t n_cols) {
@@ -125,7 +125,9 @@ optima_status optima_qp_solve_batched(const float* H, int64_t d, const float* la
       overlaps(mask, size_t(n_cols) * d, W_out, wbytes))
     return OPTIMA_E_INVAL;
   const optima_solver_opts& o = *opts;
-  if (o.max_iters < 0 || o.check_every < 1 || o.reserved != 0) return OPTIMA_E_INVAL;
+  if (o.max_iters < 0 || o.check_every < 1) return OPTIMA_E_INVAL;
+  if (o.precision != OPTIMA_PREC_FP32 && o.precision != OPTIMA_PREC_BF16X3)
+    return OPTIMA_E_UNSUPPORTED;
   if (!(o.eps_rel >= 0.f) || !(o.eps_abs >= 0.f) || !(o.step_safety >= 0.f) ||
       !(o.beta_sufficient >= 0.f) || !(o.beta_necessary >= 0.f) || !(o.beta_artificial >= 0.f))
     return OPTIMA_E_INVAL;

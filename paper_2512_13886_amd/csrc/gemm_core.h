@@ -62,6 +62,29 @@ struct MfmaOp<float> {
 
 struct Bf16Tag {};
 
+// fp32 emulated by bf16 MFMAs: every value v is stored as two bf16 planes,
+// hi = rne(v) and lo = rne(v - hi), and a product a*b is formed as
+// a_hi b_hi + a_hi b_lo + a_lo b_hi (the dropped terms are below 2^-16 |a b|).
+struct Bf16x3Tag {};
+
+__device__ inline uint32_t bf16_rne_bits(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ inline float bf16_bits_value(uint32_t h) { return __uint_as_float(h << 16); }
+
+// Plane layout of a row of dp values: for every block of 32 consecutive
+// columns, 64 bytes of hi plane then 64 bytes of lo plane. A row therefore
+// takes 4 dp bytes, like fp32, and each 128-byte K stage of the GEMM core
+// holds 32 columns of both planes.
+__device__ inline void store_split(uint16_t* row_planes, int n, float v) {
+  const uint32_t hi = bf16_rne_bits(v);
+  const uint32_t lo = bf16_rne_bits(v - bf16_bits_value(hi));
+  uint16_t* b = row_planes + (n >> 5) * 64 + (n & 31);
+  b[0] = uint16_t(hi);
+  b[32] = uint16_t(lo);
+}
+
 template <>
 struct MfmaOp<Bf16Tag> {
   __device__ static inline void run(f4 (&acc)[4][4], const uint4 (&a)[4], const uint4 (&b)[4]) {
@@ -143,6 +166,46 @@ __device__ inline void compute_stage(f4 (&acc)[4][4], const char* buf) {
   __builtin_amdgcn_sched_group_barrier(0x008, StageShape<T>::kMfmaPerChunk, 0);
   __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
   __builtin_amdgcn_sched_group_barrier(0x008, StageShape<T>::kMfmaPerChunk, 0);
+}
+
+// Split-bf16 stage: segments 0-3 of a row hold the hi plane of 32 K values,
+// segments 4-7 the lo plane; per 16x16 block the stage runs hi*hi, then
+// hi*lo and lo*hi, each a v_mfma_f32_16x16x32_bf16.
+template <>
+__device__ inline void compute_stage<Bf16x3Tag>(f4 (&acc)[4][4], const char* buf) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1, g = lane >> 4;
+  uint4 a0[4], b0[4], a1[4], b1[4];
+#pragma unroll
+  for (int mi = 0; mi < 4; ++mi) {
+    const int r = wm * 64 + mi * 16 + (lane & 15);
+    a0[mi] = *reinterpret_cast<const uint4*>(buf + r * kStageRowBytes + ((g ^ (r & 7)) * 16));
+  }
+#pragma unroll
+  for (int ni = 0; ni < 4; ++ni) {
+    const int r = wn * 64 + ni * 16 + (lane & 15);
+    b0[ni] = *reinterpret_cast<const uint4*>(buf + kTile * kStageRowBytes + r * kStageRowBytes +
+                                             ((g ^ (r & 7)) * 16));
+  }
+  MfmaOp<Bf16Tag>::run(acc, a0, b0);
+#pragma unroll
+  for (int mi = 0; mi < 4; ++mi) {
+    const int r = wm * 64 + mi * 16 + (lane & 15);
+    a1[mi] = *reinterpret_cast<const uint4*>(buf + r * kStageRowBytes + (((4 + g) ^ (r & 7)) * 16));
+  }
+#pragma unroll
+  for (int ni = 0; ni < 4; ++ni) {
+    const int r = wn * 64 + ni * 16 + (lane & 15);
+    b1[ni] = *reinterpret_cast<const uint4*>(buf + kTile * kStageRowBytes + r * kStageRowBytes +
+                                             (((4 + g) ^ (r & 7)) * 16));
+  }
+  MfmaOp<Bf16Tag>::run(acc, a0, b1);
+  MfmaOp<Bf16Tag>::run(acc, a1, b0);
+  __builtin_amdgcn_sched_group_barrier(0x020, 8, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
 }
 
 // s_waitcnt vmcnt(0), leaving expcnt and lgkmcnt unwaited.

@@ -21,6 +21,7 @@ namespace optima {
 namespace {
 
 enum GemmMode { kPlain = 0, kPlain2 = 1, kStore = 2, kFused = 3 };
+enum Prec { kPrecF32 = OPTIMA_PREC_FP32, kPrecBf16x3 = OPTIMA_PREC_BF16X3 };
 
 struct ProductArgs {
   const float* A;      // rows of the multiplied vectors, pitch dp
@@ -40,6 +41,9 @@ struct ProductArgs {
   const int* kbase;    // iterations since restart, per column, at the last check
   int s;               // iterations since the last check before this product
   const float* Lp;     // step constant L
+  const uint16_t* Ap;  // kPrecBf16x3: split planes of A (same rows as A)
+  const uint16_t* Bp;  // kPrecBf16x3: split planes of H
+  uint16_t* XoutP;     // kPrecBf16x3, kFused: split planes of the next x
 };
 
 struct RowCoef {
@@ -59,7 +63,7 @@ __device__ inline RowCoef row_coef(const ProductArgs& p, int j, float L) {
 }
 
 // Consumes y = (H x)[j][n] for column j.
-template <int MODE>
+template <int MODE, int PREC>
 __device__ inline void epilogue_elem(const ProductArgs& p, int j, int n, float y, const RowCoef& c) {
   const size_t o = size_t(j) * p.dp + n;
   if (MODE == kPlain) {
@@ -78,13 +82,14 @@ __device__ inline void epilogue_elem(const ProductArgs& p, int j, int n, float y
     p.XA[o] = (1.f - c.alpha1) * p.XA[o] + c.alpha1 * xn;
     p.HA[o] = ha;
     p.Xout[o] = xn;
+    if (PREC == kPrecBf16x3) store_split(p.XoutP + size_t(j) * p.dp * 2, n, xn);
   }
 }
 
 // The products of `splits` contiguous K ranges of one output tile; with
 // splits == 1 the tile is finished in place, otherwise each range writes its
 // partial sum to part[split][launch row][n] and k_split_epilogue adds them.
-template <int MODE>
+template <int MODE, int PREC>
 __global__ void __launch_bounds__(kThreads) k_product(ProductArgs p, int splits, float* part) {
   const int tiles_m = (p.n_rows + kTile - 1) / kTile;
   const int tiles_n = p.dp / kTile;
@@ -106,11 +111,19 @@ __global__ void __launch_bounds__(kThreads) k_product(ProductArgs p, int splits,
     int r = m0 + load_row(i);
     r = r < p.n_rows ? r : p.n_rows - 1;
     const int j = p.rows ? p.rows[r] : r;
-    a_src[i] = reinterpret_cast<const char*>(p.A + size_t(j) * p.dp) + k_off;
-    b_src[i] = reinterpret_cast<const char*>(p.B + size_t(n0 + load_row(i)) * p.dp) + k_off;
+    // Both layouts take 4 dp bytes per row.
+    const char* a_base = PREC == kPrecBf16x3 ? reinterpret_cast<const char*>(p.Ap)
+                                             : reinterpret_cast<const char*>(p.A);
+    const char* b_base = PREC == kPrecBf16x3 ? reinterpret_cast<const char*>(p.Bp)
+                                             : reinterpret_cast<const char*>(p.B);
+    a_src[i] = a_base + size_t(j) * p.dp * 4 + k_off;
+    b_src[i] = b_base + size_t(n0 + load_row(i)) * p.dp * 4 + k_off;
   }
   f4 acc[4][4];
-  gemm_tile_mainloop<float>(acc, a_src, b_src, s1 - s0);
+  if (PREC == kPrecBf16x3)
+    gemm_tile_mainloop<Bf16x3Tag>(acc, a_src, b_src, s1 - s0);
+  else
+    gemm_tile_mainloop<float>(acc, a_src, b_src, s1 - s0);
 
   if (splits > 1) {
     float* P = part + size_t(sp) * size_t(tiles_m) * kTile * size_t(p.dp);
@@ -135,13 +148,14 @@ __global__ void __launch_bounds__(kThreads) k_product(ProductArgs p, int splits,
       const int j = p.rows ? p.rows[r] : r;
       const RowCoef c = row_coef<MODE>(p, j, L);
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni) epilogue_elem<MODE>(p, j, n0 + acc_col(ni), acc[mi][ni][e], c);
+      for (int ni = 0; ni < 4; ++ni)
+        epilogue_elem<MODE, PREC>(p, j, n0 + acc_col(ni), acc[mi][ni][e], c);
     }
   }
 }
 
 // Sums the split partials in split order and applies the product epilogue.
-template <int MODE>
+template <int MODE, int PREC>
 __global__ void __launch_bounds__(kThreads) k_split_epilogue(ProductArgs p, int splits,
                                                              const float* part) {
   const int r = blockIdx.x;
@@ -154,7 +168,7 @@ __global__ void __launch_bounds__(kThreads) k_split_epilogue(ProductArgs p, int 
     const float* q = part + size_t(r) * p.dp + n;
     float y = q[0];
     for (int sp = 1; sp < splits; ++sp) y += q[sp * split_stride];
-    epilogue_elem<MODE>(p, j, n, y, c);
+    epilogue_elem<MODE, PREC>(p, j, n, y, c);
   }
 }
 
@@ -163,7 +177,8 @@ __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows
                                                      const float* X, float* Xout, float* XA,
                                                      const float* HX, const float* HA,
                                                      const float* HW0, const uint8_t* mask,
-                                                     const int* kbase, const float* Lp) {
+                                                     const int* kbase, const float* Lp,
+                                                     uint16_t* XoutP) {
   const int r = blockIdx.x;
   if (r >= n_rows) return;
   const int j = rows ? rows[r] : r;
@@ -178,13 +193,14 @@ __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows
     const float xn = keep ? X[o] - eta * g : 0.f;
     XA[o] = (1.f - alpha) * XA[o] + alpha * xn;
     Xout[o] = xn;
+    if (XoutP) store_split(XoutP + base * 2, n, xn);
   }
 }
 
 // Copies W0 into padded rows and forms the start point x = x_ag = sel(m, w0, 0).
 __global__ void __launch_bounds__(kThreads) k_prep(const float* W0, const uint8_t* mask, int n_cols,
                                                    int d, int dp, float* W0P, float* X, float* XA,
-                                                   int* flags) {
+                                                   uint16_t* XP, int* flags) {
   const int j = blockIdx.x;
   const size_t base = size_t(j) * dp;
   bool bad = false;
@@ -200,8 +216,16 @@ __global__ void __launch_bounds__(kThreads) k_prep(const float* W0, const uint8_
     const float x = keep ? w : 0.f;
     X[base + n] = x;
     XA[base + n] = x;
+    if (XP) store_split(XP + base * 2, n, x);
   }
   if (bad) atomicOr(flags, 1);
+}
+
+// Split planes of H (row pitch 4 dp bytes), built once per solve.
+__global__ void __launch_bounds__(kThreads) k_split_h(const float* Hm, int dp, uint16_t* HP) {
+  const int i = blockIdx.x;
+  for (int n = blockIdx.y * kThreads + threadIdx.x; n < dp; n += gridDim.y * kThreads)
+    store_split(HP + size_t(i) * dp * 2, n, Hm[size_t(i) * dp + n]);
 }
 
 // Zero-padded copy of H (used when d is not a multiple of the tile) with a
@@ -249,6 +273,7 @@ struct CheckArgs {
   int n_rows;
   int dp, d;
   float* X;            // current x
+  uint16_t* XP;        // its split planes (kPrecBf16x3), else NULL
   float* XA;
   float* HX;
   float* HA;
@@ -397,6 +422,7 @@ __global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
     for (int n = threadIdx.x; n < a.dp; n += kThreads) {
       xd[base + n] = xs[base + n];
       hd[base + n] = hs[base + n];
+      if (!(dec & 4) && a.XP) store_split(a.XP + base * 2, n, xs[base + n]);
     }
   }
 }
@@ -442,6 +468,7 @@ struct Layout {
   size_t part_elems;
   float* part;
   float *X0, *X1, *XA, *HX, *HA, *HW0, *Hp, *L;
+  uint16_t *XP0, *XP1, *HP;  // split planes for kPrecBf16x3
   int *rows0, *rows1, *n_active, *flags;
   ColState st;
 };
@@ -462,6 +489,9 @@ Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
   l.part_elems = std::min<size_t>(size_t(kMaxSplitTiles) * kTile * kTile,
                                   size_t(kMaxSplits) * size_t(round_up(n_cols, kTile)) * size_t(l.dp));
   l.part = c.take<float>(l.part_elems);
+  l.XP0 = c.take<uint16_t>(2 * vec);
+  l.XP1 = c.take<uint16_t>(2 * vec);
+  l.HP = c.take<uint16_t>(2 * size_t(l.dp) * size_t(l.dp));
   l.rows0 = c.take<int>(n_cols);
   l.rows1 = c.take<int>(n_cols);
   l.st.kbase = c.take<int>(n_cols);
@@ -519,22 +549,28 @@ int choose_splits(int tiles, int stages, int tiles_m, int dp, size_t part_cap) {
   return best;
 }
 
-template <int MODE>
+template <int MODE, int PREC>
 optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t s) {
   const int tiles_m = int(ceil_div(p.n_rows, kTile));
   const int tiles_n = p.dp / kTile;
   const int stages = p.dp * 4 / kStageRowBytes;
   const int S = choose_splits(tiles_m * tiles_n, stages, tiles_m, p.dp, l.part_elems);
-  hipLaunchKernelGGL(k_product<MODE>, dim3(tiles_m * tiles_n * S), dim3(kThreads), 0, s, p, S,
-                     l.part);
+  hipLaunchKernelGGL((k_product<MODE, PREC>), dim3(tiles_m * tiles_n * S), dim3(kThreads), 0, s,
+                     p, S, l.part);
   OPTIMA_LAUNCH_CHECK();
   if (S > 1) {
     const dim3 g(unsigned(p.n_rows), unsigned(ceil_div(p.dp, 4 * kThreads)));
-    hipLaunchKernelGGL(k_split_epilogue<MODE>, g, dim3(kThreads), 0, s, p, S,
+    hipLaunchKernelGGL((k_split_epilogue<MODE, PREC>), g, dim3(kThreads), 0, s, p, S,
                        static_cast<const float*>(l.part));
     OPTIMA_LAUNCH_CHECK();
   }
   return OPTIMA_OK;
+}
+
+template <int MODE>
+optima_status launch_product(const ProductArgs& p, const Layout& l, int prec, hipStream_t s) {
+  return prec == kPrecBf16x3 ? launch_product<MODE, kPrecBf16x3>(p, l, s)
+                             : launch_product<MODE, kPrecF32>(p, l, s);
 }
 
 }  // namespace
@@ -567,9 +603,15 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   OPTIMA_LAUNCH_CHECK();
   const dim3 vec_grid(unsigned(nc), unsigned(ceil_div(dp, 4 * kThreads)));
   // W0 padded copy goes to HX first; Hw0 = H w0, then Hx = Hx_ag = H x0.
+  const bool split = o.precision == kPrecBf16x3;
   hipLaunchKernelGGL(k_prep, vec_grid, dim3(kThreads), 0, s, W0, mask, nc, di, dp, l.HX, l.X0,
-                     l.XA, l.flags);
+                     l.XA, split ? l.XP0 : nullptr, l.flags);
   OPTIMA_LAUNCH_CHECK();
+  if (split) {
+    hipLaunchKernelGGL(k_split_h, dim3(unsigned(dp), unsigned(ceil_div(dp, 4 * kThreads))),
+                       dim3(kThreads), 0, s, Hm, dp, l.HP);
+    OPTIMA_LAUNCH_CHECK();
+  }
   int flags = 0;
   OPTIMA_HIP_TRY(hipMemcpyAsync(&flags, l.flags, sizeof(int), hipMemcpyDeviceToHost, s));
   OPTIMA_HIP_TRY(hipStreamSynchronize(s));
@@ -584,13 +626,15 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   p.Lp = l.L;
   p.rows = nullptr;
   p.n_rows = nc;
+  p.Bp = l.HP;
+  // The two setup products stay in fp32 (Hw0 enters every gradient).
   p.A = l.HX;
   p.out1 = l.HW0;
-  if (auto e = launch_product<kPlain>(p, l, s)) return e;
+  if (auto e = launch_product<kPlain, kPrecF32>(p, l, s)) return e;
   p.A = l.X0;
   p.out1 = l.HX;
   p.out2 = l.HA;
-  if (auto e = launch_product<kPlain2>(p, l, s)) return e;
+  if (auto e = launch_product<kPlain2, kPrecF32>(p, l, s)) return e;
   inf.gemm_calls += 2;
   inf.row_products += 2 * int64_t(nc);
 
@@ -646,6 +690,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   int* rows = l.rows0;
   int* rows_next = l.rows1;
   float* xbuf[2] = {l.X0, l.X1};
+  uint16_t* xpl[2] = {l.XP0, l.XP1};
   int cur = 0;
   int64_t t = 0;
   const int64_t ce = o.check_every;
@@ -654,7 +699,8 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     const int n = int(t_next - t);
     const dim3 ug(unsigned(n_act), unsigned(ceil_div(dp, 4 * kThreads)));
     hipLaunchKernelGGL(k_update, ug, dim3(kThreads), 0, s, rows, n_act, dp, di, xbuf[cur],
-                       xbuf[cur ^ 1], l.XA, l.HX, l.HA, l.HW0, mask, l.st.kbase, l.L);
+                       xbuf[cur ^ 1], l.XA, l.HX, l.HA, l.HW0, mask, l.st.kbase, l.L,
+                       split ? xpl[cur ^ 1] : nullptr);
     OPTIMA_LAUNCH_CHECK();
     cur ^= 1;
     p.rows = rows;
@@ -665,16 +711,19 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     if (info) OPTIMA_HIP_TRY(hipEventRecord(ev[0], s));
     for (int i = 0; i + 1 < n; ++i) {
       p.A = xbuf[cur];
+      p.Ap = xpl[cur];
       p.Xin = xbuf[cur];
       p.Xout = xbuf[cur ^ 1];
+      p.XoutP = xpl[cur ^ 1];
       p.s = i;
-      if (auto e = launch_product<kFused>(p, l, s)) return e;
+      if (auto e = launch_product<kFused>(p, l, o.precision, s)) return e;
       cur ^= 1;
     }
     p.A = xbuf[cur];
+    p.Ap = xpl[cur];
     p.out1 = l.HX;
     p.s = n - 1;
-    if (auto e = launch_product<kStore>(p, l, s)) return e;
+    if (auto e = launch_product<kStore>(p, l, o.precision, s)) return e;
     if (info) OPTIMA_HIP_TRY(hipEventRecord(ev[1], s));
     inf.gemm_calls += n;
     inf.row_products += int64_t(n) * n_act;
@@ -685,6 +734,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     ca.rows = rows;
     ca.n_rows = n_act;
     ca.X = xbuf[cur];
+    ca.XP = split ? xpl[cur] : nullptr;
     ca.initial = 0;
     ca.final_check = t == o.max_iters;
     ca.t = t;

@@ -56,13 +56,18 @@ def _opts(L, **kw):
     return L.SolverOpts.default(**kw)
 
 
-def test_tiny_fixed_1000_matches_oracle_and_closed_form(L):
+# Both arithmetic paths of the H-product must meet the same parity bar.
+PRECISIONS = [pytest.param(0, id="fp32"), pytest.param(1, id="bf16x3")]
+
+
+@pytest.mark.parametrize("prec", PRECISIONS)
+def test_tiny_fixed_1000_matches_oracle_and_closed_form(L, prec):
     cfg = workloads.TINY
     H, W0, M, lam = _oracle_layer(cfg)
     o = oracle.rapdhg(H, W0, M, lam, oracle.SolverOptions(max_iters=1000, fixed_iters=True))
     ref = oracle.closed_form(H, W0, M)
     Wg, st, info = gpu_solve(L, to_dev(H), to_dev(np.array([lam])), W0, M,
-                             _opts(L, max_iters=1000, fixed_iters=1))
+                             _opts(L, max_iters=1000, fixed_iters=1, precision=prec))
     Wg = Wg.cpu().numpy()
     _assert_w_and_f(H, W0, M, Wg, o.W, label="vs oracle rapdhg")
     _assert_w_and_f(H, W0, M, Wg, ref, label="vs closed form")
@@ -72,20 +77,22 @@ def test_tiny_fixed_1000_matches_oracle_and_closed_form(L):
     assert np.all(st["restarts"] > 0)
 
 
+@pytest.mark.parametrize("prec", PRECISIONS)
 @pytest.mark.parametrize("T", [1, 2, 7, 40, 63])
-def test_trajectory_before_first_check(L, T):
+def test_trajectory_before_first_check(L, T, prec):
     # No check happens before iteration 64, so both sides follow the same
-    # continuous map; only rounding separates them.
+    # continuous map; only rounding separates them (fp32: 2^-24 per product;
+    # bf16x3: up to 3 * 2^-16 per product).
     cfg = workloads.TINY
     H, W0, M, lam = _oracle_layer(cfg)
     o = oracle.rapdhg(H, W0, M, lam, oracle.SolverOptions(max_iters=T, fixed_iters=True))
     Wg, st, _ = gpu_solve(L, to_dev(H), to_dev(np.array([lam])), W0, M,
-                          _opts(L, max_iters=T, fixed_iters=1))
+                          _opts(L, max_iters=T, fixed_iters=1, precision=prec))
     Wg = Wg.cpu().numpy()
     _assert_zero_pattern(Wg, M)
     per_col = np.linalg.norm(Wg - o.W, axis=1) / np.linalg.norm(o.W, axis=1)
     log(f"  T={T} worst column rel={per_col.max():.3e}")
-    assert per_col.max() <= 1e-5
+    assert per_col.max() <= (1e-5 if prec == 0 else 1e-4)
     assert np.all(st["iters"] == T)
 
 
@@ -163,7 +170,8 @@ def test_columns_are_independent(L):
         assert rel_fro(part.cpu().numpy(), full[sl]) <= 1e-5
 
 
-def test_ragged_shapes_multi_tile(L):
+@pytest.mark.parametrize("prec", PRECISIONS)
+def test_ragged_shapes_multi_tile(L, prec):
     # d not a multiple of the 128-wide tile, columns spanning several row
     # tiles with a ragged tail.
     rng = np.random.default_rng(5)
@@ -177,17 +185,23 @@ def test_ragged_shapes_multi_tile(L):
         M = (rng.random((n, d)) < 0.5).astype(np.uint8)
         lam = float(np.float32(np.linalg.eigvalsh(H)[-1]))
         Wg, st, _ = gpu_solve(L, to_dev(H), to_dev(np.array([lam])), W0, M,
-                              _opts(L, max_iters=3000, fixed_iters=1))
+                              _opts(L, max_iters=3000, fixed_iters=1, precision=prec))
         _assert_w_and_f(H, W0, M, Wg.cpu().numpy(), oracle.closed_form(H, W0, M),
                         label=f"d={d} n={n}")
 
 
-def test_gpt2_shape_tight(L):
+@pytest.fixture(scope="module")
+def gpt2_layer():
+    return _oracle_layer(workloads.GPT2_FC)
+
+
+@pytest.mark.parametrize("prec", PRECISIONS)
+def test_gpt2_shape_tight(L, gpt2_layer, prec):
     cfg = workloads.GPT2_FC
     log("gpt2 fc: oracle Hessian over the full token set")
-    H, W0, M, lam = _oracle_layer(cfg)
+    H, W0, M, lam = gpt2_layer
     Wg, st, info = gpu_solve(L, to_dev(H), to_dev(np.array([lam])), W0, M,
-                             _opts(L, max_iters=4000, fixed_iters=1))
+                             _opts(L, max_iters=4000, fixed_iters=1, precision=prec))
     Wg = Wg.cpu().numpy()
     _assert_zero_pattern(Wg, M)
     cols = np.arange(0, cfg.n_cols, cfg.n_cols // 96)
@@ -195,14 +209,20 @@ def test_gpt2_shape_tight(L):
     _assert_w_and_f(H, W0[cols], M[cols], Wg[cols], ref, label="gpt2 fc")
 
 
-def test_qproj_shape_tight(L):
+@pytest.fixture(scope="module")
+def qproj_layer():
+    return _oracle_layer(workloads.Q_PROJ.with_tokens(8 * 2048))
+
+
+@pytest.mark.parametrize("prec", PRECISIONS)
+def test_qproj_shape_tight(L, qproj_layer, prec):
     # The benchmark's launch shape (d = 4096, 4096 columns, 2:4 mask) on a
     # Hessian from 16384 tokens; 32 sampled columns against the closed form.
     cfg = workloads.Q_PROJ.with_tokens(8 * 2048)
     log("q_proj: oracle Hessian over 16384 tokens")
-    H, W0, M, lam = _oracle_layer(cfg)
+    H, W0, M, lam = qproj_layer
     Wg, st, info = gpu_solve(L, to_dev(H), to_dev(np.array([lam])), W0, M,
-                             _opts(L, max_iters=5000, fixed_iters=1))
+                             _opts(L, max_iters=5000, fixed_iters=1, precision=prec))
     Wg = Wg.cpu().numpy()
     _assert_zero_pattern(Wg, M)
     cols = np.arange(0, cfg.n_cols, cfg.n_cols // 32)
@@ -224,6 +244,9 @@ def test_error_paths(L):
     with pytest.raises(L.OptimaError) as e:
         L.optima_qp_solve_batched(Hd, torch.zeros_like(lmd), W0d, Md, out)
     assert e.value.status == -3
+    with pytest.raises(L.OptimaError) as e:
+        L.optima_qp_solve_batched(Hd, lmd, W0d, Md, out, opts=_opts(L, precision=7))
+    assert e.value.status == -5
     small = torch.empty(16, dtype=torch.uint8, device=dev())
     with pytest.raises(L.OptimaError) as e:
         L.optima_qp_solve_batched(Hd, lmd, W0d, Md, out, ws=small)
