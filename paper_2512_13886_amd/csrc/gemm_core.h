@@ -31,34 +31,38 @@
 // row 4 * (lane / 16) + e, column lane % 16.
 #pragma once
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace optima {
 
 constexpr int kStageRowBytes = 128;
-constexpr int kStageBufBytes = 2 * kTile * kStageRowBytes;  // A and B tiles, 32 KiB
 
-template <typename T>
-struct MfmaOp;
-
-template <>
-struct MfmaOp<float> {
-  __device__ static inline void run(f4 (&acc)[4][4], const uint4 (&a)[4], const uint4 (&b)[4]) {
+template <int MB, int NB>
+__device__ inline void mfma_f32_blocks(f4 (&acc)[MB][NB], const uint4 (&a)[MB], const uint4 (&b)[NB]) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+  for (int e = 0; e < 4; ++e)
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi) {
+    for (int mi = 0; mi < MB; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni) {
-          const unsigned av = e == 0 ? a[mi].x : e == 1 ? a[mi].y : e == 2 ? a[mi].z : a[mi].w;
-          const unsigned bv = e == 0 ? b[ni].x : e == 1 ? b[ni].y : e == 2 ? b[ni].z : b[ni].w;
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-              __uint_as_float(av), __uint_as_float(bv), acc[mi][ni], 0, 0, 0);
-        }
+      for (int ni = 0; ni < NB; ++ni) {
+        const unsigned av = e == 0 ? a[mi].x : e == 1 ? a[mi].y : e == 2 ? a[mi].z : a[mi].w;
+        const unsigned bv = e == 0 ? b[ni].x : e == 1 ? b[ni].y : e == 2 ? b[ni].z : b[ni].w;
+        acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(av), __uint_as_float(bv),
+                                                           acc[mi][ni], 0, 0, 0);
       }
-    }
-  }
-};
+}
+
+template <int MB, int NB>
+__device__ inline void mfma_bf16_blocks(f4 (&acc)[MB][NB], const uint4 (&a)[MB], const uint4 (&b)[NB]) {
+#pragma unroll
+  for (int mi = 0; mi < MB; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < NB; ++ni)
+      acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          __builtin_bit_cast(bf16x8, a[mi]), __builtin_bit_cast(bf16x8, b[ni]), acc[mi][ni], 0, 0, 0);
+}
 
 struct Bf16Tag {};
 
@@ -85,177 +89,239 @@ __device__ inline void store_split(uint16_t* row_planes, int n, float v) {
   b[32] = uint16_t(lo);
 }
 
-template <>
-struct MfmaOp<Bf16Tag> {
-  __device__ static inline void run(f4 (&acc)[4][4], const uint4 (&a)[4], const uint4 (&b)[4]) {
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi) {
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            __builtin_bit_cast(bf16x8, a[mi]), __builtin_bit_cast(bf16x8, b[ni]),
-            acc[mi][ni], 0, 0, 0);
-      }
-    }
-  }
+// Tile configuration: a BM x BN output tile per workgroup, WGM x WGN waves,
+// each wave owning a (BM / WGM) x (BN / WGN) sub-tile of 16x16 blocks, and
+// NBUF LDS stage buffers (prefetch distance NBUF - 1 stages).
+template <int BM_, int BN_, int WGM_, int WGN_, int NBUF_>
+struct TileCfg {
+  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, NBUF = NBUF_;
+  static constexpr int kWaves = WGM * WGN;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int MB = BM / WGM / 16;  // 16-row blocks per wave
+  static constexpr int NB = BN / WGN / 16;  // 16-column blocks per wave
+  static constexpr int kLoadsA = BM / 8 / kWaves;  // 1-KiB wave loads per stage
+  static constexpr int kLoadsB = BN / 8 / kWaves;
+  static constexpr int kLoads = kLoadsA + kLoadsB;
+  static constexpr int kBufBytes = (BM + BN) * kStageRowBytes;
+  static_assert(BM % (8 * kWaves) == 0 && BN % (8 * kWaves) == 0, "load rounds");
+  static_assert(NBUF == 2 || NBUF == 3, "stage buffers");
 };
 
-// Rows of the tile that this thread's direct loads fetch: round i (0..3)
-// covers tile row load_row(i); the byte offset of the fetched 16-byte segment
-// within the row's 128-byte stage is load_seg_bytes().
+// The 128 x 128 tile with 4 waves of 64 x 64 and two stage buffers.
+using Tile128 = TileCfg<128, 128, 2, 2, 2>;
+
+// Rows of the tile that this thread's direct loads fetch: A round i covers
+// A tile row load_row<Cfg>(i), B round i covers B tile row load_row<Cfg>(i);
+// the byte offset of the fetched 16-byte segment within the row's 128-byte
+// stage is load_seg_bytes().
+template <typename Cfg>
 __device__ inline int load_row(int i) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  return (i * 4 + wave) * 8 + (lane >> 3);
+  return (i * Cfg::kWaves + wave) * 8 + (lane >> 3);
 }
 __device__ inline int load_seg_bytes() {
   const int lane = threadIdx.x & 63;
   return ((lane & 7) ^ (lane >> 3)) * 16;
 }
 
-template <typename T>
-struct StageShape;
-template <>
-struct StageShape<float> {
-  static constexpr int kMfmaPerChunk = 64;
-};
-template <>
-struct StageShape<Bf16Tag> {
-  static constexpr int kMfmaPerChunk = 16;
+template <typename Cfg>
+struct Operands {
+  const char* a[Cfg::kLoadsA];
+  const char* b[Cfg::kLoadsB];
 };
 
-__device__ inline void issue_stage(const char* const (&a_src)[4], const char* const (&b_src)[4],
-                                   int s, char* buf) {
+template <typename Cfg>
+__device__ inline void issue_stage(const Operands<Cfg>& src, int s, char* buf) {
   const size_t o = size_t(s) * kStageRowBytes;
   const int wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    char* d = buf + (i * 4 + wave) * 1024;
+  for (int i = 0; i < Cfg::kLoadsA; ++i)
     __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(a_src[i] + o),
-        (__attribute__((address_space(3))) void*)d, 16, 0, 0);
+        (const __attribute__((address_space(1))) void*)(src.a[i] + o),
+        (__attribute__((address_space(3))) void*)(buf + (i * Cfg::kWaves + wave) * 1024), 16, 0, 0);
+#pragma unroll
+  for (int i = 0; i < Cfg::kLoadsB; ++i)
     __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(b_src[i] + o),
-        (__attribute__((address_space(3))) void*)(d + kTile * kStageRowBytes), 16, 0, 0);
-  }
+        (const __attribute__((address_space(1))) void*)(src.b[i] + o),
+        (__attribute__((address_space(3))) void*)(buf + Cfg::BM * kStageRowBytes +
+                                                  (i * Cfg::kWaves + wave) * 1024),
+        16, 0, 0);
 }
 
-template <typename T>
-__device__ inline void compute_stage(f4 (&acc)[4][4], const char* buf) {
+// 16 bytes of logical segment `seg` of tile row r (A rows first, then B).
+__device__ inline uint4 lds_frag(const char* buf, int r, int seg) {
+  return *reinterpret_cast<const uint4*>(buf + r * kStageRowBytes + ((seg ^ (r & 7)) * 16));
+}
+
+template <typename Cfg, typename T>
+__device__ inline void compute_stage(f4 (&acc)[Cfg::MB][Cfg::NB], const char* buf) {
+  constexpr int MB = Cfg::MB, NB = Cfg::NB;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1, g = lane >> 4;
+  const int ra = (wave / Cfg::WGN) * MB * 16 + (lane & 15);
+  const int rb = Cfg::BM + (wave % Cfg::WGN) * NB * 16 + (lane & 15);
+  const int g = lane >> 4;
+  if constexpr (std::is_same<T, Bf16x3Tag>::value) {
+    // Segments 0-3 of a row hold the hi plane of 32 K values, 4-7 the lo
+    // plane: per block hi*hi, hi*lo, lo*hi (one 16x16x32 bf16 MFMA each).
+    uint4 a0[MB], a1[MB], b0[NB], b1[NB];
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    uint4 a[4], b[4];
+    for (int mi = 0; mi < MB; ++mi) a0[mi] = lds_frag(buf, ra + mi * 16, g);
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi) {
-      const int r = wm * 64 + mi * 16 + (lane & 15);
-      a[mi] = *reinterpret_cast<const uint4*>(buf + r * kStageRowBytes + (((4 * c + g) ^ (r & 7)) * 16));
+    for (int ni = 0; ni < NB; ++ni) b0[ni] = lds_frag(buf, rb + ni * 16, g);
+    mfma_bf16_blocks<MB, NB>(acc, a0, b0);
+#pragma unroll
+    for (int ni = 0; ni < NB; ++ni) b1[ni] = lds_frag(buf, rb + ni * 16, 4 + g);
+    mfma_bf16_blocks<MB, NB>(acc, a0, b1);
+#pragma unroll
+    for (int mi = 0; mi < MB; ++mi) a1[mi] = lds_frag(buf, ra + mi * 16, 4 + g);
+    mfma_bf16_blocks<MB, NB>(acc, a1, b0);
+    __builtin_amdgcn_sched_group_barrier(0x020, Cfg::kLoads, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, MB + NB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, MB * NB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, MB * NB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, MB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, MB * NB, 0);
+  } else {
+    constexpr int kMfmaPerChunk = std::is_same<T, float>::value ? 4 * MB * NB : MB * NB;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      uint4 a[MB], b[NB];
+#pragma unroll
+      for (int mi = 0; mi < MB; ++mi) a[mi] = lds_frag(buf, ra + mi * 16, 4 * c + g);
+#pragma unroll
+      for (int ni = 0; ni < NB; ++ni) b[ni] = lds_frag(buf, rb + ni * 16, 4 * c + g);
+      if constexpr (std::is_same<T, float>::value)
+        mfma_f32_blocks<MB, NB>(acc, a, b);
+      else
+        mfma_bf16_blocks<MB, NB>(acc, a, b);
     }
-#pragma unroll
-    for (int ni = 0; ni < 4; ++ni) {
-      const int r = wn * 64 + ni * 16 + (lane & 15);
-      b[ni] = *reinterpret_cast<const uint4*>(buf + kTile * kStageRowBytes + r * kStageRowBytes +
-                                             (((4 * c + g) ^ (r & 7)) * 16));
-    }
-    MfmaOp<T>::run(acc, a, b);
+    __builtin_amdgcn_sched_group_barrier(0x020, Cfg::kLoads, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, MB + NB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerChunk, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, MB + NB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfmaPerChunk, 0);
   }
-  // Order within the stage: the 8 direct loads issued just before, then per
-  // chunk its 8 LDS reads and its MFMAs.
-  __builtin_amdgcn_sched_group_barrier(0x020, 8, 0);
-  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-  __builtin_amdgcn_sched_group_barrier(0x008, StageShape<T>::kMfmaPerChunk, 0);
-  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-  __builtin_amdgcn_sched_group_barrier(0x008, StageShape<T>::kMfmaPerChunk, 0);
 }
 
-// Split-bf16 stage: segments 0-3 of a row hold the hi plane of 32 K values,
-// segments 4-7 the lo plane; per 16x16 block the stage runs hi*hi, then
-// hi*lo and lo*hi, each a v_mfma_f32_16x16x32_bf16.
-template <>
-__device__ inline void compute_stage<Bf16x3Tag>(f4 (&acc)[4][4], const char* buf) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1, g = lane >> 4;
-  uint4 a0[4], b0[4], a1[4], b1[4];
-#pragma unroll
-  for (int mi = 0; mi < 4; ++mi) {
-    const int r = wm * 64 + mi * 16 + (lane & 15);
-    a0[mi] = *reinterpret_cast<const uint4*>(buf + r * kStageRowBytes + ((g ^ (r & 7)) * 16));
-  }
-#pragma unroll
-  for (int ni = 0; ni < 4; ++ni) {
-    const int r = wn * 64 + ni * 16 + (lane & 15);
-    b0[ni] = *reinterpret_cast<const uint4*>(buf + kTile * kStageRowBytes + r * kStageRowBytes +
-                                             ((g ^ (r & 7)) * 16));
-  }
-  MfmaOp<Bf16Tag>::run(acc, a0, b0);
-#pragma unroll
-  for (int mi = 0; mi < 4; ++mi) {
-    const int r = wm * 64 + mi * 16 + (lane & 15);
-    a1[mi] = *reinterpret_cast<const uint4*>(buf + r * kStageRowBytes + (((4 + g) ^ (r & 7)) * 16));
-  }
-#pragma unroll
-  for (int ni = 0; ni < 4; ++ni) {
-    const int r = wn * 64 + ni * 16 + (lane & 15);
-    b1[ni] = *reinterpret_cast<const uint4*>(buf + kTile * kStageRowBytes + r * kStageRowBytes +
-                                             (((4 + g) ^ (r & 7)) * 16));
-  }
-  MfmaOp<Bf16Tag>::run(acc, a0, b1);
-  MfmaOp<Bf16Tag>::run(acc, a1, b0);
-  __builtin_amdgcn_sched_group_barrier(0x020, 8, 0);
-  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-  __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
-  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-  __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
+// s_waitcnt vmcnt(n) (0 <= n < 64), leaving expcnt and lgkmcnt unwaited.
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
 }
 
-// s_waitcnt vmcnt(0), leaving expcnt and lgkmcnt unwaited.
-__device__ inline void wait_direct_loads() { __builtin_amdgcn_s_waitcnt(0xF70); }
-
-// a_src[i] / b_src[i]: address of the 16-byte segment this thread fetches in
-// tile row load_row(i) at the first stage (row start + load_seg_bytes());
-// stage s adds s * kStageRowBytes. All addresses must be 16-byte aligned.
-template <typename T>
-__device__ inline void gemm_tile_mainloop(f4 (&acc)[4][4], const char* const (&a_src)[4],
-                                          const char* const (&b_src)[4], int n_stages) {
-  __shared__ __attribute__((aligned(1024))) char lds0[kStageBufBytes];
-  __shared__ __attribute__((aligned(1024))) char lds1[kStageBufBytes];
+// src.a[i] / src.b[i]: address of the 16-byte segment this thread fetches in
+// A / B tile row load_row<Cfg>(i) at the first stage (row start +
+// load_seg_bytes()); stage s adds s * kStageRowBytes. All addresses must be
+// 16-byte aligned. lds0..lds2 (lds2 only with NBUF == 3) must be distinct
+// __shared__ arrays of Cfg::kBufBytes declared by the kernel: the loop is
+// unrolled by NBUF so that no LDS read names an array with an in-flight load.
+template <typename Cfg, typename T>
+__device__ inline void gemm_tile_mainloop(f4 (&acc)[Cfg::MB][Cfg::NB], const Operands<Cfg>& src,
+                                          int n, char* lds0, char* lds1, char* lds2) {
 #pragma unroll
-  for (int mi = 0; mi < 4; ++mi)
+  for (int mi = 0; mi < Cfg::MB; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f4{0.f, 0.f, 0.f, 0.f};
-  if (n_stages <= 0) return;
+    for (int ni = 0; ni < Cfg::NB; ++ni) acc[mi][ni] = f4{0.f, 0.f, 0.f, 0.f};
+  if (n <= 0) return;
+  auto cl = [n](int s) { return s < n ? s : n - 1; };
 
-  issue_stage(a_src, b_src, 0, lds0);
-  int s = 0;
-  for (; s + 1 < n_stages; s += 2) {
-    wait_direct_loads();
-    __syncthreads();
-    issue_stage(a_src, b_src, s + 1, lds1);
-    compute_stage<T>(acc, lds0);
-    wait_direct_loads();
-    __syncthreads();
-    issue_stage(a_src, b_src, s + 2 < n_stages ? s + 2 : n_stages - 1, lds0);
-    compute_stage<T>(acc, lds1);
-  }
-  if (s < n_stages) {  // odd count: the last stage is in lds0
-    wait_direct_loads();
-    __syncthreads();
-    compute_stage<T>(acc, lds0);
+  if constexpr (Cfg::NBUF == 2) {
+    issue_stage<Cfg>(src, 0, lds0);
+    int s = 0;
+    for (; s + 1 < n; s += 2) {
+      wait_vmcnt<0>();
+      __syncthreads();
+      issue_stage<Cfg>(src, s + 1, lds1);
+      compute_stage<Cfg, T>(acc, lds0);
+      wait_vmcnt<0>();
+      __syncthreads();
+      issue_stage<Cfg>(src, cl(s + 2), lds0);
+      compute_stage<Cfg, T>(acc, lds1);
+    }
+    if (s < n) {  // odd count: the last stage is in lds0
+      wait_vmcnt<0>();
+      __syncthreads();
+      compute_stage<Cfg, T>(acc, lds0);
+    }
+  } else {
+    issue_stage<Cfg>(src, 0, lds0);
+    issue_stage<Cfg>(src, cl(1), lds1);
+    int s = 0;
+    for (; s + 2 < n; s += 3) {
+      wait_vmcnt<Cfg::kLoads>();  // stage s landed, stage s + 1 may still fly
+      __syncthreads();
+      issue_stage<Cfg>(src, s + 2, lds2);
+      compute_stage<Cfg, T>(acc, lds0);
+      wait_vmcnt<Cfg::kLoads>();
+      __syncthreads();
+      issue_stage<Cfg>(src, cl(s + 3), lds0);
+      compute_stage<Cfg, T>(acc, lds1);
+      wait_vmcnt<Cfg::kLoads>();
+      __syncthreads();
+      issue_stage<Cfg>(src, cl(s + 4), lds1);
+      compute_stage<Cfg, T>(acc, lds2);
+    }
+    if (s < n) {  // one or two stages left, in lds0 and lds1
+      wait_vmcnt<Cfg::kLoads>();
+      __syncthreads();
+      compute_stage<Cfg, T>(acc, lds0);
+      if (s + 1 < n) {
+        wait_vmcnt<0>();
+        __syncthreads();
+        compute_stage<Cfg, T>(acc, lds1);
+      }
+    }
   }
   // No direct load may still be writing LDS when the workgroup moves on.
-  wait_direct_loads();
+  wait_vmcnt<0>();
   __syncthreads();
+}
+
+// Epilogue staging of a 128 x 128 fp32 accumulator tile through the (then
+// idle) stage buffers: tile rows 0-63 go to buf0 and 64-127 to buf1, 512
+// bytes per row, 16-byte column chunk c of row r at physical chunk
+// c ^ (r & 31). Both the MFMA-layout writes (16 lanes per row, four rows
+// 4 apart) and the row-chunk reads are free of bank conflicts. After a
+// barrier every thread can read 16-byte chunks of 4 consecutive columns.
+template <typename Cfg>
+__device__ inline void stage_tile(const f4 (&acc)[Cfg::MB][Cfg::NB], char* buf0, char* buf1) {
+  static_assert(Cfg::BM == 128 && Cfg::BN == 128, "staging covers 128 x 128 tiles");
+  static_assert(Cfg::kBufBytes >= 64 * 512, "stage buffers too small for the tile");
+#pragma unroll
+  for (int mi = 0; mi < Cfg::MB; ++mi)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) / Cfg::WGN;
+      const int wn = (threadIdx.x >> 6) % Cfg::WGN;
+      const int r = wm * Cfg::MB * 16 + mi * 16 + 4 * (lane >> 4) + e;
+      char* row = (r < 64 ? buf0 : buf1) + (r & 63) * 512;
+#pragma unroll
+      for (int ni = 0; ni < Cfg::NB; ++ni) {
+        const int col = wn * Cfg::NB * 16 + ni * 16 + (lane & 15);
+        const int ch = (col >> 2) ^ (r & 31);
+        *reinterpret_cast<float*>(row + ch * 16 + (col & 3) * 4) = acc[mi][ni][e];
+      }
+    }
+}
+
+__device__ inline float4 staged_chunk(const char* buf0, const char* buf1, int r, int c) {
+  const char* row = (r < 64 ? buf0 : buf1) + (r & 63) * 512;
+  return *reinterpret_cast<const float4*>(row + ((c ^ (r & 31)) * 16));
 }
 
 // Output coordinates of accumulator element (mi, ni, e) of this thread,
 // relative to the tile origin.
+template <typename Cfg>
 __device__ inline int acc_row(int mi, int e) {
-  const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) >> 1;
-  return wm * 64 + mi * 16 + 4 * (lane >> 4) + e;
+  const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) / Cfg::WGN;
+  return wm * Cfg::MB * 16 + mi * 16 + 4 * (lane >> 4) + e;
 }
+template <typename Cfg>
 __device__ inline int acc_col(int ni) {
-  const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) & 1;
-  return wn * 64 + ni * 16 + (lane & 15);
+  const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) % Cfg::WGN;
+  return wn * Cfg::NB * 16 + ni * 16 + (lane & 15);
 }
 
 // Maps a linear workgroup index to an output tile so that the workgroups that

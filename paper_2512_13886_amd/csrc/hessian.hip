@@ -78,32 +78,34 @@ template <typename T>
 __global__ void __launch_bounds__(kThreads) k_syrk(const char* XT, int64_t pitch_bytes,
                                                    int stages, int splits, int64_t dp,
                                                    float* part, int first) {
+  __shared__ __attribute__((aligned(1024))) char lds0[Tile128::kBufBytes];
+  __shared__ __attribute__((aligned(1024))) char lds1[Tile128::kBufBytes];
   const int tile = blockIdx.x / splits;
   const int sp = blockIdx.x - tile * splits;
   int ti, tj;
   tri_tile(tile, &ti, &tj);
   const int s0 = int(int64_t(stages) * sp / splits);
   const int s1 = int(int64_t(stages) * (sp + 1) / splits);
-  const char* a_src[4];
-  const char* b_src[4];
+  using Cfg = Tile128;
+  Operands<Cfg> src;
   const int64_t k_off = int64_t(s0) * kStageRowBytes + load_seg_bytes();
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t r = load_row(i);
-    a_src[i] = XT + (int64_t(ti) * kTile + r) * pitch_bytes + k_off;
-    b_src[i] = XT + (int64_t(tj) * kTile + r) * pitch_bytes + k_off;
-  }
-  f4 acc[4][4];
-  gemm_tile_mainloop<T>(acc, a_src, b_src, s1 - s0);
+  for (int i = 0; i < Cfg::kLoadsA; ++i)
+    src.a[i] = XT + (int64_t(ti) * kTile + load_row<Cfg>(i)) * pitch_bytes + k_off;
+#pragma unroll
+  for (int i = 0; i < Cfg::kLoadsB; ++i)
+    src.b[i] = XT + (int64_t(tj) * kTile + load_row<Cfg>(i)) * pitch_bytes + k_off;
+  f4 acc[Cfg::MB][Cfg::NB];
+  gemm_tile_mainloop<Cfg, T>(acc, src, s1 - s0, lds0, lds1, nullptr);
   float* P = part + size_t(sp) * size_t(dp) * size_t(dp);
 #pragma unroll
   for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int64_t i = int64_t(ti) * kTile + acc_row(mi, e);
+      const int64_t i = int64_t(ti) * kTile + acc_row<Cfg>(mi, e);
 #pragma unroll
       for (int ni = 0; ni < 4; ++ni) {
-        const int64_t j = int64_t(tj) * kTile + acc_col(ni);
+        const int64_t j = int64_t(tj) * kTile + acc_col<Cfg>(ni);
         float* q = P + i * dp + j;
         *q = first ? acc[mi][ni][e] : *q + acc[mi][ni][e];
       }

@@ -62,35 +62,91 @@ __device__ inline RowCoef row_coef(const ProductArgs& p, int j, float L) {
   return c;
 }
 
-// Consumes y = (H x)[j][n] for column j.
+__device__ inline float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ inline void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+
+// Keep flags of columns n..n+3 (n a multiple of 4) of mask row j.
+__device__ inline void mask4(const uint8_t* mask, int d, int j, int n, bool (&keep)[4]) {
+  const uint8_t* m = mask + size_t(j) * d + n;
+  if ((d & 3) == 0 && n + 3 < d) {
+    const uchar4 v = *reinterpret_cast<const uchar4*>(m);
+    keep[0] = v.x != 0;
+    keep[1] = v.y != 0;
+    keep[2] = v.z != 0;
+    keep[3] = v.w != 0;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) keep[e] = n + e < d && m[e] != 0;
+  }
+}
+
+// Split planes of 4 consecutive values at column n (a multiple of 4) of a
+// plane-layout row: two 8-byte stores.
+__device__ inline void store_split4(uint16_t* row_planes, int n, const float (&v)[4]) {
+  uint32_t hi[4], lo[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    hi[e] = bf16_rne_bits(v[e]);
+    lo[e] = bf16_rne_bits(v[e] - bf16_bits_value(hi[e]));
+  }
+  uint16_t* b = row_planes + (n >> 5) * 64 + (n & 31);
+  *reinterpret_cast<uint2*>(b) = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
+  *reinterpret_cast<uint2*>(b + 32) = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
+}
+
+// Consumes y = (H x)[j][n..n+3] for column j (n a multiple of 4).
 template <int MODE, int PREC>
-__device__ inline void epilogue_elem(const ProductArgs& p, int j, int n, float y, const RowCoef& c) {
+__device__ inline void epilogue4(const ProductArgs& p, int j, int n, float4 y4, const RowCoef& c) {
   const size_t o = size_t(j) * p.dp + n;
   if (MODE == kPlain) {
-    p.out1[o] = y;
+    st4(p.out1 + o, y4);
   } else if (MODE == kPlain2) {
-    p.out1[o] = y;
-    p.out2[o] = y;
+    st4(p.out1 + o, y4);
+    st4(p.out2 + o, y4);
   } else if (MODE == kStore) {
-    p.HA[o] = (1.f - c.alpha) * p.HA[o] + c.alpha * y;
-    p.out1[o] = y;
+    float4 ha = ld4(p.HA + o);
+    ha.x = (1.f - c.alpha) * ha.x + c.alpha * y4.x;
+    ha.y = (1.f - c.alpha) * ha.y + c.alpha * y4.y;
+    ha.z = (1.f - c.alpha) * ha.z + c.alpha * y4.z;
+    ha.w = (1.f - c.alpha) * ha.w + c.alpha * y4.w;
+    st4(p.HA + o, ha);
+    st4(p.out1 + o, y4);
   } else {  // kFused: finish this iteration's products, run the next update
-    const float ha = (1.f - c.alpha) * p.HA[o] + c.alpha * y;
-    const float g = 2.f * ((1.f - c.alpha1) * ha + c.alpha1 * y - p.HW0[o]);
-    const bool keep = n < p.d && p.mask[size_t(j) * p.d + n] != 0;
-    const float xn = keep ? p.Xin[o] - c.eta1 * g : 0.f;
-    p.XA[o] = (1.f - c.alpha1) * p.XA[o] + c.alpha1 * xn;
-    p.HA[o] = ha;
-    p.Xout[o] = xn;
-    if (PREC == kPrecBf16x3) store_split(p.XoutP + size_t(j) * p.dp * 2, n, xn);
+    const float4 ha4 = ld4(p.HA + o), hw4 = ld4(p.HW0 + o), xi4 = ld4(p.Xin + o),
+                 xa4 = ld4(p.XA + o);
+    const float y[4] = {y4.x, y4.y, y4.z, y4.w};
+    const float hav[4] = {ha4.x, ha4.y, ha4.z, ha4.w};
+    const float hwv[4] = {hw4.x, hw4.y, hw4.z, hw4.w};
+    const float xiv[4] = {xi4.x, xi4.y, xi4.z, xi4.w};
+    const float xav[4] = {xa4.x, xa4.y, xa4.z, xa4.w};
+    bool keep[4];
+    mask4(p.mask, p.d, j, n, keep);
+    float ha[4], xn[4], xa[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      ha[e] = (1.f - c.alpha) * hav[e] + c.alpha * y[e];
+      const float g = 2.f * ((1.f - c.alpha1) * ha[e] + c.alpha1 * y[e] - hwv[e]);
+      xn[e] = keep[e] ? xiv[e] - c.eta1 * g : 0.f;
+      xa[e] = (1.f - c.alpha1) * xav[e] + c.alpha1 * xn[e];
+    }
+    st4(p.XA + o, make_float4(xa[0], xa[1], xa[2], xa[3]));
+    st4(p.HA + o, make_float4(ha[0], ha[1], ha[2], ha[3]));
+    st4(p.Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
+    if (PREC == kPrecBf16x3) store_split4(p.XoutP + size_t(j) * p.dp * 2, n, xn);
   }
 }
 
 // The products of `splits` contiguous K ranges of one output tile; with
 // splits == 1 the tile is finished in place, otherwise each range writes its
 // partial sum to part[split][launch row][n] and k_split_epilogue adds them.
+// The accumulators pass through LDS so that the epilogue works on 16-byte
+// chunks of 4 consecutive columns (full-width loads and stores).
 template <int MODE, int PREC>
-__global__ void __launch_bounds__(kThreads) k_product(ProductArgs p, int splits, float* part) {
+__global__ void __launch_bounds__(Tile128::kThreads) k_product(ProductArgs p, int splits,
+                                                               float* part) {
+  using Cfg = Tile128;
+  __shared__ __attribute__((aligned(1024))) char lds0[Cfg::kBufBytes];
+  __shared__ __attribute__((aligned(1024))) char lds1[Cfg::kBufBytes];
   const int tiles_m = (p.n_rows + kTile - 1) / kTile;
   const int tiles_n = p.dp / kTile;
   const int n_tiles = tiles_m * tiles_n;
@@ -103,54 +159,47 @@ __global__ void __launch_bounds__(kThreads) k_product(ProductArgs p, int splits,
   const int s0 = int(int64_t(stages) * sp / splits);
   const int s1 = int(int64_t(stages) * (sp + 1) / splits);
 
-  const char* a_src[4];
-  const char* b_src[4];
+  Operands<Cfg> src;
   const size_t k_off = size_t(s0) * kStageRowBytes + load_seg_bytes();
+  // Both layouts take 4 dp bytes per row.
+  const char* a_base = PREC == kPrecBf16x3 ? reinterpret_cast<const char*>(p.Ap)
+                                           : reinterpret_cast<const char*>(p.A);
+  const char* b_base = PREC == kPrecBf16x3 ? reinterpret_cast<const char*>(p.Bp)
+                                           : reinterpret_cast<const char*>(p.B);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int r = m0 + load_row(i);
+  for (int i = 0; i < Cfg::kLoadsA; ++i) {
+    int r = m0 + load_row<Cfg>(i);
     r = r < p.n_rows ? r : p.n_rows - 1;
     const int j = p.rows ? p.rows[r] : r;
-    // Both layouts take 4 dp bytes per row.
-    const char* a_base = PREC == kPrecBf16x3 ? reinterpret_cast<const char*>(p.Ap)
-                                             : reinterpret_cast<const char*>(p.A);
-    const char* b_base = PREC == kPrecBf16x3 ? reinterpret_cast<const char*>(p.Bp)
-                                             : reinterpret_cast<const char*>(p.B);
-    a_src[i] = a_base + size_t(j) * p.dp * 4 + k_off;
-    b_src[i] = b_base + size_t(n0 + load_row(i)) * p.dp * 4 + k_off;
+    src.a[i] = a_base + size_t(j) * p.dp * 4 + k_off;
   }
-  f4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < Cfg::kLoadsB; ++i)
+    src.b[i] = b_base + size_t(n0 + load_row<Cfg>(i)) * p.dp * 4 + k_off;
+  f4 acc[Cfg::MB][Cfg::NB];
   if (PREC == kPrecBf16x3)
-    gemm_tile_mainloop<Bf16x3Tag>(acc, a_src, b_src, s1 - s0);
+    gemm_tile_mainloop<Cfg, Bf16x3Tag>(acc, src, s1 - s0, lds0, lds1, nullptr);
   else
-    gemm_tile_mainloop<float>(acc, a_src, b_src, s1 - s0);
+    gemm_tile_mainloop<Cfg, float>(acc, src, s1 - s0, lds0, lds1, nullptr);
 
-  if (splits > 1) {
-    float* P = part + size_t(sp) * size_t(tiles_m) * kTile * size_t(p.dp);
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = m0 + acc_row(mi, e);
-        if (r >= p.n_rows) continue;
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni) P[size_t(r) * p.dp + n0 + acc_col(ni)] = acc[mi][ni][e];
-      }
-    return;
-  }
+  stage_tile<Cfg>(acc, lds0, lds1);
+  __syncthreads();
   const float L = (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f;
-#pragma unroll
-  for (int mi = 0; mi < 4; ++mi) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = m0 + acc_row(mi, e);
-      if (r >= p.n_rows) continue;
-      const int j = p.rows ? p.rows[r] : r;
-      const RowCoef c = row_coef<MODE>(p, j, L);
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni)
-        epilogue_elem<MODE, PREC>(p, j, n0 + acc_col(ni), acc[mi][ni][e], c);
+  float* P = part + size_t(sp) * size_t(tiles_m) * kTile * size_t(p.dp);
+#pragma unroll 4
+  for (int q = 0; q < kTile * kTile / 4 / Cfg::kThreads; ++q) {
+    const int c = threadIdx.x + Cfg::kThreads * q;  // 16-byte chunk of the tile
+    const int r = c >> 5, ch = c & 31;
+    const int rg = m0 + r;
+    if (rg >= p.n_rows) continue;
+    const float4 y = staged_chunk(lds0, lds1, r, ch);
+    const int n = n0 + 4 * ch;
+    if (splits > 1) {
+      st4(P + size_t(rg) * p.dp + n, y);
+      continue;
     }
+    const int j = p.rows ? p.rows[rg] : rg;
+    epilogue4<MODE, PREC>(p, j, n, y, row_coef<MODE>(p, j, L));
   }
 }
 
@@ -164,11 +213,17 @@ __global__ void __launch_bounds__(kThreads) k_split_epilogue(ProductArgs p, int 
   const int tiles_m = (p.n_rows + kTile - 1) / kTile;
   const size_t split_stride = size_t(tiles_m) * kTile * size_t(p.dp);
   const RowCoef c = row_coef<MODE>(p, j, (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f);
-  for (int n = blockIdx.y * kThreads + threadIdx.x; n < p.dp; n += gridDim.y * kThreads) {
+  for (int n = 4 * (blockIdx.y * kThreads + threadIdx.x); n < p.dp; n += 4 * gridDim.y * kThreads) {
     const float* q = part + size_t(r) * p.dp + n;
-    float y = q[0];
-    for (int sp = 1; sp < splits; ++sp) y += q[sp * split_stride];
-    epilogue_elem<MODE, PREC>(p, j, n, y, c);
+    float4 y = ld4(q);
+    for (int sp = 1; sp < splits; ++sp) {
+      const float4 t = ld4(q + sp * split_stride);
+      y.x += t.x;
+      y.y += t.y;
+      y.z += t.z;
+      y.w += t.w;
+    }
+    epilogue4<MODE, PREC>(p, j, n, y, c);
   }
 }
 
@@ -186,14 +241,25 @@ __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows
   const float alpha = 2.f / (k + 2.f);
   const float eta = (k + 1.f) / (2.f * *Lp);
   const size_t base = size_t(j) * dp;
-  for (int n = blockIdx.y * kThreads + threadIdx.x; n < dp; n += gridDim.y * kThreads) {
+  for (int n = 4 * (blockIdx.y * kThreads + threadIdx.x); n < dp; n += 4 * gridDim.y * kThreads) {
     const size_t o = base + n;
-    const float g = 2.f * ((1.f - alpha) * HA[o] + alpha * HX[o] - HW0[o]);
-    const bool keep = n < d && mask[size_t(j) * d + n] != 0;
-    const float xn = keep ? X[o] - eta * g : 0.f;
-    XA[o] = (1.f - alpha) * XA[o] + alpha * xn;
-    Xout[o] = xn;
-    if (XoutP) store_split(XoutP + base * 2, n, xn);
+    const float4 ha4 = ld4(HA + o), hx4 = ld4(HX + o), hw4 = ld4(HW0 + o), x4 = ld4(X + o),
+                 xa4 = ld4(XA + o);
+    const float hav[4] = {ha4.x, ha4.y, ha4.z, ha4.w}, hxv[4] = {hx4.x, hx4.y, hx4.z, hx4.w};
+    const float hwv[4] = {hw4.x, hw4.y, hw4.z, hw4.w}, xv[4] = {x4.x, x4.y, x4.z, x4.w};
+    const float xav[4] = {xa4.x, xa4.y, xa4.z, xa4.w};
+    bool keep[4];
+    mask4(mask, d, j, n, keep);
+    float xn[4], xa[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float g = 2.f * ((1.f - alpha) * hav[e] + alpha * hxv[e] - hwv[e]);
+      xn[e] = keep[e] ? xv[e] - eta * g : 0.f;
+      xa[e] = (1.f - alpha) * xav[e] + alpha * xn[e];
+    }
+    st4(XA + o, make_float4(xa[0], xa[1], xa[2], xa[3]));
+    st4(Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
+    if (XoutP) store_split4(XoutP + base * 2, n, xn);
   }
 }
 
