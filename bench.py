@@ -12,10 +12,14 @@ tokens with heavy-tailed features and 8 outlier channels):
 All inputs (X, W0, mask, start vector) are resident in HBM before timing.
 `value` is QP columns solved per second for the whole step. The JSON line also
 carries rAPDHG iterations/s, the roofline of the dominant kernel (the batched
-H-product, timed with HIP events on its stream inside the library) and the CPU
-oracle's throughput on a bounded sample of the same workload.
+H-product with the fused update, over the timed steps' own launches, timed with
+HIP events on its stream inside the library) and the CPU oracle's throughput on
+a bounded sample of the same workload. After the timed steps an untimed
+full-batch leg runs all 4096 columns for a fixed number of iterations (the
+iteration rate at B = C); --fixed-iters 0 leaves it out.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+                       [--precision bf16x3|fp32] [--fixed-iters N]
 """
 from __future__ import annotations
 
@@ -32,12 +36,15 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "QP columns solved/sec + rAPDHG iters/sec on 4096×4096 layer; MFMA % of peak"
+# Published dense MFMA peaks of MI355X.
 FP32_MFMA_PEAK_TFLOPS = 157.3
+BF16_MFMA_PEAK_TFLOPS = 2500.0
 HBM_PEAK_GBS = 8000.0
 
 # HBM traffic of the product kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (profiles/), valid only for the kernel sources they were taken on.
-TRAFFIC = None  # {"sources_sha1": "...", "bytes_per_launch": ...}
+TRAFFIC = {"sources_sha1": "4635400bde2627c92ab3f1dc3737c18f53a59e20",
+           "bytes_per_launch": 421010 * 1024}
 
 
 def log(msg: str):
@@ -93,12 +100,13 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-cols", type=int, default=32)
-    ap.add_argument("--cpu-sample-chunks", type=int, default=8)
+    ap.add_argument("--cpu-sample-cols", type=int, default=256)
+    ap.add_argument("--cpu-sample-chunks", type=int, default=32)
     ap.add_argument("--fixed-iters", type=int, default=1000,
-                    help="iterations of the full-batch leg that sets the roofline")
-    ap.add_argument("--precision", choices=["fp32", "bf16x3"], default="fp32",
-                    help="arithmetic of the per-iteration H-products")
+                    help="iterations of the untimed full-batch leg (0: skip it)")
+    ap.add_argument("--precision", choices=["fp32", "bf16x3"], default=None,
+                    help="arithmetic of the per-iteration H-products (default: the "
+                         "library's, bf16x3)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="first run one 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -143,9 +151,13 @@ def main() -> int:
     qws = torch.empty(L.optima_qp_workspace_bytes(d, C), dtype=torch.uint8, device=dev)
     iters = torch.zeros(C, dtype=torch.int32, device=dev)
     conv = torch.zeros(C, dtype=torch.uint8, device=dev)
-    prec = {"fp32": L.PREC_FP32, "bf16x3": L.PREC_BF16X3}[args.precision]
     # Table 8: tol 0.01 / 0.01, 100000 iterations
-    opts = L.SolverOpts.default(precision=prec)
+    opts = L.SolverOpts.default()
+    if args.precision is not None:
+        opts.precision = {"fp32": L.PREC_FP32, "bf16x3": L.PREC_BF16X3}[args.precision]
+    prec = opts.precision
+    prec_name = "bf16x3" if prec == L.PREC_BF16X3 else "fp32"
+    torch.cuda.reset_peak_memory_stats(dev)
     torch.cuda.synchronize()
 
     def step():
@@ -190,24 +202,57 @@ def main() -> int:
         f"per-column iterations {per_col_it.min()}..{per_col_it.max()})")
     log(f"H-product: {launches} launches, avg {avg_launch_us:.1f} us, {achieved:.1f} TFLOP/s")
 
-    # Full-batch leg: all 4096 columns for a fixed number of iterations. It
-    # gives the iteration rate at B = C and the roofline of the H-product.
-    fixed = L.SolverOpts.default(max_iters=args.fixed_iters, fixed_iters=1, precision=prec)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    finfo = L.optima_qp_solve_batched(H, lmax, W0d, Md, Wout, opts=fixed, ws=qws)
-    e1.record()
-    torch.cuda.synchronize()
-    fixed_ms = e0.elapsed_time(e1)
-    f_flops = 2.0 * d * d * finfo["timed_row_products"]
-    f_launch_us = finfo["timed_product_ms"] * 1e3 / finfo["timed_launches"]
-    fixed_tflops = f_flops / (finfo["timed_product_ms"] * 1e-3) / 1e12
-    log(f"fixed {args.fixed_iters} iterations x {C} columns: {fixed_ms:.1f} ms, H-product "
-        f"{fixed_tflops:.1f} TFLOP/s, avg launch {f_launch_us:.1f} us")
+    # Full-batch leg: all 4096 columns for a fixed number of iterations, the
+    # iteration rate at B = C (not part of the timed step).
+    fixed_batch = None
+    if args.fixed_iters > 0:
+        fixed = L.SolverOpts.default(max_iters=args.fixed_iters, fixed_iters=1, precision=prec)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        finfo = L.optima_qp_solve_batched(H, lmax, W0d, Md, Wout, opts=fixed, ws=qws)
+        e1.record()
+        torch.cuda.synchronize()
+        fixed_ms = e0.elapsed_time(e1)
+        f_flops = 2.0 * d * d * finfo["timed_row_products"]
+        f_launch_us = finfo["timed_product_ms"] * 1e3 / finfo["timed_launches"]
+        fixed_tflops = f_flops / (finfo["timed_product_ms"] * 1e-3) / 1e12
+        log(f"fixed {args.fixed_iters} iterations x {C} columns: {fixed_ms:.1f} ms, H-product "
+            f"{fixed_tflops:.1f} TFLOP/s, avg launch {f_launch_us:.1f} us")
+        fixed_batch = {"iters": args.fixed_iters, "columns": C, "ms": fixed_ms,
+                       "iters_per_s": args.fixed_iters / (fixed_ms * 1e-3),
+                       "column_iters_per_s": args.fixed_iters * C / (fixed_ms * 1e-3),
+                       "product_tflops": fixed_tflops, "product_avg_launch_us": f_launch_us}
 
-    traffic = None
-    if TRAFFIC and TRAFFIC.get("sources_sha1") == kernel_sources_sha1():
+    traffic = None  # the counter passes were taken on the bf16x3 kernels
+    if (TRAFFIC and prec == L.PREC_BF16X3
+            and TRAFFIC.get("sources_sha1") == kernel_sources_sha1()):
         traffic = TRAFFIC["bytes_per_launch"]
+
+    # Roofline of the dominant kernel over the timed steps: algorithmic flops
+    # (2 d^2 per column per iteration) over the device time of its launches.
+    if prec == L.PREC_BF16X3:
+        roofline = {
+            "kernel": "k_product<fused, bf16x3>: H-product x H over the active columns "
+                      "(M = active columns, N = K = 4096) on v_mfma_f32_16x16x32_bf16, three "
+                      "bf16 products per fp32 product, fused rAPDHG update in the epilogue",
+            "bound": "mfma", "achieved": achieved, "peak": BF16_MFMA_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": achieved / BF16_MFMA_PEAK_TFLOPS,
+            "traffic": traffic,
+            "mfma_issued_tflops": 3.0 * achieved,
+            "mfma_issued_frac": 3.0 * achieved / BF16_MFMA_PEAK_TFLOPS,
+            "fp32_equivalent_frac": achieved / FP32_MFMA_PEAK_TFLOPS,
+        }
+    else:
+        roofline = {
+            "kernel": "k_product<fused, fp32>: H-product over the active columns "
+                      "(M = active columns, N = K = 4096) on v_mfma_f32_16x16x4_f32, fused "
+                      "rAPDHG update in the epilogue",
+            "bound": "mfma", "achieved": achieved, "peak": FP32_MFMA_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": achieved / FP32_MFMA_PEAK_TFLOPS,
+            "traffic": traffic,
+        }
+    roofline.update({"avg_launch_us": avg_launch_us, "launches": launches,
+                     "flops_per_launch": flops / launches})
 
     out = {
         "metric": METRIC,
@@ -220,7 +265,7 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": prec_name,
         "data": "synthetic",
         "config": {
             "workload": ("q_proj layer d_in=4096 x 4096 columns: Hessian from 262144 bf16 "
@@ -228,29 +273,16 @@ def main() -> int:
                          "rAPDHG at tol 0.01/0.01, max 100000 iterations"),
             "d": d, "n_cols": C, "n_tok": N, "x_dtype": "bf16", "mask": "2:4",
             "eps_rel": 0.01, "eps_abs": 0.01, "check_every": 64,
+            "product_precision": prec_name,
         },
         "rapdhg_iters_per_s": it / (solve_ms * 1e-3),
         "column_iters_per_s": col_it / (solve_ms * 1e-3),
         "iterations": it,
         "phase_ms": {"hessian": hess_ms, "damp_spectral": spec_ms, "solve": solve_ms},
         "hessian_tflops": 2.0 * N * d * d / 2 / (hess_ms * 1e-3) / 1e12,
-        "fixed_batch": {"iters": args.fixed_iters, "columns": C, "ms": fixed_ms,
-                        "iters_per_s": args.fixed_iters / (fixed_ms * 1e-3),
-                        "column_iters_per_s": args.fixed_iters * C / (fixed_ms * 1e-3)},
-        "paper_mode_product": {"tflops": achieved, "avg_launch_us": avg_launch_us,
-                               "launches_per_step": launches / args.steps},
-        "roofline": {
-            "kernel": "k_product<3>/<2>: fp32 MFMA H-product (M=N=K=4096) with the fused "
-                      "rAPDHG update in its epilogue, full batch",
-            "bound": "mfma",
-            "achieved": fixed_tflops,
-            "peak": FP32_MFMA_PEAK_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": fixed_tflops / FP32_MFMA_PEAK_TFLOPS,
-            "traffic": traffic,
-            "avg_launch_us": f_launch_us,
-            "flops_per_launch": f_flops / finfo["timed_launches"],
-        },
+        "fixed_batch": fixed_batch,
+        "peak_device_memory_gib": torch.cuda.max_memory_allocated(dev) / 2**30,
+        "roofline": roofline,
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")

@@ -100,7 +100,7 @@ void optima_solver_opts_default(optima_solver_opts* o) {
   o->beta_artificial = 0.36f;
   o->step_safety = 1e-3f;
   o->restarts = 1;
-  o->precision = OPTIMA_PREC_FP32;
+  o->precision = OPTIMA_PREC_BF16X3;
 }
 
 size_t optima_qp_workspace_bytes(int64_t d, int64_t n_cols) {
