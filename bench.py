@@ -5,7 +5,8 @@ One step prunes-and-reconstructs one synthetic Llama-3-8B-shaped q_proj layer
 (d_in = 4096, 4096 output columns, 2:4 Wanda mask, 262144 bf16 calibration
 tokens with heavy-tailed features and 8 outlier channels):
 
-  Hessian H = X^T X over all 262144 tokens -> damping -> spectral norm ->
+  Hessian H = X^T X over all 262144 tokens -> damping -> spectral norm
+  (block-16 subspace iteration) ->
   batched rAPDHG solve of the 4096 column QPs at the paper's tolerance
   (relative = absolute = 0.01, at most 100000 iterations).
 
@@ -40,6 +41,8 @@ METRIC = "QP columns solved/sec + rAPDHG iters/sec on 4096×4096 layer; MFMA % o
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 HBM_PEAK_GBS = 8000.0
+# Start vectors of the subspace iteration that sets the step size.
+SPECTRAL_BLOCK = 16
 
 # HBM traffic of the product kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (profiles/), valid only for the kernel sources they were taken on.
@@ -74,7 +77,8 @@ def cpu_baseline(cfg, X, W0, mask, sample_cols: int, sample_chunks: int) -> dict
     t_hess = time.perf_counter() - t0
     H, _ = oracle.damp(H, cfg.rel_damp)
     t0 = time.perf_counter()
-    lam, _ = oracle.power_iteration(H, workloads.power_start(cfg.d), 1000, 1e-6)
+    lam, _ = oracle.subspace_iteration(H, workloads.power_start_block(cfg.d, SPECTRAL_BLOCK),
+                                       1000, 1e-6)
     t_pow = time.perf_counter() - t0
     cols = np.linspace(0, cfg.n_cols - 1, sample_cols).astype(int)
     t0 = time.perf_counter()
@@ -87,7 +91,7 @@ def cpu_baseline(cfg, X, W0, mask, sample_cols: int, sample_chunks: int) -> dict
         "kind": "oracle",
         "sample": (f"fp64 NumPy oracle: Hessian over {sample_chunks} of {cfg.n_chunks} "
                    f"2048-token sequences (time scaled x{cfg.n_chunks // sample_chunks}), "
-                   f"power iteration, paper-tolerance rAPDHG on {sample_cols} of "
+                   f"block-{SPECTRAL_BLOCK} subspace iteration, paper-tolerance rAPDHG on {sample_cols} of "
                    f"{cfg.n_cols} columns (time scaled x{cfg.n_cols // sample_cols}; "
                    f"max {int(r.iters.max())} iterations); measured "
                    f"{t_hess + t_pow + t_solve:.1f} s of CPU work"),
@@ -133,13 +137,13 @@ def main() -> int:
     X = workloads.x_all(cfg)
     W0 = workloads.w0(cfg)
     mask = workloads.layer_mask(cfg, W0, workloads.col_sq_norms(cfg, X))
-    v0 = workloads.power_start(cfg.d)
+    V0 = workloads.power_start_block(cfg.d, SPECTRAL_BLOCK)
     log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
 
     Xd = torch.from_numpy(X.view(np.int16)).view(torch.bfloat16).to(dev)
     W0d = torch.from_numpy(W0).to(dev)
     Md = torch.from_numpy(mask).to(dev)
-    v0d = torch.from_numpy(v0).to(dev)
+    V0d = torch.from_numpy(V0).to(dev)
     d, C, N = cfg.d, cfg.n_cols, cfg.n_tok
     H = torch.empty((d, d), dtype=torch.float32, device=dev)
     lam = torch.empty(1, dtype=torch.float32, device=dev)
@@ -147,7 +151,8 @@ def main() -> int:
     Wout = torch.empty_like(W0d)
     hws = torch.empty(L.optima_hessian_workspace_bytes(N, d, L.DTYPE_BF16), dtype=torch.uint8,
                       device=dev)
-    sws = torch.empty(L.optima_spectral_norm_workspace_bytes(d), dtype=torch.uint8, device=dev)
+    sws = torch.empty(L.optima_spectral_norm_workspace_bytes(d, SPECTRAL_BLOCK),
+                      dtype=torch.uint8, device=dev)
     qws = torch.empty(L.optima_qp_workspace_bytes(d, C), dtype=torch.uint8, device=dev)
     iters = torch.zeros(C, dtype=torch.int32, device=dev)
     conv = torch.zeros(C, dtype=torch.uint8, device=dev)
@@ -166,7 +171,7 @@ def main() -> int:
         L.optima_hessian_accumulate(Xd, H, accumulate=False, ws=hws)
         ev[1].record()
         L.optima_hessian_damp(H, cfg.rel_damp, lam)
-        L.optima_spectral_norm(H, v0d, lmax, max_iters=1000, tol=1e-6, ws=sws)
+        L.optima_spectral_norm(H, V0d, lmax, max_iters=1000, tol=1e-6, ws=sws)
         ev[2].record()
         info = L.optima_qp_solve_batched(H, lmax, W0d, Md, Wout, opts=opts, ws=qws,
                                          stats={"iters": iters, "converged": conv})

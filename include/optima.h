@@ -100,18 +100,34 @@ optima_status optima_hessian_damp(float* H, int64_t d, float rel_damp,
 /* ---------------------------------------------------------------------------
  * Spectral norm of H for the solver's step size (Section 3.3: the first-order
  * method's bottleneck is products with H; its step needs ||Q|| = 2 lambda_max).
- * Power iteration from the caller's start vector v0[d] (device, not modified):
- * iteration i forms y = H v with v of unit length, rho_i = v^T y and
- * v <- y / ||y||, stopping once |rho_i - rho_{i-1}| <= tol * rho_i or after
- * max_iters iterations. lambda_max (device, one float) receives the last rho;
- * iters (device int32, may be NULL) the iteration count. H must be symmetric
- * and 16-byte aligned. Blocking: the call synchronises `stream` a few times to
- * test convergence. ws: optima_spectral_norm_workspace_bytes(d) bytes.
+ * H must be symmetric positive semi-definite (X^T X + lambda I is), [d][d]
+ * fp32, 4-byte aligned (16-byte alignment and d % 4 == 0 enable vector loads).
+ *
+ * V0: [block][d] fp32 device array of start vectors (row a is vector a), not
+ * modified; 1 <= block <= OPTIMA_SPECTRAL_MAX_BLOCK.
+ *   block == 1: power iteration. Iteration i forms y = H v with v of unit
+ *     length, rho_i = v^T y and v <- y / ||y||.
+ *   block >= 2: subspace (orthogonal) iteration with Rayleigh-Ritz.
+ *     Iteration i multiplies an orthonormal basis Q of the current block by
+ *     H (Y = H Q, one pass over H) and takes rho_i = the largest Ritz value
+ *     of span(Q), i.e. the largest eigenvalue of Q^T H Q; the next basis spans
+ *     Y (Cholesky QR in fp64). Convergence goes as lambda_{block+1} /
+ *     lambda_1 instead of lambda_2 / lambda_1, so Hessians whose top
+ *     eigenvalues cluster (outlier channels) need a handful of passes. The
+ *     b x b eigenvalue is found by repeated squaring, within 1e-8 relative.
+ *     Directions that become numerically dependent (Cholesky pivot below
+ *     1e-14 of the diagonal) are dropped.
+ * Both stop once |rho_i - rho_{i-1}| <= tol * rho_i, or after max_iters
+ * iterations. lambda_max (device, one float) receives the last rho (NaN if H
+ * holds NaN/Inf and block >= 2); iters (device int32, may be NULL) the
+ * iteration count. Blocking: the call synchronises `stream` a few times to
+ * test convergence. ws: optima_spectral_norm_workspace_bytes(d, block) bytes.
  * ------------------------------------------------------------------------- */
-size_t optima_spectral_norm_workspace_bytes(int64_t d);
-optima_status optima_spectral_norm(const float* H, int64_t d, const float* v0,
-                                   int max_iters, float tol, void* ws,
-                                   size_t ws_bytes, float* lambda_max,
+#define OPTIMA_SPECTRAL_MAX_BLOCK 16
+size_t optima_spectral_norm_workspace_bytes(int64_t d, int block);
+optima_status optima_spectral_norm(const float* H, int64_t d, const float* V0,
+                                   int block, int max_iters, float tol,
+                                   void* ws, size_t ws_bytes, float* lambda_max,
                                    int32_t* iters, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------

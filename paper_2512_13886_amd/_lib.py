@@ -75,9 +75,9 @@ _hess_ws = _sig("optima_hessian_workspace_bytes", _sz, [_i64, _i64, _i32])
 _hess_acc = _sig("optima_hessian_accumulate", _i32,
                  [_vp, _i32, _i64, _i64, _vp, _i32, _vp, _sz, _vp])
 _damp = _sig("optima_hessian_damp", _i32, [_vp, _i64, _f32, _vp, _vp])
-_spec_ws = _sig("optima_spectral_norm_workspace_bytes", _sz, [_i64])
+_spec_ws = _sig("optima_spectral_norm_workspace_bytes", _sz, [_i64, _i32])
 _spec = _sig("optima_spectral_norm", _i32,
-             [_vp, _i64, _vp, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
+             [_vp, _i64, _vp, _i32, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
 _opts_default = _sig("optima_solver_opts_default", None, [ctypes.POINTER(_Opts)])
 _qp_ws = _sig("optima_qp_workspace_bytes", _sz, [_i64, _i64])
 _qp_solve = _sig("optima_qp_solve_batched", _i32,
@@ -186,22 +186,35 @@ def optima_hessian_damp(H: torch.Tensor, rel_damp: float, lambda_out: torch.Tens
     _check(_damp(_ptr(H), H.shape[0], float(rel_damp), _ptr(lambda_out), _stream(stream)))
 
 
-def optima_spectral_norm_workspace_bytes(d: int) -> int:
-    return int(_spec_ws(d))
+SPECTRAL_MAX_BLOCK = 16
 
 
-def optima_spectral_norm(H: torch.Tensor, v0: torch.Tensor, lambda_max: torch.Tensor,
+def optima_spectral_norm_workspace_bytes(d: int, block: int = 1) -> int:
+    return int(_spec_ws(d, block))
+
+
+def optima_spectral_norm(H: torch.Tensor, V0: torch.Tensor, lambda_max: torch.Tensor,
                          max_iters: int = 1000, tol: float = 1e-6,
                          ws: torch.Tensor | None = None, iters: torch.Tensor | None = None,
                          stream=None) -> None:
+    """lambda_max(H). V0 is one start vector [d] (power iteration) or a block
+    of start vectors [block, d] (subspace iteration with Rayleigh-Ritz)."""
     _need_cuda("H", H, torch.float32)
-    _need_cuda("v0", v0, torch.float32)
+    _need_cuda("V0", V0, torch.float32)
     _need_cuda("lambda_max", lambda_max, torch.float32)
     if iters is not None:
         _need_cuda("iters", iters, torch.int32)
     d = H.shape[0]
-    ws, nbytes = _workspace(optima_spectral_norm_workspace_bytes(d), ws, H.device)
-    _check(_spec(_ptr(H), d, _ptr(v0), int(max_iters), float(tol), _ptr(ws), nbytes,
+    if V0.dim() == 1:
+        block = 1
+    elif V0.dim() == 2:
+        block = V0.shape[0]
+    else:
+        raise ValueError("V0 must be [d] or [block, d]")
+    if V0.shape[-1] != d:
+        raise ValueError("V0 vectors must have length d")
+    ws, nbytes = _workspace(optima_spectral_norm_workspace_bytes(d, block), ws, H.device)
+    _check(_spec(_ptr(H), d, _ptr(V0), int(block), int(max_iters), float(tol), _ptr(ws), nbytes,
                  _ptr(lambda_max), _ptr(iters), _stream(stream)))
 
 

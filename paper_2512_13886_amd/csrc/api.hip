@@ -7,9 +7,10 @@ size_t hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype);
 optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_t d, float* H,
                                  int accumulate, void* ws, hipStream_t s);
 optima_status hessian_damp(float* H, int64_t d, float rel, float* lambda_out, hipStream_t s);
-size_t spectral_norm_workspace_bytes(int64_t d);
-optima_status spectral_norm(const float* H, int64_t d, const float* v0, int max_iters, float tol,
-                            void* ws, float* lambda_max, int32_t* iters, hipStream_t s);
+size_t spectral_norm_workspace_bytes(int64_t d, int block);
+optima_status spectral_norm(const float* H, int64_t d, const float* V0, int block, int max_iters,
+                            float tol, void* ws, float* lambda_max, int32_t* iters,
+                            hipStream_t s);
 size_t qp_workspace_bytes(int64_t d, int64_t n_cols);
 optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const float* W0,
                        const uint8_t* mask, int64_t n_cols, const optima_solver_opts& o, void* ws,
@@ -42,7 +43,7 @@ const char* optima_status_string(optima_status status) {
   }
 }
 
-int optima_abi_version(void) { return 2; }
+int optima_abi_version(void) { return 3; }
 
 size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
   if (n_tok < 0 || d < 1 || d > kMaxDim) return 0;
@@ -74,18 +75,22 @@ optima_status optima_hessian_damp(float* H, int64_t d, float rel_damp, float* la
   return optima::hessian_damp(H, d, rel_damp, lambda_out, stream);
 }
 
-size_t optima_spectral_norm_workspace_bytes(int64_t d) {
-  if (d < 1 || d > kMaxDim) return 0;
-  return optima::spectral_norm_workspace_bytes(d);
+size_t optima_spectral_norm_workspace_bytes(int64_t d, int block) {
+  if (d < 1 || d > kMaxDim || block < 1 || block > OPTIMA_SPECTRAL_MAX_BLOCK) return 0;
+  return optima::spectral_norm_workspace_bytes(d, block);
 }
 
-optima_status optima_spectral_norm(const float* H, int64_t d, const float* v0, int max_iters,
-                                   float tol, void* ws, size_t ws_bytes, float* lambda_max,
-                                   int32_t* iters, hipStream_t stream) {
-  if (!H || !v0 || !lambda_max || d < 1 || d > kMaxDim || max_iters < 1 || !(tol >= 0.f))
+optima_status optima_spectral_norm(const float* H, int64_t d, const float* V0, int block,
+                                   int max_iters, float tol, void* ws, size_t ws_bytes,
+                                   float* lambda_max, int32_t* iters, hipStream_t stream) {
+  if (!H || !V0 || !lambda_max || d < 1 || d > kMaxDim || max_iters < 1 || !(tol >= 0.f))
     return OPTIMA_E_INVAL;
-  if (!ws || ws_bytes < optima::spectral_norm_workspace_bytes(d)) return OPTIMA_E_WORKSPACE;
-  return optima::spectral_norm(H, d, v0, max_iters, tol, ws, lambda_max, iters, stream);
+  if (block < 1 || block > OPTIMA_SPECTRAL_MAX_BLOCK) return OPTIMA_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(V0) & 3) || (reinterpret_cast<uintptr_t>(H) & 3))
+    return OPTIMA_E_INVAL;
+  if (!ws || ws_bytes < optima::spectral_norm_workspace_bytes(d, block))
+    return OPTIMA_E_WORKSPACE;
+  return optima::spectral_norm(H, d, V0, block, max_iters, tol, ws, lambda_max, iters, stream);
 }
 
 void optima_solver_opts_default(optima_solver_opts* o) {

@@ -1,7 +1,27 @@
-// Largest eigenvalue of the damped Hessian by power iteration; it sets the
-// solver's step constant L = 2 lambda_max (1 + safety). Each iteration is one
-// HBM-bound pass over H (a GEMV with one wave per row, 16-byte loads) and a
-// one-workgroup pass that forms the Rayleigh quotient and the next norm.
+// Largest eigenvalue of the damped Hessian; it sets the solver's step constant
+// L = 2 lambda_max (1 + safety).
+//
+// block == 1: power iteration. Each iteration is one HBM-bound pass over H (a
+// GEMV with one wave per row, 16-byte loads); the next launch reduces the
+// Rayleigh quotient and the norm.
+//
+// block = b in [2, 16]: subspace iteration with Rayleigh-Ritz. With Y_{i-1}
+// the previous block (b vectors, fp32) and R_{i-1} the Cholesky factor of its
+// Gram matrix (Y_{i-1}^T Y_{i-1} = R^T R, so Q_i = Y_{i-1} R^-1 is an
+// orthonormal basis of its span), pass i computes
+//     Y_i = (H Y_{i-1}) R_{i-1}^-1  (= H Q_i)
+// on v_mfma_f32_16x16x4_f32 in one read of H, and per workgroup the fp64
+// partial sums over its rows of G = Y_i^T Y_i, T = Q_i^T Y_i and
+// S = Q_i^T Q_i. A one-workgroup finish sums the partials in a fixed order
+// and forms the Ritz values of span(Q_i) as the eigenvalues of
+// L_S^-1 T L_S^-T (S = L_S L_S^T; exact even if Q_i is not quite
+// orthonormal). The largest one comes from repeated squaring of that b x b
+// matrix: after m squarings (trace-normalised) M is proportional to C^(2^m),
+// and trace(C M) / trace(M) is within (b - 1) / (e 2^m) relative of
+// lambda_max(C) for positive semi-definite C. The finish then factors G for
+// the next pass. Directions whose Cholesky pivot falls below 1e-14 of their
+// diagonal are numerically dependent and are dropped (their rows and columns
+// of the factor's inverse are zero).
 #include "common.h"
 
 namespace optima {
@@ -170,19 +190,314 @@ __global__ void __launch_bounds__(1024) k_power_init(const float* v0, int64_t d,
 
 __global__ void k_copy_iters(const PowState* st, int32_t* iters) { *iters = st->iters; }
 
+// ---------------------------------------------------------------------------
+// Subspace iteration (block >= 2)
+// ---------------------------------------------------------------------------
+
+constexpr int kMaxBlock = 16;
+constexpr int kSubRows = 32;                 // rows of H per workgroup
+constexpr int kSubThreads = 512;             // 8 waves: 2 row blocks x 4 slices of K
+constexpr int kGram = kMaxBlock * kMaxBlock;
+constexpr int kPart = 3 * kGram;             // G, T, S partials per workgroup
+constexpr int kSquarings = 32;
+constexpr double kDropRel = 1e-14;
+constexpr int kPitch = kMaxBlock + 1;
+
+struct SubState {
+  double theta;  // largest Ritz value of the last pass
+  int conv;
+  int iters;
+};
+
+// Lower Cholesky factor L (A = L L^T) of the leading b x b block of A, which
+// is overwritten. Run by all threads of a 256-thread workgroup; thread t owns
+// entry (t / 16, t % 16). A pivot not above kDropRel times the column's
+// original diagonal (or NaN) drops the direction: its column of L stays 0.
+__device__ void chol_drop(double (*A)[kPitch], double (*L)[kPitch], double* diag0, int b) {
+  const int t = threadIdx.x, i = t >> 4, k = t & 15;
+  if (t < kMaxBlock) diag0[t] = A[t][t];
+  L[i][k] = 0.0;
+  __syncthreads();
+  for (int j = 0; j < b; ++j) {
+    const double p = A[j][j];
+    const bool keep = p > kDropRel * diag0[j];
+    if (keep && k == j && i >= j && i < b) L[i][j] = i == j ? sqrt(p) : A[i][j] / sqrt(p);
+    __syncthreads();
+    if (keep && i > j && k > j && i < b && k < b) A[i][k] -= L[i][j] * L[k][j];
+    __syncthreads();
+  }
+}
+
+// X = L^-1 for a lower-triangular L whose zero diagonal entries mark dropped
+// directions (their rows and columns of X are 0). Thread c < b owns column c.
+__device__ void inv_lower(double (*L)[kPitch], double (*X)[kPitch], int b) {
+  const int t = threadIdx.x;
+  X[t >> 4][t & 15] = 0.0;
+  __syncthreads();
+  if (t < b) {
+    const int c = t;
+    for (int i = c; i < b; ++i) {
+      if (L[i][i] == 0.0) continue;
+      double s = i == c ? 1.0 : 0.0;
+      for (int k = c; k < i; ++k) s -= L[i][k] * X[k][c];
+      X[i][c] = s / L[i][i];
+    }
+  }
+  __syncthreads();
+}
+
+// Pass i >= 1 (see the file comment); workgroup blk covers rows
+// [32 blk, 32 blk + 32) of the padded row range [0, dpp).
+template <bool VEC4>
+__global__ void __launch_bounds__(kSubThreads) k_subspace_pass(const float* H, int64_t d,
+                                                               int64_t dpp, const float* Yprev,
+                                                               float* Ycur, const double* Rinv,
+                                                               double* part, SubState* st) {
+  if (st->conv) return;
+  __shared__ float red[kSubThreads / 64][256];
+  __shared__ double Rs[kGram];
+  __shared__ double Zs[kSubRows][kPitch], Ys[kSubRows][kPitch], Qs[kSubRows][kPitch];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int rb = w & 1, ks = w >> 1;
+  const int64_t r0 = int64_t(blockIdx.x) * kSubRows;
+  for (int i = tid; i < kGram; i += kSubThreads) Rs[i] = Rinv[i];
+
+  // Z = H Y_{i-1}^T for this workgroup's rows. MFMA lane l supplies row
+  // (l % 16) of H and vector (l % 16) of Y at contraction indices
+  // 16 c + 4 (l / 16) + {0..3}: four MFMAs per 16-wide chunk c of K, each
+  // fed by one 16-byte load per operand.
+  const int64_t row = r0 + rb * 16 + (lane & 15);
+  const bool row_ok = row < d;
+  const float* hrow = H + (row_ok ? row : 0) * d;
+  const float* yrow = Yprev + int64_t(lane & 15) * dpp + 4 * (lane >> 4);
+  const int kq = 4 * (lane >> 4);
+  const int64_t nch = dpp / 16;
+  f4 acc = {0.f, 0.f, 0.f, 0.f};
+  auto load_a = [&](int64_t c) {
+    const int64_t k = c * 16 + kq;
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (VEC4) {
+      if (row_ok && k < d) a = *reinterpret_cast<const float4*>(hrow + k);
+    } else if (row_ok) {
+      if (k < d) a.x = hrow[k];
+      if (k + 1 < d) a.y = hrow[k + 1];
+      if (k + 2 < d) a.z = hrow[k + 2];
+      if (k + 3 < d) a.w = hrow[k + 3];
+    }
+    return a;
+  };
+  auto mfma4 = [&](float4 a, float4 y) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, y.x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, y.y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, y.z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, y.w, acc, 0, 0, 0);
+  };
+  int64_t c = ks;
+  for (; c + 12 < nch; c += 16) {
+    const float4 a0 = load_a(c), a1 = load_a(c + 4), a2 = load_a(c + 8), a3 = load_a(c + 12);
+    const float4 y0 = *reinterpret_cast<const float4*>(yrow + c * 16);
+    const float4 y1 = *reinterpret_cast<const float4*>(yrow + (c + 4) * 16);
+    const float4 y2 = *reinterpret_cast<const float4*>(yrow + (c + 8) * 16);
+    const float4 y3 = *reinterpret_cast<const float4*>(yrow + (c + 12) * 16);
+    mfma4(a0, y0);
+    mfma4(a1, y1);
+    mfma4(a2, y2);
+    mfma4(a3, y3);
+  }
+  for (; c < nch; c += 4) mfma4(load_a(c), *reinterpret_cast<const float4*>(yrow + c * 16));
+#pragma unroll
+  for (int e = 0; e < 4; ++e) red[w][e * 64 + lane] = acc[e];
+  __syncthreads();
+  // Sum the four K slices in a fixed order. MFMA output (lane, e) is row
+  // 4 (lane / 16) + e, vector lane % 16 of the 16 x 16 tile.
+  {
+    const int b2 = tid >> 8, within = tid & 255, ln = within & 63, e = within >> 6;
+    double z = 0.0;
+    for (int q = 0; q < 4; ++q) z += double(red[b2 + 2 * q][e * 64 + ln]);
+    Zs[b2 * 16 + 4 * (ln >> 4) + e][ln & 15] = z;
+  }
+  __syncthreads();
+  // Y_i = Z R^-1 (stored in fp32), Q_i = Y_{i-1} R^-1 for these rows.
+  {
+    const int r = tid >> 4, a = tid & 15;
+    double yn = 0.0, q = 0.0;
+    for (int k = 0; k < kMaxBlock; ++k) {
+      yn += Zs[r][k] * Rs[k * kMaxBlock + a];
+      q += double(Yprev[int64_t(k) * dpp + r0 + r]) * Rs[k * kMaxBlock + a];
+    }
+    const float yf = float(yn);
+    Ycur[int64_t(a) * dpp + r0 + r] = yf;
+    Ys[r][a] = double(yf);
+    Qs[r][a] = q;
+  }
+  __syncthreads();
+  if (tid < kGram) {
+    const int a = tid >> 4, b2 = tid & 15;
+    double g = 0.0, tt = 0.0, ss = 0.0;
+    for (int r = 0; r < kSubRows; ++r) {
+      g += Ys[r][a] * Ys[r][b2];
+      tt += Qs[r][a] * Ys[r][b2];
+      ss += Qs[r][a] * Qs[r][b2];
+    }
+    double* P = part + size_t(blockIdx.x) * kPart;
+    P[tid] = g;
+    P[kGram + tid] = tt;
+    P[2 * kGram + tid] = ss;
+  }
+}
+
+// Y_0 = the caller's start vectors (zero-padded to 16 x dpp) and the partial
+// Gram sums of Y_0 over this workgroup's rows.
+__global__ void __launch_bounds__(kSubThreads) k_subspace_init(const float* V0, int b, int64_t d,
+                                                               int64_t dpp, float* Y0,
+                                                               double* part, SubState* st) {
+  __shared__ double Ys[kSubRows][kPitch];
+  const int tid = threadIdx.x, r = tid >> 4, a = tid & 15;
+  const int64_t row = int64_t(blockIdx.x) * kSubRows + r;
+  const float v = (a < b && row < d) ? V0[int64_t(a) * d + row] : 0.f;
+  Y0[int64_t(a) * dpp + row] = v;
+  Ys[r][a] = double(v);
+  if (blockIdx.x == 0 && tid == 0) {
+    st->theta = 0.0;
+    st->conv = 0;
+    st->iters = 0;
+  }
+  __syncthreads();
+  if (tid < kGram) {
+    const int i = tid >> 4, j = tid & 15;
+    double g = 0.0;
+    for (int q = 0; q < kSubRows; ++q) g += Ys[q][i] * Ys[q][j];
+    double* P = part + size_t(blockIdx.x) * kPart;
+    P[tid] = g;
+    P[kGram + tid] = 0.0;
+    P[2 * kGram + tid] = 0.0;
+  }
+}
+
+// Finish of pass `it` (0: the start block only). One workgroup of 256.
+__global__ void __launch_bounds__(256) k_subspace_finish(const double* part, int nblk, int b,
+                                                         int it, float tol, double* Rinv,
+                                                         SubState* st, float* lambda_out) {
+  if (st->conv) return;
+  __shared__ double G[kMaxBlock][kPitch], T[kMaxBlock][kPitch], S[kMaxBlock][kPitch];
+  __shared__ double L[kMaxBlock][kPitch], X[kMaxBlock][kPitch], W[kMaxBlock][kPitch];
+  __shared__ double M[kMaxBlock][kPitch];
+  __shared__ double diag0[kMaxBlock], rowsum[kMaxBlock];
+  __shared__ int bad;
+  const int t = threadIdx.x, i = t >> 4, j = t & 15;
+  if (t == 0) bad = 0;
+  __syncthreads();
+  {
+    double g = 0.0, tt = 0.0, ss = 0.0;
+    for (int k = 0; k < nblk; ++k) {
+      const double* P = part + size_t(k) * kPart;
+      g += P[t];
+      tt += P[kGram + t];
+      ss += P[2 * kGram + t];
+    }
+    G[i][j] = g;
+    T[i][j] = tt;
+    S[i][j] = ss;
+    if (!isfinite(g) || !isfinite(tt) || !isfinite(ss)) bad = 1;
+  }
+  __syncthreads();
+  if (bad) {
+    if (t == 0) {
+      *lambda_out = __builtin_nanf("");
+      st->iters = it;
+      st->conv = 1;
+    }
+    return;
+  }
+  if (it >= 1) {
+    // C = L_S^-1 T L_S^-T, symmetrised.
+    chol_drop(S, L, diag0, b);
+    inv_lower(L, X, b);
+    double w = 0.0;
+    for (int k = 0; k < kMaxBlock; ++k) w += X[i][k] * T[k][j];
+    W[i][j] = w;
+    __syncthreads();
+    double cij = 0.0, cji = 0.0;
+    for (int k = 0; k < kMaxBlock; ++k) {
+      cij += W[i][k] * X[j][k];
+      cji += W[j][k] * X[i][k];
+    }
+    const double cs = 0.5 * (cij + cji);
+    __syncthreads();
+    T[i][j] = cs;  // T now holds C
+    __syncthreads();
+    double tr = 0.0;
+    for (int k = 0; k < kMaxBlock; ++k) tr += T[k][k];
+    double theta = 0.0;
+    if (tr > 0.0) {
+      M[i][j] = cs / tr;
+      __syncthreads();
+      for (int q = 0; q < kSquarings; ++q) {
+        double m2 = 0.0;
+        for (int k = 0; k < kMaxBlock; ++k) m2 += M[i][k] * M[k][j];
+        W[i][j] = m2;
+        __syncthreads();
+        double tr2 = 0.0;
+        for (int k = 0; k < kMaxBlock; ++k) tr2 += W[k][k];
+        M[i][j] = m2 / tr2;
+        __syncthreads();
+      }
+      if (t < kMaxBlock) {
+        double rs = 0.0;
+        for (int k = 0; k < kMaxBlock; ++k) rs += T[t][k] * M[t][k];
+        rowsum[t] = rs;
+      }
+      __syncthreads();
+      double num = 0.0, den = 0.0;
+      for (int k = 0; k < kMaxBlock; ++k) {
+        num += rowsum[k];
+        den += M[k][k];
+      }
+      theta = num / den;
+    }
+    const bool done = theta == 0.0 ||
+                      (it >= 2 && fabs(theta - st->theta) <= double(tol) * fabs(theta));
+    __syncthreads();
+    if (t == 0) {
+      st->theta = theta;
+      st->iters = it;
+      *lambda_out = float(theta);
+      if (done) st->conv = 1;
+    }
+    if (done) return;
+  }
+  // Factor of the next pass: G = R^T R with R = L_G^T, so R^-1 = (L_G^-1)^T.
+  chol_drop(G, L, diag0, b);
+  inv_lower(L, X, b);
+  Rinv[i * kMaxBlock + j] = X[j][i];
+}
+
+__global__ void k_copy_sub_iters(const SubState* st, int32_t* iters) { *iters = st->iters; }
+
 }  // namespace
 
-size_t spectral_norm_workspace_bytes(int64_t d) {
+size_t spectral_norm_workspace_bytes(int64_t d, int block) {
   Carver c(nullptr);
-  c.take<float>(size_t(d));
-  c.take<float>(size_t(d));
-  c.take<double2>(2 * size_t(ceil_div(d, kRowsPerBlock)));
-  c.take<PowState>(1);
+  if (block == 1) {
+    c.take<float>(size_t(d));
+    c.take<float>(size_t(d));
+    c.take<double2>(2 * size_t(ceil_div(d, kRowsPerBlock)));
+    c.take<PowState>(1);
+  } else {
+    const int64_t dpp = round_up(d, kSubRows);
+    c.take<float>(size_t(kMaxBlock) * size_t(dpp));
+    c.take<float>(size_t(kMaxBlock) * size_t(dpp));
+    c.take<double>(size_t(dpp / kSubRows) * kPart);
+    c.take<double>(kGram);
+    c.take<SubState>(1);
+  }
   return c.bytes();
 }
 
-optima_status spectral_norm(const float* H, int64_t d, const float* v0, int max_iters, float tol,
-                            void* ws, float* lambda_max, int32_t* iters, hipStream_t s) {
+namespace {
+
+optima_status power_iteration(const float* H, int64_t d, const float* v0, int max_iters, float tol,
+                              void* ws, float* lambda_max, int32_t* iters, hipStream_t s) {
   Carver c(ws);
   float* buf[2] = {c.take<float>(size_t(d)), c.take<float>(size_t(d))};
   const int nblk = int(ceil_div(d, kRowsPerBlock));
@@ -220,6 +535,60 @@ optima_status spectral_norm(const float* H, int64_t d, const float* v0, int max_
   }
   OPTIMA_HIP_TRY(hipStreamSynchronize(s));
   return OPTIMA_OK;
+}
+
+optima_status subspace_iteration(const float* H, int64_t d, const float* V0, int b,
+                                 int max_iters, float tol, void* ws, float* lambda_max,
+                                 int32_t* iters, hipStream_t s) {
+  const int64_t dpp = round_up(d, kSubRows);
+  const int nblk = int(dpp / kSubRows);
+  Carver c(ws);
+  float* Y[2] = {c.take<float>(size_t(kMaxBlock) * size_t(dpp)),
+                 c.take<float>(size_t(kMaxBlock) * size_t(dpp))};
+  double* part = c.take<double>(size_t(nblk) * kPart);
+  double* Rinv = c.take<double>(kGram);
+  SubState* st = c.take<SubState>(1);
+  hipLaunchKernelGGL(k_subspace_init, dim3(unsigned(nblk)), dim3(kSubThreads), 0, s, V0, b, d,
+                     dpp, Y[0], part, st);
+  OPTIMA_LAUNCH_CHECK();
+  hipLaunchKernelGGL(k_subspace_finish, dim3(1), dim3(256), 0, s, part, nblk, b, 0, tol, Rinv,
+                     st, lambda_max);
+  OPTIMA_LAUNCH_CHECK();
+  const bool vec4 = (d % 4) == 0 && aligned16(H);
+  constexpr int kPoll = 4;
+  for (int it = 1; it <= max_iters; ++it) {
+    if (vec4)
+      hipLaunchKernelGGL(k_subspace_pass<true>, dim3(unsigned(nblk)), dim3(kSubThreads), 0, s, H,
+                         d, dpp, Y[(it - 1) & 1], Y[it & 1], Rinv, part, st);
+    else
+      hipLaunchKernelGGL(k_subspace_pass<false>, dim3(unsigned(nblk)), dim3(kSubThreads), 0, s, H,
+                         d, dpp, Y[(it - 1) & 1], Y[it & 1], Rinv, part, st);
+    OPTIMA_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_subspace_finish, dim3(1), dim3(256), 0, s, part, nblk, b, it, tol, Rinv,
+                       st, lambda_max);
+    OPTIMA_LAUNCH_CHECK();
+    if (it % kPoll == 0 && it < max_iters) {
+      int conv = 0;
+      OPTIMA_HIP_TRY(hipMemcpyAsync(&conv, &st->conv, sizeof(int), hipMemcpyDeviceToHost, s));
+      OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+      if (conv) break;
+    }
+  }
+  if (iters) {
+    hipLaunchKernelGGL(k_copy_sub_iters, dim3(1), dim3(1), 0, s, st, iters);
+    OPTIMA_LAUNCH_CHECK();
+  }
+  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  return OPTIMA_OK;
+}
+
+}  // namespace
+
+optima_status spectral_norm(const float* H, int64_t d, const float* V0, int block, int max_iters,
+                            float tol, void* ws, float* lambda_max, int32_t* iters,
+                            hipStream_t s) {
+  if (block == 1) return power_iteration(H, d, V0, max_iters, tol, ws, lambda_max, iters, s);
+  return subspace_iteration(H, d, V0, block, max_iters, tol, ws, lambda_max, iters, s);
 }
 
 }  // namespace optima

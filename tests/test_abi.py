@@ -65,6 +65,10 @@ def test_workspace_queries():
     assert h >= 4096 * 65536 * 2
     assert L.optima_hessian_workspace_bytes(10, 4096, 7) == 0
     assert L.optima_spectral_norm_workspace_bytes(4096) >= 2 * 4096 * 4
+    assert L.optima_spectral_norm_workspace_bytes(4096, 16) >= 2 * 16 * 4096 * 4
+    assert L.optima_spectral_norm_workspace_bytes(4096, 17) == 0
+    assert L.optima_spectral_norm_workspace_bytes(4096, 0) == 0
+    assert L.SPECTRAL_MAX_BLOCK == 16
 
 
 def test_validation_returns_before_launch(lib):
@@ -81,5 +85,9 @@ def test_validation_returns_before_launch(lib):
     assert q(None, 8, None, None, None, 4, None, None, 0, None, None, None, None) == -1
     g = lib.optima_spectral_norm
     g.restype = ctypes.c_int
-    g.argtypes = [vp, i64, vp, ctypes.c_int, ctypes.c_float, vp, ctypes.c_size_t, vp, vp, vp]
-    assert g(vp(256), 8, vp(512), 0, 1e-6, None, 0, vp(1024), None, None) == -1  # max_iters
+    g.argtypes = [vp, i64, vp, ctypes.c_int, ctypes.c_int, ctypes.c_float, vp, ctypes.c_size_t,
+                  vp, vp, vp]
+    assert g(vp(256), 8, vp(512), 1, 0, 1e-6, None, 0, vp(1024), None, None) == -1  # max_iters
+    assert g(vp(256), 8, vp(512), 0, 10, 1e-6, None, 0, vp(1024), None, None) == -1  # block
+    assert g(vp(256), 8, vp(512), 17, 10, 1e-6, None, 0, vp(1024), None, None) == -1
+    assert g(vp(256), 8, vp(512), 4, 10, 1e-6, None, 0, vp(1024), None, None) == -4  # ws

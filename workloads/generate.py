@@ -188,6 +188,18 @@ def power_start(d: int, seed: int = 0) -> np.ndarray:
     return rng.standard_normal(d).astype(np.float32)
 
 
+def power_start_block(d: int, block: int, seed: int = 0) -> np.ndarray:
+    """Start vectors of the subspace iteration, shape (block, d), fp32.
+
+    Row 0 is power_start(d, seed); row j > 0 is drawn from its own stream.
+    """
+    rows = [power_start(d, seed)]
+    for j in range(1, block):
+        rng = np.random.default_rng(np.random.SeedSequence([seed, TENSOR_V0, d, j]))
+        rows.append(rng.standard_normal(d).astype(np.float32))
+    return np.stack(rows)
+
+
 def layer_inputs(cfg: LayerConfig, threads: int | None = None) -> dict:
     """X (storage form), W0, column square norms and mask for one layer."""
     from .masks import layer_mask
