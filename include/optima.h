@@ -53,8 +53,9 @@ typedef int optima_status;
  * BF16X3: every fp32 operand v is split into bf16 planes hi = rne(v),
  *   lo = rne(v - hi), and a*b is formed as hi*hi + hi*lo + lo*hi on
  *   v_mfma_f32_16x16x32_bf16 with fp32 accumulation; the dropped terms are
- *   below 3 * 2^-16 |a b| per product. The two setup products (H w0, H x0)
- *   always use FP32. BF16X3 is the default: on the 4096-wide outlier layer its
+ *   below 3 * 2^-16 |a b| per product. The precision applies to every
+ *   product of a solve, the setup products H w0 and H x0 included. BF16X3 is
+ *   the default: on the 4096-wide outlier layer its
  *   solutions differ from FP32's by under 1e-5 relative (Frobenius) and it
  *   runs the iteration about 2.5x faster. */
 #define OPTIMA_PREC_FP32 0
@@ -76,9 +77,11 @@ int optima_abi_version(void);
  * formed exactly and summed in fp32. Both triangles of H are written and the
  * result is exactly symmetric; with accumulate = 1 the lower triangle of the
  * incoming H is read and taken as the whole matrix. n_tok = 0 leaves H as it is
- * (accumulate = 1) or zeroes it. X must be 16-byte aligned; H may alias nothing
- * else. ws must hold optima_hessian_workspace_bytes(n_tok, d, dtype) bytes
- * (token-slab transpose buffer and split-K partial sums).
+ * (accumulate = 1) or zeroes it. X must be 16-byte aligned (OPTIMA_E_INVAL
+ * otherwise); H may alias nothing else. ws must hold
+ * optima_hessian_workspace_bytes(n_tok, d, dtype) bytes: split-K partial sums,
+ * plus a token-slab transpose buffer unless X is bf16 with d % 256 == 0 (then
+ * token rows are read in place and only a 64-row tail buffer is needed).
  * ------------------------------------------------------------------------- */
 size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype);
 optima_status optima_hessian_accumulate(const void* X, int dtype, int64_t n_tok,

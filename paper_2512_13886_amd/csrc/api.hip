@@ -58,7 +58,7 @@ optima_status optima_hessian_accumulate(const void* X, int dtype, int64_t n_tok,
   if (!H || n_tok < 0 || d < 1 || d > kMaxDim) return OPTIMA_E_INVAL;
   if (n_tok > 0 && !X) return OPTIMA_E_INVAL;
   const size_t esz = dtype == OPTIMA_DTYPE_BF16 ? 2 : 4;
-  if (X && (reinterpret_cast<uintptr_t>(X) % esz)) return OPTIMA_E_INVAL;
+  if (n_tok > 0 && !optima::aligned16(X)) return OPTIMA_E_INVAL;
   if (X && overlaps(X, size_t(n_tok) * size_t(d) * esz, H, size_t(d) * size_t(d) * 4))
     return OPTIMA_E_INVAL;
   if (n_tok > 0) {

@@ -4,22 +4,25 @@
 // contractions: the batched H-product Y[b][n] = sum_k Z[b][k] H[n][k] (H is
 // symmetric) and the Hessian block H[i][j] = sum_t XT[i][t] XT[j][t].
 //
-// Work split: 256 threads = 4 waves in a 2x2 grid, each wave owning a 64x64
-// sub-tile as 4x4 blocks of 16x16 MFMA outputs (16 accumulators of 4 floats).
-// K advances in stages of 128 bytes per row (32 fp32 or 64 bf16 values).
+// Work split: WGM x WGN waves, each owning a (BM / WGM) x (BN / WGN) sub-tile
+// as blocks of 16x16 MFMA outputs (4 floats per lane each), times KSPLIT
+// groups of such waves that share the tile and take disjoint K slices of
+// every stage (their partial sums are added when the tile is staged for the
+// epilogue). K advances in stages of SRB = 128 or 256 bytes per row (32 or 64
+// fp32, 64 or 128 bf16 values).
 //
 // Operands move HBM/L2 -> LDS with gfx950's direct loads
 // (global_load_lds_dwordx4): no registers are spent on prefetch and the loads
 // of stage s + 1 are issued right after the barrier that frees their buffer,
 // ahead of the LDS reads and MFMAs of stage s (enforced with scheduling
 // groups). One wave's direct load writes 1 KiB of LDS contiguously (lane l at
-// byte 16 l), i.e. 8 tile rows of 128 bytes; to keep the fragment reads free
-// of bank conflicts without padding, the 16-byte segment g of tile row r is
-// stored at physical segment g ^ (r & 7), and each lane fetches from global
-// memory the logical segment that belongs at its physical slot. The two stage
-// buffers are distinct LDS arrays and the stage loop is unrolled by two, so
-// that no LDS read shares an object with an in-flight direct load and the
-// compiler adds no wait for it.
+// byte 16 l), i.e. 1024 / SRB tile rows; to keep the fragment reads free of
+// bank conflicts without padding, the 16-byte segment g of tile row r is
+// stored at physical segment g ^ (r % (SRB / 16)), and each lane fetches from
+// global memory the logical segment that belongs at its physical slot. The
+// stage buffers are distinct LDS arrays and the stage loop is unrolled by
+// their count, so that no LDS read shares an object with an in-flight direct
+// load and the compiler adds no wait for it.
 //
 // Fragment layout (v_mfma_f32_16x16x4_f32 and v_mfma_f32_16x16x32_bf16): lane
 // l supplies row (l % 16) of a 16-row block and the K group (l / 16). One
@@ -37,6 +40,7 @@
 
 namespace optima {
 
+// Stage width of the 4-wave 128 x 128 configuration.
 constexpr int kStageRowBytes = 128;
 
 template <int MB, int NB>
@@ -79,8 +83,8 @@ __device__ inline float bf16_bits_value(uint32_t h) { return __uint_as_float(h <
 
 // Plane layout of a row of dp values: for every block of 32 consecutive
 // columns, 64 bytes of hi plane then 64 bytes of lo plane. A row therefore
-// takes 4 dp bytes, like fp32, and each 128-byte K stage of the GEMM core
-// holds 32 columns of both planes.
+// takes 4 dp bytes, like fp32, and each 128-byte piece of a K stage holds 32
+// columns of both planes.
 __device__ inline void store_split(uint16_t* row_planes, int n, float v) {
   const uint32_t hi = bf16_rne_bits(v);
   const uint32_t lo = bf16_rne_bits(v - bf16_bits_value(hi));
@@ -89,39 +93,55 @@ __device__ inline void store_split(uint16_t* row_planes, int n, float v) {
   b[32] = uint16_t(lo);
 }
 
-// Tile configuration: a BM x BN output tile per workgroup, WGM x WGN waves,
-// each wave owning a (BM / WGM) x (BN / WGN) sub-tile of 16x16 blocks, and
-// NBUF LDS stage buffers (prefetch distance NBUF - 1 stages).
-template <int BM_, int BN_, int WGM_, int WGN_, int NBUF_>
+// Tile configuration: a BM x BN output tile per workgroup, WGM x WGN x KSPLIT
+// waves, each owning a (BM / WGM) x (BN / WGN) sub-tile of 16x16 blocks and
+// 1 / KSPLIT of every stage's K, NBUF LDS stage buffers (prefetch distance
+// NBUF - 1 stages) and SRB bytes per row and stage.
+template <int BM_, int BN_, int WGM_, int WGN_, int NBUF_, int KSPLIT_ = 1, int SRB_ = 128>
 struct TileCfg {
   static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, NBUF = NBUF_;
-  static constexpr int kWaves = WGM * WGN;
+  static constexpr int KSPLIT = KSPLIT_, SRB = SRB_;
+  static constexpr int kTileWaves = WGM * WGN;     // waves per K group
+  static constexpr int kWaves = kTileWaves * KSPLIT;
   static constexpr int kThreads = 64 * kWaves;
   static constexpr int MB = BM / WGM / 16;  // 16-row blocks per wave
   static constexpr int NB = BN / WGN / 16;  // 16-column blocks per wave
-  static constexpr int kLoadsA = BM / 8 / kWaves;  // 1-KiB wave loads per stage
-  static constexpr int kLoadsB = BN / 8 / kWaves;
+  static constexpr int kSegs = SRB / 16;    // 16-byte segments per row and stage
+  static constexpr int kRowsPerLoad = 1024 / SRB;
+  static constexpr int kLoadsA = BM / kRowsPerLoad / kWaves;  // 1-KiB wave loads per stage
+  static constexpr int kLoadsB = BN / kRowsPerLoad / kWaves;
   static constexpr int kLoads = kLoadsA + kLoadsB;
-  static constexpr int kBufBytes = (BM + BN) * kStageRowBytes;
-  static_assert(BM % (8 * kWaves) == 0 && BN % (8 * kWaves) == 0, "load rounds");
+  static constexpr int kBufBytes = (BM + BN) * SRB;
+  // 64-byte chunks (4 segments: 16 fp32 or 32 bf16 K values per row) per
+  // stage, and per wave.
+  static constexpr int kChunks = SRB / 64;
+  static constexpr int kWaveChunks = kChunks / KSPLIT;
+  static_assert(SRB == 128 || SRB == 256, "stage width");
+  static_assert(BM % (kRowsPerLoad * kWaves) == 0 && BN % (kRowsPerLoad * kWaves) == 0,
+                "load rounds");
   static_assert(NBUF == 2 || NBUF == 3, "stage buffers");
+  static_assert(kWaveChunks >= 2 && kWaveChunks % 2 == 0, "K slice of a wave");
 };
 
-// The 128 x 128 tile with 4 waves of 64 x 64 and two stage buffers.
+// The 128 x 128 tile with 4 waves of 64 x 64 and two 128-byte stage buffers.
 using Tile128 = TileCfg<128, 128, 2, 2, 2>;
+// The 128 x 128 tile with 8 waves: two K groups of 4 waves of 64 x 64 over
+// 256-byte stages (two waves per SIMD with one workgroup per CU).
+using Tile128K2 = TileCfg<128, 128, 2, 2, 2, 2, 256>;
 
 // Rows of the tile that this thread's direct loads fetch: A round i covers
 // A tile row load_row<Cfg>(i), B round i covers B tile row load_row<Cfg>(i);
-// the byte offset of the fetched 16-byte segment within the row's 128-byte
-// stage is load_seg_bytes().
+// the byte offset of the fetched 16-byte segment within the row's stage is
+// load_seg_bytes<Cfg>(i).
 template <typename Cfg>
 __device__ inline int load_row(int i) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  return (i * Cfg::kWaves + wave) * 8 + (lane >> 3);
+  return (i * Cfg::kWaves + wave) * Cfg::kRowsPerLoad + lane / Cfg::kSegs;
 }
-__device__ inline int load_seg_bytes() {
+template <typename Cfg>
+__device__ inline int load_seg_bytes(int i) {
   const int lane = threadIdx.x & 63;
-  return ((lane & 7) ^ (lane >> 3)) * 16;
+  return ((lane % Cfg::kSegs) ^ (load_row<Cfg>(i) % Cfg::kSegs)) * 16;
 }
 
 template <typename Cfg>
@@ -132,7 +152,7 @@ struct Operands {
 
 template <typename Cfg>
 __device__ inline void issue_stage(const Operands<Cfg>& src, int s, char* buf) {
-  const size_t o = size_t(s) * kStageRowBytes;
+  const size_t o = size_t(s) * Cfg::SRB;
   const int wave = threadIdx.x >> 6;
 #pragma unroll
   for (int i = 0; i < Cfg::kLoadsA; ++i)
@@ -143,37 +163,48 @@ __device__ inline void issue_stage(const Operands<Cfg>& src, int s, char* buf) {
   for (int i = 0; i < Cfg::kLoadsB; ++i)
     __builtin_amdgcn_global_load_lds(
         (const __attribute__((address_space(1))) void*)(src.b[i] + o),
-        (__attribute__((address_space(3))) void*)(buf + Cfg::BM * kStageRowBytes +
+        (__attribute__((address_space(3))) void*)(buf + Cfg::BM * Cfg::SRB +
                                                   (i * Cfg::kWaves + wave) * 1024),
         16, 0, 0);
 }
 
 // 16 bytes of logical segment `seg` of tile row r (A rows first, then B).
+template <typename Cfg>
 __device__ inline uint4 lds_frag(const char* buf, int r, int seg) {
-  return *reinterpret_cast<const uint4*>(buf + r * kStageRowBytes + ((seg ^ (r & 7)) * 16));
+  return *reinterpret_cast<const uint4*>(buf + r * Cfg::SRB + ((seg ^ (r % Cfg::kSegs)) * 16));
+}
+
+// This wave's K group (which slice of every stage it multiplies).
+template <typename Cfg>
+__device__ inline int k_group() {
+  return (threadIdx.x >> 6) / Cfg::kTileWaves;
 }
 
 template <typename Cfg, typename T>
 __device__ inline void compute_stage(f4 (&acc)[Cfg::MB][Cfg::NB], const char* buf) {
   constexpr int MB = Cfg::MB, NB = Cfg::NB;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) % Cfg::kTileWaves;
   const int ra = (wave / Cfg::WGN) * MB * 16 + (lane & 15);
   const int rb = Cfg::BM + (wave % Cfg::WGN) * NB * 16 + (lane & 15);
   const int g = lane >> 4;
+  const int c0 = k_group<Cfg>() * Cfg::kWaveChunks;  // first 64-byte chunk of this wave
   if constexpr (std::is_same<T, Bf16x3Tag>::value) {
-    // Segments 0-3 of a row hold the hi plane of 32 K values, 4-7 the lo
-    // plane: per block hi*hi, hi*lo, lo*hi (one 16x16x32 bf16 MFMA each).
+    // A pair of chunks is one 32-column block: segments 0-3 hold its hi
+    // plane, 4-7 its lo plane. Per output block hi*hi, hi*lo, lo*hi (one
+    // 16x16x32 bf16 MFMA each).
+    static_assert(Cfg::kWaveChunks == 2, "one plane block per wave and stage");
+    const int sg = 4 * c0;
     uint4 a0[MB], a1[MB], b0[NB], b1[NB];
 #pragma unroll
-    for (int mi = 0; mi < MB; ++mi) a0[mi] = lds_frag(buf, ra + mi * 16, g);
+    for (int mi = 0; mi < MB; ++mi) a0[mi] = lds_frag<Cfg>(buf, ra + mi * 16, sg + g);
 #pragma unroll
-    for (int ni = 0; ni < NB; ++ni) b0[ni] = lds_frag(buf, rb + ni * 16, g);
+    for (int ni = 0; ni < NB; ++ni) b0[ni] = lds_frag<Cfg>(buf, rb + ni * 16, sg + g);
     mfma_bf16_blocks<MB, NB>(acc, a0, b0);
 #pragma unroll
-    for (int ni = 0; ni < NB; ++ni) b1[ni] = lds_frag(buf, rb + ni * 16, 4 + g);
+    for (int ni = 0; ni < NB; ++ni) b1[ni] = lds_frag<Cfg>(buf, rb + ni * 16, sg + 4 + g);
     mfma_bf16_blocks<MB, NB>(acc, a0, b1);
 #pragma unroll
-    for (int mi = 0; mi < MB; ++mi) a1[mi] = lds_frag(buf, ra + mi * 16, 4 + g);
+    for (int mi = 0; mi < MB; ++mi) a1[mi] = lds_frag<Cfg>(buf, ra + mi * 16, sg + 4 + g);
     mfma_bf16_blocks<MB, NB>(acc, a1, b0);
     __builtin_amdgcn_sched_group_barrier(0x020, Cfg::kLoads, 0);
     __builtin_amdgcn_sched_group_barrier(0x100, MB + NB, 0);
@@ -183,14 +214,15 @@ __device__ inline void compute_stage(f4 (&acc)[Cfg::MB][Cfg::NB], const char* bu
     __builtin_amdgcn_sched_group_barrier(0x100, MB, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, MB * NB, 0);
   } else {
+    static_assert(Cfg::kWaveChunks == 2, "two chunks per wave and stage");
     constexpr int kMfmaPerChunk = std::is_same<T, float>::value ? 4 * MB * NB : MB * NB;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       uint4 a[MB], b[NB];
 #pragma unroll
-      for (int mi = 0; mi < MB; ++mi) a[mi] = lds_frag(buf, ra + mi * 16, 4 * c + g);
+      for (int mi = 0; mi < MB; ++mi) a[mi] = lds_frag<Cfg>(buf, ra + mi * 16, 4 * (c0 + c) + g);
 #pragma unroll
-      for (int ni = 0; ni < NB; ++ni) b[ni] = lds_frag(buf, rb + ni * 16, 4 * c + g);
+      for (int ni = 0; ni < NB; ++ni) b[ni] = lds_frag<Cfg>(buf, rb + ni * 16, 4 * (c0 + c) + g);
       if constexpr (std::is_same<T, float>::value)
         mfma_f32_blocks<MB, NB>(acc, a, b);
       else
@@ -213,7 +245,7 @@ __device__ inline void wait_vmcnt() {
 
 // src.a[i] / src.b[i]: address of the 16-byte segment this thread fetches in
 // A / B tile row load_row<Cfg>(i) at the first stage (row start +
-// load_seg_bytes()); stage s adds s * kStageRowBytes. All addresses must be
+// load_seg_bytes<Cfg>(i)); stage s adds s * Cfg::SRB. All addresses must be
 // 16-byte aligned. lds0..lds2 (lds2 only with NBUF == 3) must be distinct
 // __shared__ arrays of Cfg::kBufBytes declared by the kernel: the loop is
 // unrolled by NBUF so that no LDS read names an array with an in-flight load.
@@ -283,27 +315,36 @@ __device__ inline void gemm_tile_mainloop(f4 (&acc)[Cfg::MB][Cfg::NB], const Ope
 // idle) stage buffers: tile rows 0-63 go to buf0 and 64-127 to buf1, 512
 // bytes per row, 16-byte column chunk c of row r at physical chunk
 // c ^ (r & 31). Both the MFMA-layout writes (16 lanes per row, four rows
-// 4 apart) and the row-chunk reads are free of bank conflicts. After a
-// barrier every thread can read 16-byte chunks of 4 consecutive columns.
+// 4 apart) and the row-chunk reads are free of bank conflicts. With K groups
+// the first group writes and the others add their partial sums in group
+// order. After a barrier every thread can read 16-byte chunks of 4
+// consecutive columns.
 template <typename Cfg>
 __device__ inline void stage_tile(const f4 (&acc)[Cfg::MB][Cfg::NB], char* buf0, char* buf1) {
   static_assert(Cfg::BM == 128 && Cfg::BN == 128, "staging covers 128 x 128 tiles");
   static_assert(Cfg::kBufBytes >= 64 * 512, "stage buffers too small for the tile");
+  const int lane = threadIdx.x & 63, wave = (threadIdx.x >> 6) % Cfg::kTileWaves;
+  const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
+  const int kg = k_group<Cfg>();
 #pragma unroll
-  for (int mi = 0; mi < Cfg::MB; ++mi)
+  for (int grp = 0; grp < Cfg::KSPLIT; ++grp) {
+    if (grp > 0) __syncthreads();
+    if (kg != grp) continue;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) / Cfg::WGN;
-      const int wn = (threadIdx.x >> 6) % Cfg::WGN;
-      const int r = wm * Cfg::MB * 16 + mi * 16 + 4 * (lane >> 4) + e;
-      char* row = (r < 64 ? buf0 : buf1) + (r & 63) * 512;
+    for (int mi = 0; mi < Cfg::MB; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < Cfg::NB; ++ni) {
-        const int col = wn * Cfg::NB * 16 + ni * 16 + (lane & 15);
-        const int ch = (col >> 2) ^ (r & 31);
-        *reinterpret_cast<float*>(row + ch * 16 + (col & 3) * 4) = acc[mi][ni][e];
+      for (int e = 0; e < 4; ++e) {
+        const int r = wm * Cfg::MB * 16 + mi * 16 + 4 * (lane >> 4) + e;
+        char* row = (r < 64 ? buf0 : buf1) + (r & 63) * 512;
+#pragma unroll
+        for (int ni = 0; ni < Cfg::NB; ++ni) {
+          const int col = wn * Cfg::NB * 16 + ni * 16 + (lane & 15);
+          const int ch = (col >> 2) ^ (r & 31);
+          float* q = reinterpret_cast<float*>(row + ch * 16 + (col & 3) * 4);
+          *q = grp == 0 ? acc[mi][ni][e] : *q + acc[mi][ni][e];
+        }
       }
-    }
+  }
 }
 
 __device__ inline float4 staged_chunk(const char* buf0, const char* buf1, int r, int c) {
@@ -312,14 +353,16 @@ __device__ inline float4 staged_chunk(const char* buf0, const char* buf1, int r,
 }
 
 // Output coordinates of accumulator element (mi, ni, e) of this thread,
-// relative to the tile origin.
+// relative to the tile origin (configurations without K groups).
 template <typename Cfg>
 __device__ inline int acc_row(int mi, int e) {
+  static_assert(Cfg::KSPLIT == 1, "K groups hold partial sums");
   const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) / Cfg::WGN;
   return wm * Cfg::MB * 16 + mi * 16 + 4 * (lane >> 4) + e;
 }
 template <typename Cfg>
 __device__ inline int acc_col(int ni) {
+  static_assert(Cfg::KSPLIT == 1, "K groups hold partial sums");
   const int lane = threadIdx.x & 63, wn = (threadIdx.x >> 6) % Cfg::WGN;
   return wn * Cfg::NB * 16 + ni * 16 + (lane & 15);
 }

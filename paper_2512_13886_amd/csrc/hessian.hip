@@ -14,6 +14,12 @@
 //
 // bf16 tokens use v_mfma_f32_16x16x32_bf16 (the bf16 x bf16 products are exact
 // in fp32); fp32 tokens use v_mfma_f32_16x16x4_f32.
+//
+// bf16 tokens with d a multiple of 256 (every transformer width here) take a
+// direct path instead: no transpose. Token rows go from X straight into LDS
+// and the MFMA operands are gathered from there with gfx950's transposing LDS
+// read, on 256 x 256 lower-triangular tiles; the whole token range is one
+// launch, split along the tokens so that the tiles fill all CUs evenly.
 #include "common.h"
 #include "gemm_core.h"
 
@@ -88,13 +94,15 @@ __global__ void __launch_bounds__(kThreads) k_syrk(const char* XT, int64_t pitch
   const int s1 = int(int64_t(stages) * (sp + 1) / splits);
   using Cfg = Tile128;
   Operands<Cfg> src;
-  const int64_t k_off = int64_t(s0) * kStageRowBytes + load_seg_bytes();
+  const int64_t k_off = int64_t(s0) * Cfg::SRB;
 #pragma unroll
   for (int i = 0; i < Cfg::kLoadsA; ++i)
-    src.a[i] = XT + (int64_t(ti) * kTile + load_row<Cfg>(i)) * pitch_bytes + k_off;
+    src.a[i] = XT + (int64_t(ti) * kTile + load_row<Cfg>(i)) * pitch_bytes + k_off +
+               load_seg_bytes<Cfg>(i);
 #pragma unroll
   for (int i = 0; i < Cfg::kLoadsB; ++i)
-    src.b[i] = XT + (int64_t(tj) * kTile + load_row<Cfg>(i)) * pitch_bytes + k_off;
+    src.b[i] = XT + (int64_t(tj) * kTile + load_row<Cfg>(i)) * pitch_bytes + k_off +
+               load_seg_bytes<Cfg>(i);
   f4 acc[Cfg::MB][Cfg::NB];
   gemm_tile_mainloop<Cfg, T>(acc, src, s1 - s0, lds0, lds1, nullptr);
   float* P = part + size_t(sp) * size_t(dp) * size_t(dp);
@@ -153,11 +161,246 @@ __global__ void __launch_bounds__(1024) k_damp(float* H, int64_t d, float rel, f
   for (int64_t i = threadIdx.x; i < d; i += 1024) H[i * d + i] = float(double(H[i * d + i]) + lam);
 }
 
+// ---------------------------------------------------------------------------
+// Direct path (bf16, d % 256 == 0)
+// ---------------------------------------------------------------------------
+//
+// Workgroup: one 256 x 256 output tile (ti, tj), ti >= tj, over a contiguous
+// range of 64-token stages; 8 waves in a 4 x 2 grid, each wave owning 64 x
+// 128 outputs (4 x 8 blocks of 16 x 16). Stage buffer: block A holds
+// X[t][256 ti + 0..255] and block B X[t][256 tj + 0..255] for the stage's 64
+// tokens, one 512-byte row per token, written by direct loads (one wave load
+// = 1 KiB = 2 token rows). Within a row the 16-byte segment g sits at
+// physical segment g ^ swz(row), which keeps both the loads' writes and the
+// transposing reads free of bank conflicts.
+//
+// Operands: ds_read_b64_tr_b16 treats the eight-byte reads of each 16-lane
+// group as a 4 x 16 matrix of 16-bit values (lane j supplies row j / 4,
+// columns 4 (j % 4) .. 4 (j % 4) + 3) and returns column i to lane i. Lanes
+// j of group g address token row 8 g + 4 h + j / 4 and features
+// f + 4 (j % 4): lane i then holds tokens 8 g + 4 h + 0..3 of feature f + i,
+// and the reads for h = 0 and h = 1 together give the 8 consecutive tokens
+// that a 16x16x32 bf16 MFMA takes from lane (g, i), for both operands. The
+// output block (lane, e) is then H[f_a + 4 g + e][f_b + i] as in the NT core.
+namespace dt {
+constexpr int kRows = 64;                   // tokens per stage
+constexpr int kBlock = 256;                 // features per operand block (tile side)
+constexpr int kRowBytes = 2 * kBlock;       // 512
+constexpr int kBlockBytes = kRows * kRowBytes;
+constexpr int kBufBytes = 2 * kBlockBytes;  // 64 KiB per stage buffer
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kLoads = kBlockBytes / 1024 / kWaves;  // wave loads per block per thread
+constexpr int kMB = 4, kNB = 8;             // 16x16 blocks per wave
+constexpr int kMaxSplits = 64;
+constexpr int kCus = 256;                   // MI355X compute units (sizing only)
+
+// Physical XOR of the 16-byte segment index for token row r of a stage:
+// flips segment bits 1-3 by (r & 3) and bit 3 of r.
+__device__ inline int swz(int r) { return 2 * ((r & 3) | (((r >> 3) & 1) << 2)); }
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+
+__device__ inline uint2 tr_read(const char* p) {
+  const v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4s*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+// Direct loads of one stage: this thread's A and B source addresses for the
+// stage's first load round; round i adds 16 token rows.
+__device__ inline void issue(const char* a, const char* b, int64_t round_bytes, char* buf) {
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i)
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(a + i * round_bytes),
+        (__attribute__((address_space(3))) void*)(buf + (i * kWaves + wave) * 1024), 16, 0, 0);
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i)
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(b + i * round_bytes),
+        (__attribute__((address_space(3))) void*)(buf + kBlockBytes + (i * kWaves + wave) * 1024),
+        16, 0, 0);
+}
+
+__device__ inline void compute(f4 (&acc)[kMB][kNB], const char* buf) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int g = lane >> 4, j = lane & 15;
+  // Token row 32 kk + 8 g + 4 h + j / 4 has (row & 3) = j / 4 and bit 3 of
+  // the row equal to g & 1, so its swizzle depends on the lane only.
+  const int sw = 2 * ((j >> 2) | ((g & 1) << 2));
+  const int intra = 8 * (j & 1);
+  const int seg_lane = (j & 3) >> 1;
+  auto frag_off = [&](int f0) { return (((f0 >> 3) + seg_lane) ^ sw) * 16 + intra; };
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int r0 = 32 * kk + 8 * g + (j >> 2);
+    const char* A0 = buf + r0 * kRowBytes;
+    const char* A1 = A0 + 4 * kRowBytes;
+    uint4 a[kMB], b[kNB];
+#pragma unroll
+    for (int mi = 0; mi < kMB; ++mi) {
+      const int o = frag_off(wm * 64 + 16 * mi);
+      const uint2 lo = tr_read(A0 + o), hi = tr_read(A1 + o);
+      a[mi] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+#pragma unroll
+    for (int ni = 0; ni < kNB; ++ni) {
+      const int o = frag_off(wn * 128 + 16 * ni);
+      const uint2 lo = tr_read(A0 + kBlockBytes + o), hi = tr_read(A1 + kBlockBytes + o);
+      b[ni] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+#pragma unroll
+    for (int mi = 0; mi < kMB; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < kNB; ++ni)
+        acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, a[mi]), __builtin_bit_cast(bf16x8, b[ni]), acc[mi][ni], 0,
+            0, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x020, 2 * kLoads, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * (kMB + kNB), 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, kMB * kNB, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * (kMB + kNB), 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, kMB * kNB, 0);
+}
+
+}  // namespace dt
+
+// X: [n_rows][d] bf16 with n_rows >= stages * 64 of the rows from `X`; tile
+// idx / splits over the triangle of d / 256 blocks; split sp covers stages
+// [stages sp / splits, stages (sp + 1) / splits). Writes (first) or adds the
+// tile's partial sum into part[sp] ([d][d] fp32).
+__global__ void __launch_bounds__(dt::kThreads) k_syrk_direct(const uint16_t* X, int64_t d,
+                                                              int stages, int splits,
+                                                              float* part, int first) {
+  using namespace dt;
+  __shared__ __attribute__((aligned(1024))) char lds0[kBufBytes];
+  __shared__ __attribute__((aligned(1024))) char lds1[kBufBytes];
+  const int tile = blockIdx.x / splits;
+  const int sp = blockIdx.x - tile * splits;
+  int ti, tj;
+  tri_tile(tile, &ti, &tj);
+  const int s0 = int(int64_t(stages) * sp / splits);
+  const int s1 = int(int64_t(stages) * (sp + 1) / splits);
+  const int n = s1 - s0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // This thread's rows and segment in load round 0: token row 2 wave + lane / 32,
+  // physical segment lane % 32.
+  const int row = 2 * wave + (lane >> 5);
+  const int lseg = (lane & 31) ^ swz(row);
+  const int64_t row_bytes = d * 2;
+  const char* xb = reinterpret_cast<const char*>(X) + (int64_t(s0) * kRows + row) * row_bytes +
+                   lseg * 16;
+  const char* a = xb + int64_t(ti) * kBlock * 2;
+  const char* b = xb + int64_t(tj) * kBlock * 2;
+  const int64_t round_bytes = 16 * row_bytes;
+  const int64_t stage_bytes = kRows * row_bytes;
+
+  f4 acc[kMB][kNB];
+#pragma unroll
+  for (int mi = 0; mi < kMB; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < kNB; ++ni) acc[mi][ni] = f4{0.f, 0.f, 0.f, 0.f};
+  if (n > 0) {
+    auto cl = [n](int q) { return q < n ? q : n - 1; };
+    issue(a, b, round_bytes, lds0);
+    int q = 0;
+    for (; q + 1 < n; q += 2) {
+      wait_vmcnt<0>();
+      __syncthreads();
+      issue(a + (q + 1) * stage_bytes, b + (q + 1) * stage_bytes, round_bytes, lds1);
+      compute(acc, lds0);
+      wait_vmcnt<0>();
+      __syncthreads();
+      issue(a + cl(q + 2) * stage_bytes, b + cl(q + 2) * stage_bytes, round_bytes, lds0);
+      compute(acc, lds1);
+    }
+    if (q < n) {
+      wait_vmcnt<0>();
+      __syncthreads();
+      compute(acc, lds0);
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+  float* P = part + size_t(sp) * size_t(d) * size_t(d);
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int mi = 0; mi < kMB; ++mi)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t i = int64_t(ti) * kBlock + wm * 64 + mi * 16 + 4 * (lane >> 4) + e;
+#pragma unroll
+      for (int ni = 0; ni < kNB; ++ni) {
+        const int64_t jj = int64_t(tj) * kBlock + wn * 128 + ni * 16 + (lane & 15);
+        float* q = P + i * d + jj;
+        *q = first ? acc[mi][ni][e] : *q + acc[mi][ni][e];
+      }
+    }
+}
+
+// Copies `rows` (< 64) token rows starting at t0 into a zero-padded 64-row
+// buffer so that the direct path never loads past the end of X.
+__global__ void __launch_bounds__(kThreads) k_tail_rows(const uint16_t* X, int64_t d, int64_t t0,
+                                                        int rows, uint16_t* out) {
+  const int64_t total = int64_t(dt::kRows) * d;
+  for (int64_t e = int64_t(blockIdx.x) * kThreads + threadIdx.x; e < total;
+       e += int64_t(gridDim.x) * kThreads) {
+    const int64_t r = e / d;
+    out[e] = r < rows ? X[(t0 + r) * d + (e - r * d)] : uint16_t(0);
+  }
+}
+
+struct DirectPlan {
+  int64_t tiles;
+  int full_stages, tail_rows, splits;
+  size_t part_elems;
+};
+
+bool direct_ok(int64_t d, int dtype) {
+  return dtype == OPTIMA_DTYPE_BF16 && d % dt::kBlock == 0;
+}
+
+DirectPlan direct_plan(int64_t n_tok, int64_t d) {
+  DirectPlan p{};
+  const int64_t nt = d / dt::kBlock;
+  p.tiles = nt * (nt + 1) / 2;
+  p.full_stages = int(n_tok / dt::kRows);
+  p.tail_rows = int(n_tok % dt::kRows);
+  // Splits along the tokens: the fewest rounds of workgroups per CU relative
+  // to the work, with 1% per split for the partial sums; at most 4 GiB of
+  // partials.
+  int best = 1;
+  double best_cost = 1e30;
+  const int max_s = std::max(1, std::min(dt::kMaxSplits, p.full_stages));
+  for (int S = 1; S <= max_s; ++S) {
+    if (S > 1 && double(S) * double(d) * double(d) * 4.0 > double(int64_t(1) << 32)) break;
+    const double rounds = double(ceil_div(p.tiles * S, dt::kCus));
+    const double c = rounds / S * (1.0 + 0.01 * S);
+    if (c < best_cost - 1e-12) {
+      best = S;
+      best_cost = c;
+    }
+  }
+  p.splits = best;
+  p.part_elems = size_t(best) * size_t(d) * size_t(d);
+  return p;
+}
+
 }  // namespace
 
 size_t hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
-  const HessPlan p = plan(n_tok, d, dtype);
   Carver c(nullptr);
+  if (direct_ok(d, dtype)) {
+    const DirectPlan p = direct_plan(n_tok, d);
+    c.take<float>(p.part_elems);
+    c.take<uint16_t>(size_t(dt::kRows) * size_t(d));
+    return c.bytes();
+  }
+  const HessPlan p = plan(n_tok, d, dtype);
   c.take<char>(p.xt_elems * p.esz);
   c.take<float>(p.part_elems);
   return c.bytes();
@@ -167,6 +410,34 @@ optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_
                                  int accumulate, void* ws, hipStream_t s) {
   if (n_tok == 0) {
     if (!accumulate) OPTIMA_HIP_TRY(hipMemsetAsync(H, 0, size_t(d) * size_t(d) * sizeof(float), s));
+    return OPTIMA_OK;
+  }
+  if (direct_ok(d, dtype) && aligned16(X)) {
+    const DirectPlan p = direct_plan(n_tok, d);
+    Carver c(ws);
+    float* part = c.take<float>(p.part_elems);
+    uint16_t* tail = c.take<uint16_t>(size_t(dt::kRows) * size_t(d));
+    const uint16_t* Xb = static_cast<const uint16_t*>(X);
+    int splits = p.splits;
+    if (p.full_stages > 0) {
+      hipLaunchKernelGGL(k_syrk_direct, dim3(unsigned(p.tiles * splits)), dim3(dt::kThreads), 0,
+                         s, Xb, d, p.full_stages, splits, part, 1);
+      OPTIMA_LAUNCH_CHECK();
+    } else {
+      splits = 1;
+    }
+    if (p.tail_rows > 0) {
+      hipLaunchKernelGGL(k_tail_rows, dim3(256), dim3(kThreads), 0, s, Xb, d,
+                         int64_t(p.full_stages) * dt::kRows, p.tail_rows, tail);
+      OPTIMA_LAUNCH_CHECK();
+      hipLaunchKernelGGL(k_syrk_direct, dim3(unsigned(p.tiles)), dim3(dt::kThreads), 0, s, tail,
+                         d, 1, 1, part, p.full_stages > 0 ? 0 : 1);
+      OPTIMA_LAUNCH_CHECK();
+    }
+    const int64_t B = ceil_div(d, 64);
+    hipLaunchKernelGGL(k_hess_reduce, dim3(unsigned(B * (B + 1) / 2)), dim3(kThreads), 0, s, part,
+                       splits, d, d, H, accumulate);
+    OPTIMA_LAUNCH_CHECK();
     return OPTIMA_OK;
   }
   const HessPlan p = plan(n_tok, d, dtype);

@@ -141,10 +141,15 @@ __device__ inline void epilogue4(const ProductArgs& p, int j, int n, float4 y4, 
 // partial sum to part[split][launch row][n] and k_split_epilogue adds them.
 // The accumulators pass through LDS so that the epilogue works on 16-byte
 // chunks of 4 consecutive columns (full-width loads and stores).
+// Four waves per workgroup and 64 KiB of LDS let two workgroups share a CU,
+// so one workgroup's memory-bound fused update overlaps the other's MFMA main
+// loop (eight-wave tiles that fill a CU alone leave that update exposed).
+using ProductTile = Tile128;
+
 template <int MODE, int PREC>
-__global__ void __launch_bounds__(Tile128::kThreads) k_product(ProductArgs p, int splits,
-                                                               float* part) {
-  using Cfg = Tile128;
+__global__ void __launch_bounds__(ProductTile::kThreads) k_product(ProductArgs p, int splits,
+                                                                   float* part) {
+  using Cfg = ProductTile;
   __shared__ __attribute__((aligned(1024))) char lds0[Cfg::kBufBytes];
   __shared__ __attribute__((aligned(1024))) char lds1[Cfg::kBufBytes];
   const int tiles_m = (p.n_rows + kTile - 1) / kTile;
@@ -155,12 +160,12 @@ __global__ void __launch_bounds__(Tile128::kThreads) k_product(ProductArgs p, in
   int tm, tn;
   tile_of_block(lin, n_tiles, tiles_m, tiles_n, &tm, &tn);
   const int m0 = tm * kTile, n0 = tn * kTile;
-  const int stages = p.dp * 4 / kStageRowBytes;
+  const int stages = p.dp * 4 / Cfg::SRB;
   const int s0 = int(int64_t(stages) * sp / splits);
   const int s1 = int(int64_t(stages) * (sp + 1) / splits);
 
   Operands<Cfg> src;
-  const size_t k_off = size_t(s0) * kStageRowBytes + load_seg_bytes();
+  const size_t k_off = size_t(s0) * Cfg::SRB;
   // Both layouts take 4 dp bytes per row.
   const char* a_base = PREC == kPrecBf16x3 ? reinterpret_cast<const char*>(p.Ap)
                                            : reinterpret_cast<const char*>(p.A);
@@ -171,11 +176,11 @@ __global__ void __launch_bounds__(Tile128::kThreads) k_product(ProductArgs p, in
     int r = m0 + load_row<Cfg>(i);
     r = r < p.n_rows ? r : p.n_rows - 1;
     const int j = p.rows ? p.rows[r] : r;
-    src.a[i] = a_base + size_t(j) * p.dp * 4 + k_off;
+    src.a[i] = a_base + size_t(j) * p.dp * 4 + k_off + load_seg_bytes<Cfg>(i);
   }
 #pragma unroll
   for (int i = 0; i < Cfg::kLoadsB; ++i)
-    src.b[i] = b_base + size_t(n0 + load_row<Cfg>(i)) * p.dp * 4 + k_off;
+    src.b[i] = b_base + size_t(n0 + load_row<Cfg>(i)) * p.dp * 4 + k_off + load_seg_bytes<Cfg>(i);
   f4 acc[Cfg::MB][Cfg::NB];
   if (PREC == kPrecBf16x3)
     gemm_tile_mainloop<Cfg, Bf16x3Tag>(acc, src, s1 - s0, lds0, lds1, nullptr);
@@ -266,7 +271,7 @@ __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows
 // Copies W0 into padded rows and forms the start point x = x_ag = sel(m, w0, 0).
 __global__ void __launch_bounds__(kThreads) k_prep(const float* W0, const uint8_t* mask, int n_cols,
                                                    int d, int dp, float* W0P, float* X, float* XA,
-                                                   uint16_t* XP, int* flags) {
+                                                   uint16_t* XP, uint16_t* WP, int* flags) {
   const int j = blockIdx.x;
   const size_t base = size_t(j) * dp;
   bool bad = false;
@@ -283,6 +288,7 @@ __global__ void __launch_bounds__(kThreads) k_prep(const float* W0, const uint8_
     X[base + n] = x;
     XA[base + n] = x;
     if (XP) store_split(XP + base * 2, n, x);
+    if (WP) store_split(WP + base * 2, n, w);
   }
   if (bad) atomicOr(flags, 1);
 }
@@ -619,10 +625,10 @@ template <int MODE, int PREC>
 optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t s) {
   const int tiles_m = int(ceil_div(p.n_rows, kTile));
   const int tiles_n = p.dp / kTile;
-  const int stages = p.dp * 4 / kStageRowBytes;
+  const int stages = p.dp * 4 / ProductTile::SRB;
   const int S = choose_splits(tiles_m * tiles_n, stages, tiles_m, p.dp, l.part_elems);
-  hipLaunchKernelGGL((k_product<MODE, PREC>), dim3(tiles_m * tiles_n * S), dim3(kThreads), 0, s,
-                     p, S, l.part);
+  hipLaunchKernelGGL((k_product<MODE, PREC>), dim3(tiles_m * tiles_n * S),
+                     dim3(ProductTile::kThreads), 0, s, p, S, l.part);
   OPTIMA_LAUNCH_CHECK();
   if (S > 1) {
     const dim3 g(unsigned(p.n_rows), unsigned(ceil_div(p.dp, 4 * kThreads)));
@@ -670,8 +676,9 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   const dim3 vec_grid(unsigned(nc), unsigned(ceil_div(dp, 4 * kThreads)));
   // W0 padded copy goes to HX first; Hw0 = H w0, then Hx = Hx_ag = H x0.
   const bool split = o.precision == kPrecBf16x3;
+  // Split planes: x0 into XP0, W0 into XP1 (free until the first update).
   hipLaunchKernelGGL(k_prep, vec_grid, dim3(kThreads), 0, s, W0, mask, nc, di, dp, l.HX, l.X0,
-                     l.XA, split ? l.XP0 : nullptr, l.flags);
+                     l.XA, split ? l.XP0 : nullptr, split ? l.XP1 : nullptr, l.flags);
   OPTIMA_LAUNCH_CHECK();
   if (split) {
     hipLaunchKernelGGL(k_split_h, dim3(unsigned(dp), unsigned(ceil_div(dp, 4 * kThreads))),
@@ -693,14 +700,18 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   p.rows = nullptr;
   p.n_rows = nc;
   p.Bp = l.HP;
-  // The two setup products stay in fp32 (Hw0 enters every gradient).
+  // The setup products use the solve's precision too: H w0 and H x0 then
+  // agree bit for bit wherever w0 and x0 do (all-kept columns start at
+  // their optimum with a zero gradient).
   p.A = l.HX;
+  p.Ap = l.XP1;
   p.out1 = l.HW0;
-  if (auto e = launch_product<kPlain, kPrecF32>(p, l, s)) return e;
+  if (auto e = launch_product<kPlain>(p, l, o.precision, s)) return e;
   p.A = l.X0;
+  p.Ap = l.XP0;
   p.out1 = l.HX;
   p.out2 = l.HA;
-  if (auto e = launch_product<kPlain2, kPrecF32>(p, l, s)) return e;
+  if (auto e = launch_product<kPlain2>(p, l, o.precision, s)) return e;
   inf.gemm_calls += 2;
   inf.row_products += 2 * int64_t(nc);
 

@@ -37,6 +37,11 @@ def _check_h(Hg: np.ndarray, Ho: np.ndarray, rel=1e-5, ent=2e-5):
     ("bf16_ragged", workloads.GPT2_FC, (3000, 200)),
     ("f32_ragged", workloads.TINY, (77, 5)),
     ("bf16_one_tile", workloads.Q_PROJ, (130, 128)),
+    # bf16 with d % 256 == 0: token rows read in place (direct path)
+    ("bf16_direct_one_tile_tail", workloads.Q_PROJ, (130, 256)),
+    ("bf16_direct_tail_only", workloads.Q_PROJ, (50, 512)),
+    ("bf16_direct_exact_stages", workloads.GPT2_FC, (640, 768)),
+    ("bf16_direct_split", workloads.Q_PROJ, (8256, 1024)),
 ])
 def test_hessian_parity_small(L, case):
     name, cfg, shape = case
@@ -66,6 +71,21 @@ def test_hessian_accumulate_in_sequences(L):
     assert torch.all(H0 == 7.0)
     L.optima_hessian_accumulate(Xd[:0], H0, accumulate=False)
     assert torch.all(H0 == 0.0)
+
+
+def test_hessian_direct_accumulate_in_sequences(L):
+    # The direct path: sequences of 2048 tokens and a ragged 100-token one,
+    # accumulated into an H that starts non-zero.
+    cfg = workloads.Q_PROJ.with_tokens(3 * 2048)
+    X = np.ascontiguousarray(workloads.x_all(cfg)[:, :512])
+    X = np.concatenate([X, X[:100]])
+    Xd = to_dev_x(X)
+    H = torch.full((512, 512), 5.0, dtype=torch.float32, device=dev())
+    bounds = [0, 2048, 4096, 6144, 6244]
+    for c in range(4):
+        L.optima_hessian_accumulate(Xd[bounds[c]:bounds[c + 1]], H, accumulate=True)
+    Ho = oracle.hessian([workloads.x_to_f64(X[bounds[c]:bounds[c + 1]]) for c in range(4)])
+    _check_h(H.cpu().numpy().astype(np.float64), Ho + 5.0)
 
 
 def test_hessian_gpt2_full_size(L):
