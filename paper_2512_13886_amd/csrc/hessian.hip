@@ -188,12 +188,21 @@ constexpr int kBlock = 256;                 // features per operand block (tile 
 constexpr int kRowBytes = 2 * kBlock;       // 512
 constexpr int kBlockBytes = kRows * kRowBytes;
 constexpr int kBufBytes = 2 * kBlockBytes;  // 64 KiB per stage buffer
-constexpr int kWaves = 8;
-constexpr int kThreads = 64 * kWaves;
-constexpr int kLoads = kBlockBytes / 1024 / kWaves;  // wave loads per block per thread
-constexpr int kMB = 4, kNB = 8;             // 16x16 blocks per wave
 constexpr int kMaxSplits = 64;
 constexpr int kCus = 256;                   // MI355X compute units (sizing only)
+
+// Wave layout of the 256 x 256 tile: WAVES / 2 x 2 waves; with 8 waves each
+// owns 64 x 128 outputs and two waves share each SIMD. (Four waves of
+// 128 x 128 would halve the LDS reads per MFMA, but need more than the 512
+// registers of a lane.)
+template <int WAVES>
+struct Cfg {
+  static constexpr int kWaves = WAVES;
+  static constexpr int kThreads = 64 * WAVES;
+  static constexpr int WGN = 2, WGM = WAVES / WGN;
+  static constexpr int kMB = kBlock / WGM / 16, kNB = kBlock / WGN / 16;
+  static constexpr int kLoads = kBlockBytes / 1024 / WAVES;  // wave loads per block per thread
+};
 
 // Physical XOR of the 16-byte segment index for token row r of a stage:
 // flips segment bits 1-3 by (r & 3) and bit 3 of r.
@@ -207,135 +216,154 @@ __device__ inline uint2 tr_read(const char* p) {
   return __builtin_bit_cast(uint2, v);
 }
 
-// Direct loads of one stage: this thread's A and B source addresses for the
-// stage's first load round; round i adds 16 token rows.
-__device__ inline void issue(const char* a, const char* b, int64_t round_bytes, char* buf) {
+// Direct loads of one stage. Round i of this thread fetches token row
+// row0 + 2 WAVES i (row0 = 2 wave + lane / 32) at physical segment lane % 32;
+// `a` / `b` point at that row's A / B block for round 0 without the segment
+// offset, seg[i & 1] is the logical segment's byte offset for the round.
+template <typename C>
+__device__ inline void issue(const char* a, const char* b, int64_t round_bytes, const int (&seg)[2],
+                             char* buf) {
   const int wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int i = 0; i < kLoads; ++i)
+  for (int i = 0; i < C::kLoads; ++i)
     __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(a + i * round_bytes),
-        (__attribute__((address_space(3))) void*)(buf + (i * kWaves + wave) * 1024), 16, 0, 0);
+        (const __attribute__((address_space(1))) void*)(a + i * round_bytes + seg[i & 1]),
+        (__attribute__((address_space(3))) void*)(buf + (i * C::kWaves + wave) * 1024), 16, 0, 0);
 #pragma unroll
-  for (int i = 0; i < kLoads; ++i)
+  for (int i = 0; i < C::kLoads; ++i)
     __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(b + i * round_bytes),
-        (__attribute__((address_space(3))) void*)(buf + kBlockBytes + (i * kWaves + wave) * 1024),
+        (const __attribute__((address_space(1))) void*)(b + i * round_bytes + seg[i & 1]),
+        (__attribute__((address_space(3))) void*)(buf + kBlockBytes + (i * C::kWaves + wave) * 1024),
         16, 0, 0);
 }
 
-__device__ inline void compute(f4 (&acc)[kMB][kNB], const char* buf) {
+// Operand fragments of K step kk (32 tokens) of the stage in `buf`.
+template <typename C>
+__device__ inline void read_frags(const char* buf, int kk, uint4 (&a)[C::kMB], uint4 (&b)[C::kNB]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int g = lane >> 4, j = lane & 15;
   // Token row 32 kk + 8 g + 4 h + j / 4 has (row & 3) = j / 4 and bit 3 of
   // the row equal to g & 1, so its swizzle depends on the lane only.
   const int sw = 2 * ((j >> 2) | ((g & 1) << 2));
   const int intra = 8 * (j & 1);
   const int seg_lane = (j & 3) >> 1;
-  auto frag_off = [&](int f0) { return (((f0 >> 3) + seg_lane) ^ sw) * 16 + intra; };
+  const char* A0 = buf + (32 * kk + 8 * g + (j >> 2)) * kRowBytes;
+  const char* A1 = A0 + 4 * kRowBytes;
+#pragma unroll
+  for (int mi = 0; mi < C::kMB; ++mi) {
+    const int o = (((((wm * C::kMB + mi) * 16) >> 3) + seg_lane) ^ sw) * 16 + intra;
+    const uint2 lo = tr_read(A0 + o), hi = tr_read(A1 + o);
+    a[mi] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  }
+#pragma unroll
+  for (int ni = 0; ni < C::kNB; ++ni) {
+    const int o = (((((wn * C::kNB + ni) * 16) >> 3) + seg_lane) ^ sw) * 16 + intra;
+    const uint2 lo = tr_read(A0 + kBlockBytes + o), hi = tr_read(A1 + kBlockBytes + o);
+    b[ni] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  }
+}
+
+template <typename C>
+__device__ inline void mfma_step(f4 (&acc)[C::kMB][C::kNB], const uint4 (&a)[C::kMB],
+                                 const uint4 (&b)[C::kNB]) {
+#pragma unroll
+  for (int mi = 0; mi < C::kMB; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < C::kNB; ++ni)
+      acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          __builtin_bit_cast(bf16x8, a[mi]), __builtin_bit_cast(bf16x8, b[ni]), acc[mi][ni], 0, 0,
+          0);
+}
+
+template <typename C>
+__device__ inline void compute(f4 (&acc)[C::kMB][C::kNB], const char* buf) {
+  constexpr int kReads = 2 * (C::kMB + C::kNB), kMfma = C::kMB * C::kNB;
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk) {
-    const int r0 = 32 * kk + 8 * g + (j >> 2);
-    const char* A0 = buf + r0 * kRowBytes;
-    const char* A1 = A0 + 4 * kRowBytes;
-    uint4 a[kMB], b[kNB];
-#pragma unroll
-    for (int mi = 0; mi < kMB; ++mi) {
-      const int o = frag_off(wm * 64 + 16 * mi);
-      const uint2 lo = tr_read(A0 + o), hi = tr_read(A1 + o);
-      a[mi] = make_uint4(lo.x, lo.y, hi.x, hi.y);
-    }
-#pragma unroll
-    for (int ni = 0; ni < kNB; ++ni) {
-      const int o = frag_off(wn * 128 + 16 * ni);
-      const uint2 lo = tr_read(A0 + kBlockBytes + o), hi = tr_read(A1 + kBlockBytes + o);
-      b[ni] = make_uint4(lo.x, lo.y, hi.x, hi.y);
-    }
-#pragma unroll
-    for (int mi = 0; mi < kMB; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < kNB; ++ni)
-        acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            __builtin_bit_cast(bf16x8, a[mi]), __builtin_bit_cast(bf16x8, b[ni]), acc[mi][ni], 0,
-            0, 0);
+    uint4 a[C::kMB], b[C::kNB];
+    read_frags<C>(buf, kk, a, b);
+    mfma_step<C>(acc, a, b);
   }
-  __builtin_amdgcn_sched_group_barrier(0x020, 2 * kLoads, 0);
-  __builtin_amdgcn_sched_group_barrier(0x100, 2 * (kMB + kNB), 0);
-  __builtin_amdgcn_sched_group_barrier(0x008, kMB * kNB, 0);
-  __builtin_amdgcn_sched_group_barrier(0x100, 2 * (kMB + kNB), 0);
-  __builtin_amdgcn_sched_group_barrier(0x008, kMB * kNB, 0);
+  __builtin_amdgcn_sched_group_barrier(0x020, 2 * C::kLoads, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
 }
 
 }  // namespace dt
 
-// X: [n_rows][d] bf16 with n_rows >= stages * 64 of the rows from `X`; tile
-// idx / splits over the triangle of d / 256 blocks; split sp covers stages
-// [stages sp / splits, stages (sp + 1) / splits). Writes (first) or adds the
-// tile's partial sum into part[sp] ([d][d] fp32).
-__global__ void __launch_bounds__(dt::kThreads) k_syrk_direct(const uint16_t* X, int64_t d,
-                                                              int stages, int splits,
-                                                              float* part, int first) {
+// X: [n_rows][d] bf16 with n_rows >= stages * 64. Workgroup b handles split
+// sp = b / n_tiles of tile b % n_tiles of the triangle of d / 256 blocks;
+// split sp covers stages [stages sp / splits, stages (sp + 1) / splits).
+// Writes (first) or adds the tile's partial sum into part[sp] ([d][d] fp32).
+template <int WAVES>
+__global__ void __launch_bounds__(64 * WAVES) k_syrk_direct(const uint16_t* X, int64_t d,
+                                                            int stages, int splits, float* part,
+                                                            int first) {
   using namespace dt;
+  using C = Cfg<WAVES>;
   __shared__ __attribute__((aligned(1024))) char lds0[kBufBytes];
   __shared__ __attribute__((aligned(1024))) char lds1[kBufBytes];
-  const int tile = blockIdx.x / splits;
-  const int sp = blockIdx.x - tile * splits;
+  // Split-major order: the workgroups resident at one time work on one or
+  // two token ranges, so every block of X they share is fetched into the
+  // L2 / MALL once for all of them.
+  const int n_tiles = int(gridDim.x) / splits;
+  const int sp = blockIdx.x / n_tiles;
+  const int tile = blockIdx.x - sp * n_tiles;
   int ti, tj;
   tri_tile(tile, &ti, &tj);
   const int s0 = int(int64_t(stages) * sp / splits);
   const int s1 = int(int64_t(stages) * (sp + 1) / splits);
   const int n = s1 - s0;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // This thread's rows and segment in load round 0: token row 2 wave + lane / 32,
-  // physical segment lane % 32.
   const int row = 2 * wave + (lane >> 5);
-  const int lseg = (lane & 31) ^ swz(row);
+  const int seg[2] = {((lane & 31) ^ swz(row)) * 16, ((lane & 31) ^ swz(row + 2 * WAVES)) * 16};
   const int64_t row_bytes = d * 2;
-  const char* xb = reinterpret_cast<const char*>(X) + (int64_t(s0) * kRows + row) * row_bytes +
-                   lseg * 16;
+  const char* xb = reinterpret_cast<const char*>(X) + (int64_t(s0) * kRows + row) * row_bytes;
   const char* a = xb + int64_t(ti) * kBlock * 2;
   const char* b = xb + int64_t(tj) * kBlock * 2;
-  const int64_t round_bytes = 16 * row_bytes;
+  const int64_t round_bytes = 2 * WAVES * row_bytes;
   const int64_t stage_bytes = kRows * row_bytes;
 
-  f4 acc[kMB][kNB];
+  f4 acc[C::kMB][C::kNB];
 #pragma unroll
-  for (int mi = 0; mi < kMB; ++mi)
+  for (int mi = 0; mi < C::kMB; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < kNB; ++ni) acc[mi][ni] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int ni = 0; ni < C::kNB; ++ni) acc[mi][ni] = f4{0.f, 0.f, 0.f, 0.f};
   if (n > 0) {
     auto cl = [n](int q) { return q < n ? q : n - 1; };
-    issue(a, b, round_bytes, lds0);
+    issue<C>(a, b, round_bytes, seg, lds0);
     int q = 0;
     for (; q + 1 < n; q += 2) {
       wait_vmcnt<0>();
       __syncthreads();
-      issue(a + (q + 1) * stage_bytes, b + (q + 1) * stage_bytes, round_bytes, lds1);
-      compute(acc, lds0);
+      issue<C>(a + (q + 1) * stage_bytes, b + (q + 1) * stage_bytes, round_bytes, seg, lds1);
+      compute<C>(acc, lds0);
       wait_vmcnt<0>();
       __syncthreads();
-      issue(a + cl(q + 2) * stage_bytes, b + cl(q + 2) * stage_bytes, round_bytes, lds0);
-      compute(acc, lds1);
+      issue<C>(a + cl(q + 2) * stage_bytes, b + cl(q + 2) * stage_bytes, round_bytes, seg, lds0);
+      compute<C>(acc, lds1);
     }
     if (q < n) {
       wait_vmcnt<0>();
       __syncthreads();
-      compute(acc, lds0);
+      compute<C>(acc, lds0);
     }
     wait_vmcnt<0>();
     __syncthreads();
   }
   float* P = part + size_t(sp) * size_t(d) * size_t(d);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
 #pragma unroll
-  for (int mi = 0; mi < kMB; ++mi)
+  for (int mi = 0; mi < C::kMB; ++mi)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int64_t i = int64_t(ti) * kBlock + wm * 64 + mi * 16 + 4 * (lane >> 4) + e;
+      const int64_t i = int64_t(ti) * kBlock + (wm * C::kMB + mi) * 16 + 4 * (lane >> 4) + e;
 #pragma unroll
-      for (int ni = 0; ni < kNB; ++ni) {
-        const int64_t jj = int64_t(tj) * kBlock + wn * 128 + ni * 16 + (lane & 15);
+      for (int ni = 0; ni < C::kNB; ++ni) {
+        const int64_t jj = int64_t(tj) * kBlock + (wn * C::kNB + ni) * 16 + (lane & 15);
         float* q = P + i * d + jj;
         *q = first ? acc[mi][ni][e] : *q + acc[mi][ni][e];
       }
@@ -353,6 +381,8 @@ __global__ void __launch_bounds__(kThreads) k_tail_rows(const uint16_t* X, int64
     out[e] = r < rows ? X[(t0 + r) * d + (e - r * d)] : uint16_t(0);
   }
 }
+
+constexpr int kDirectWaves = 8;  // the layout of k_syrk_direct that the library launches
 
 struct DirectPlan {
   int64_t tiles;
@@ -420,8 +450,8 @@ optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_
     const uint16_t* Xb = static_cast<const uint16_t*>(X);
     int splits = p.splits;
     if (p.full_stages > 0) {
-      hipLaunchKernelGGL(k_syrk_direct, dim3(unsigned(p.tiles * splits)), dim3(dt::kThreads), 0,
-                         s, Xb, d, p.full_stages, splits, part, 1);
+      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(unsigned(p.tiles * splits)),
+                         dim3(64 * kDirectWaves), 0, s, Xb, d, p.full_stages, splits, part, 1);
       OPTIMA_LAUNCH_CHECK();
     } else {
       splits = 1;
@@ -430,8 +460,9 @@ optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_
       hipLaunchKernelGGL(k_tail_rows, dim3(256), dim3(kThreads), 0, s, Xb, d,
                          int64_t(p.full_stages) * dt::kRows, p.tail_rows, tail);
       OPTIMA_LAUNCH_CHECK();
-      hipLaunchKernelGGL(k_syrk_direct, dim3(unsigned(p.tiles)), dim3(dt::kThreads), 0, s, tail,
-                         d, 1, 1, part, p.full_stages > 0 ? 0 : 1);
+      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(unsigned(p.tiles)),
+                         dim3(64 * kDirectWaves), 0, s, tail, d, 1, 1, part,
+                         p.full_stages > 0 ? 0 : 1);
       OPTIMA_LAUNCH_CHECK();
     }
     const int64_t B = ceil_div(d, 64);
