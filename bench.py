@@ -136,7 +136,8 @@ def main() -> int:
     t0 = time.perf_counter()
     X = workloads.x_all(cfg)
     W0 = workloads.w0(cfg)
-    mask = workloads.layer_mask(cfg, W0, workloads.col_sq_norms(cfg, X))
+    col_sq = workloads.col_sq_norms(cfg, X)
+    mask = workloads.layer_mask(cfg, W0, col_sq)
     V0 = workloads.power_start_block(cfg.d, SPECTRAL_BLOCK)
     log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
 
@@ -228,6 +229,34 @@ def main() -> int:
                        "column_iters_per_s": args.fixed_iters * C / (fixed_ms * 1e-3),
                        "product_tflops": fixed_tflops, "product_avg_launch_us": f_launch_us}
 
+    # Device mask selection (the selector ahead of the update; not part of
+    # the step, whose mask is an input): both patterns on this layer's W0 and
+    # fp64 column norms, 5 launches each.
+    csd = torch.from_numpy(col_sq).to(dev)
+    md = torch.empty_like(Md)
+
+    def time_mask(pattern, sparsity, reps=5):
+        L.optima_wanda_mask(W0d, csd, md, pattern, sparsity)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            L.optima_wanda_mask(W0d, csd, md, pattern, sparsity)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    m24_ms = time_mask(L.MASK_2TO4, 0.5)
+    m24_same = bool(torch.equal(md, Md))
+    mun_ms = time_mask(L.MASK_UNSTRUCTURED, 0.5)
+    mask_bytes = 5.0 * C * d  # read W0 (4 B), write the mask (1 B) per element
+    mask_select = {"two_four_ms": m24_ms, "unstructured_50_ms": mun_ms,
+                   "two_four_gbps": mask_bytes / (m24_ms * 1e-3) / 1e9,
+                   "unstructured_gbps": mask_bytes / (mun_ms * 1e-3) / 1e9,
+                   "algorithmic_bytes_per_element": 5,
+                   "two_four_equals_host_mask": m24_same}
+    log(f"mask selection: 2:4 {m24_ms * 1e3:.1f} us, unstructured {mun_ms * 1e3:.1f} us, "
+        f"2:4 equals the host mask: {m24_same}")
+
     traffic = None  # the counter passes were taken on the bf16x3 kernels
     if (TRAFFIC and prec == L.PREC_BF16X3
             and TRAFFIC.get("sources_sha1") == kernel_sources_sha1()):
@@ -286,6 +315,7 @@ def main() -> int:
         "phase_ms": {"hessian": hess_ms, "damp_spectral": spec_ms, "solve": solve_ms},
         "hessian_tflops": 2.0 * N * d * d / 2 / (hess_ms * 1e-3) / 1e12,
         "fixed_batch": fixed_batch,
+        "mask_select": mask_select,
         "peak_device_memory_gib": torch.cuda.max_memory_allocated(dev) / 2**30,
         "roofline": roofline,
     }

@@ -47,6 +47,7 @@ typedef int optima_status;
 
 #define OPTIMA_DTYPE_F32 0
 #define OPTIMA_DTYPE_BF16 1
+#define OPTIMA_DTYPE_F64 2
 
 /* Arithmetic of the solver's per-iteration H-products (optima_solver_opts).
  * FP32: v_mfma_f32_16x16x4_f32, fp32 products and sums.
@@ -132,6 +133,33 @@ optima_status optima_spectral_norm(const float* H, int64_t d, const float* V0,
                                    int block, int max_iters, float tol,
                                    void* ws, size_t ws_bytes, float* lambda_max,
                                    int32_t* iters, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Wanda mask selection -- the mask M that the weight update starts from
+ * (Algorithm 1 takes it from a selector; the configurations use the Wanda
+ * saliency cited in Section 2, with the 2:4 pattern of Section 4).
+ *
+ * W0: [n_cols][d] fp32 (row j = column QP j), 4-byte aligned. col_sq: the
+ * squared input norms c[i] = sum_t X[t][i]^2, element i at col_sq[i * stride],
+ * fp32 (OPTIMA_DTYPE_F32) or fp64 (OPTIMA_DTYPE_F64); e.g. the diagonal of the
+ * undamped Hessian is H with stride d + 1. mask: [n_cols][d] uint8 output
+ * (1 keeps), 4-byte aligned, overlapping neither input.
+ * score[j][i] = W0[j][i]^2 * c[i] in fp64 (the square of the saliency
+ * |W0[j][i]| sqrt(c[i]), same order; exact square, one rounded product).
+ * pattern OPTIMA_MASK_UNSTRUCTURED keeps the d - floor(sparsity * d) highest
+ * scores of every row (0 <= sparsity <= 1); OPTIMA_MASK_2TO4 keeps the two
+ * highest of every group [4g, 4g + 4) of a row (d % 4 == 0). Equal scores go
+ * to the lower index; NaN scores rank below all others; -0 equals +0. The
+ * result is a pure function of the input values: bit-exact against any IEEE
+ * implementation of the same rule. Asynchronous on `stream`.
+ * ------------------------------------------------------------------------- */
+#define OPTIMA_MASK_UNSTRUCTURED 0
+#define OPTIMA_MASK_2TO4 1
+optima_status optima_wanda_mask(const float* W0, int64_t n_cols, int64_t d,
+                                const void* col_sq, int col_sq_dtype,
+                                int64_t col_sq_stride, int pattern,
+                                double sparsity, uint8_t* mask,
+                                hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Batched column-QP solve -- Eq. (6), Algorithm 1, Section 3.3-3.4.

@@ -26,6 +26,12 @@ subspace_iteration
                  lambda_2/lambda_1, which matters for Hessians whose top
                  eigenvalues cluster (outlier channels). b = 1 is
                  power_iteration.
+wanda_mask       The mask the weight update starts from (Algorithm 1 takes M from
+                 a selector; the configurations use Wanda, cited in Section 2,
+                 with the 2:4 pattern of Section 4): score w0_ji^2 c_i in fp64
+                 (the square of the saliency |w0_ji| sqrt(c_i), same order), per
+                 row the d - floor(s d) highest scores, or the two highest of
+                 every group of 4; ties go to the lower index, NaN scores last.
 objective        Eq. (4)/(6): f_j = dw_j^T H dw_j with dw_j = w_j - w0_j.
 closed_form      Eq. (10)-(11): the unconstrained QP over the kept set I has
                  Q = H_II, c = -2 H_IS w_S, so dw_I = H_II^{-1} H_IS w_S and
@@ -64,7 +70,9 @@ hessian, damp, objective, closed_form, kkt_solve: pinned by brute force, exact
 rational arithmetic and closed forms in the CPU tests. power_iteration: pinned
 by LAPACK eigenvalues. subspace_iteration: pinned by LAPACK eigenvalues of
 matrices with known spectra, the Ritz upper bound, a hand-worked 2x2 case and
-its reduction to power_iteration at b = 1. rapdhg: its fixed point is pinned by closed_form and its
+its reduction to power_iteration at b = 1. wanda_mask: pinned by the rank
+definition evaluated by brute force (an entry is kept iff fewer than k
+entries beat it), hand-made ties and the keep counts. rapdhg: its fixed point is pinned by closed_form and its
 iterates by the invariants (pruned entries exactly +0.0, accepted restarts never
 raise the objective, the accelerated O(1/k^2) bound without restarts); the exact
 trajectory (step schedule, restart constants) is the reading above and is
@@ -160,6 +168,41 @@ def subspace_iteration(H: np.ndarray, V0: np.ndarray, max_iters: int = 1000,
             return theta, it
         theta_prev = theta
     return theta, max_iters
+
+
+# ----------------------------------------------------------------------------
+# Mask selection (the input of the weight update)
+# ----------------------------------------------------------------------------
+
+def wanda_mask(W0: np.ndarray, col_sq: np.ndarray, pattern: str, sparsity: float = 0.5):
+    """Wanda mask, rows of W0 = column QPs, uint8 (1 keeps).
+
+    score[j][i] = W0[j][i]^2 * col_sq[i] in fp64 (W0[j][i]^2 is exact). pattern
+    "unstructured" keeps the d - floor(sparsity * d) highest scores of every
+    row; "2:4" keeps the two highest of every group [4g, 4g + 4) of a row.
+    Among equal scores the lower index comes first; NaN scores come last.
+    """
+    W = np.asarray(W0, dtype=np.float64)
+    c = np.asarray(col_sq, dtype=np.float64)
+    score = (W * W) * c[None, :]
+    n, d = W.shape
+    mask = np.zeros((n, d), dtype=np.uint8)
+    idx = np.arange(d)
+    if pattern == "unstructured":
+        keep = d - int(np.floor(sparsity * d))
+        for j in range(n):
+            order = np.lexsort((idx, -score[j]))  # by score descending, then index
+            mask[j, order[:keep]] = 1
+    elif pattern == "2:4":
+        if d % 4:
+            raise ValueError("2:4 needs d divisible by 4")
+        for j in range(n):
+            for g in range(0, d, 4):
+                order = np.lexsort((idx[g:g + 4], -score[j, g:g + 4]))
+                mask[j, g + order[:2]] = 1
+    else:
+        raise ValueError(pattern)
+    return mask
 
 
 # ----------------------------------------------------------------------------

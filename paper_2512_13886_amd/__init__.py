@@ -5,19 +5,19 @@ declared in include/optima.h). This package is its thin Python binding; the
 names match the C entry points. Importing it fails loudly if the library has
 not been built (python -m paper_2512_13886_amd.build).
 """
-from ._lib import (OptimaError, SolverOpts, DTYPE_F32, DTYPE_BF16, PREC_FP32, PREC_BF16X3,
-                   SPECTRAL_MAX_BLOCK, library_path,
+from ._lib import (OptimaError, SolverOpts, DTYPE_F32, DTYPE_BF16, DTYPE_F64, PREC_FP32,
+                   PREC_BF16X3, SPECTRAL_MAX_BLOCK, MASK_UNSTRUCTURED, MASK_2TO4, library_path,
                    optima_status_string, optima_abi_version,
                    optima_hessian_workspace_bytes, optima_hessian_accumulate,
                    optima_hessian_damp, optima_spectral_norm_workspace_bytes,
-                   optima_spectral_norm, optima_qp_workspace_bytes,
+                   optima_spectral_norm, optima_wanda_mask, optima_qp_workspace_bytes,
                    optima_qp_solve_batched)
 
 __all__ = [
-    "OptimaError", "SolverOpts", "DTYPE_F32", "DTYPE_BF16", "PREC_FP32", "PREC_BF16X3",
-    "SPECTRAL_MAX_BLOCK", "library_path",
+    "OptimaError", "SolverOpts", "DTYPE_F32", "DTYPE_BF16", "DTYPE_F64", "PREC_FP32",
+    "PREC_BF16X3", "SPECTRAL_MAX_BLOCK", "MASK_UNSTRUCTURED", "MASK_2TO4", "library_path",
     "optima_status_string", "optima_abi_version", "optima_hessian_workspace_bytes",
     "optima_hessian_accumulate", "optima_hessian_damp",
-    "optima_spectral_norm_workspace_bytes", "optima_spectral_norm",
+    "optima_spectral_norm_workspace_bytes", "optima_spectral_norm", "optima_wanda_mask",
     "optima_qp_workspace_bytes", "optima_qp_solve_batched",
 ]

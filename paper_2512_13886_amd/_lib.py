@@ -23,6 +23,7 @@ OPTIMA_E_WORKSPACE = -4
 OPTIMA_E_UNSUPPORTED = -5
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
+DTYPE_F64 = 2
 PREC_FP32 = 0
 PREC_BF16X3 = 1
 
@@ -78,6 +79,8 @@ _damp = _sig("optima_hessian_damp", _i32, [_vp, _i64, _f32, _vp, _vp])
 _spec_ws = _sig("optima_spectral_norm_workspace_bytes", _sz, [_i64, _i32])
 _spec = _sig("optima_spectral_norm", _i32,
              [_vp, _i64, _vp, _i32, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
+_mask = _sig("optima_wanda_mask", _i32,
+             [_vp, _i64, _i64, _vp, _i32, _i64, _i32, ctypes.c_double, _vp, _vp])
 _opts_default = _sig("optima_solver_opts_default", None, [ctypes.POINTER(_Opts)])
 _qp_ws = _sig("optima_qp_workspace_bytes", _sz, [_i64, _i64])
 _qp_solve = _sig("optima_qp_solve_batched", _i32,
@@ -216,6 +219,33 @@ def optima_spectral_norm(H: torch.Tensor, V0: torch.Tensor, lambda_max: torch.Te
     ws, nbytes = _workspace(optima_spectral_norm_workspace_bytes(d, block), ws, H.device)
     _check(_spec(_ptr(H), d, _ptr(V0), int(block), int(max_iters), float(tol), _ptr(ws), nbytes,
                  _ptr(lambda_max), _ptr(iters), _stream(stream)))
+
+
+MASK_UNSTRUCTURED = 0
+MASK_2TO4 = 1
+
+
+def optima_wanda_mask(W0: torch.Tensor, col_sq: torch.Tensor, mask: torch.Tensor,
+                      pattern: int = MASK_UNSTRUCTURED, sparsity: float = 0.5,
+                      col_sq_stride: int = 1, stream=None) -> None:
+    """Wanda mask of W0 [n_cols, d] into mask [n_cols, d] (uint8, 1 keeps).
+
+    col_sq holds the squared input norms, element i at flat index
+    i * col_sq_stride (float32 or float64); the undamped Hessian H [d, d] with
+    col_sq_stride = d + 1 passes its diagonal."""
+    _need_cuda("W0", W0, torch.float32)
+    _need_cuda("col_sq", col_sq)
+    _need_cuda("mask", mask, torch.uint8)
+    if W0.dim() != 2 or mask.shape != W0.shape:
+        raise ValueError("W0 and mask must be [n_cols, d]")
+    n, d = W0.shape
+    dt = {torch.float32: DTYPE_F32, torch.float64: DTYPE_F64}.get(col_sq.dtype)
+    if dt is None:
+        raise ValueError("col_sq must be float32 or float64")
+    if d > 0 and (d - 1) * int(col_sq_stride) + 1 > col_sq.numel():
+        raise ValueError("col_sq too short for d and the stride")
+    _check(_mask(_ptr(W0), n, d, _ptr(col_sq), dt, int(col_sq_stride), int(pattern),
+                 float(sparsity), _ptr(mask), _stream(stream)))
 
 
 def optima_qp_workspace_bytes(d: int, n_cols: int) -> int:

@@ -11,6 +11,9 @@ size_t spectral_norm_workspace_bytes(int64_t d, int block);
 optima_status spectral_norm(const float* H, int64_t d, const float* V0, int block, int max_iters,
                             float tol, void* ws, float* lambda_max, int32_t* iters,
                             hipStream_t s);
+optima_status wanda_mask(const float* W0, int64_t n_cols, int64_t d, const void* col_sq,
+                         int col_dtype, int64_t col_stride, int pattern, double sparsity,
+                         uint8_t* mask, hipStream_t s);
 size_t qp_workspace_bytes(int64_t d, int64_t n_cols);
 optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const float* W0,
                        const uint8_t* mask, int64_t n_cols, const optima_solver_opts& o, void* ws,
@@ -43,7 +46,7 @@ const char* optima_status_string(optima_status status) {
   }
 }
 
-int optima_abi_version(void) { return 3; }
+int optima_abi_version(void) { return 4; }
 
 size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
   if (n_tok < 0 || d < 1 || d > kMaxDim) return 0;
@@ -91,6 +94,33 @@ optima_status optima_spectral_norm(const float* H, int64_t d, const float* V0, i
   if (!ws || ws_bytes < optima::spectral_norm_workspace_bytes(d, block))
     return OPTIMA_E_WORKSPACE;
   return optima::spectral_norm(H, d, V0, block, max_iters, tol, ws, lambda_max, iters, stream);
+}
+
+optima_status optima_wanda_mask(const float* W0, int64_t n_cols, int64_t d, const void* col_sq,
+                                int col_sq_dtype, int64_t col_sq_stride, int pattern,
+                                double sparsity, uint8_t* mask, hipStream_t stream) {
+  if (d < 1 || d > kMaxDim || n_cols < 0 || n_cols > kMaxCols) return OPTIMA_E_INVAL;
+  if (n_cols == 0) return OPTIMA_OK;
+  if (!W0 || !col_sq || !mask || col_sq_stride < 1) return OPTIMA_E_INVAL;
+  if (col_sq_dtype != OPTIMA_DTYPE_F32 && col_sq_dtype != OPTIMA_DTYPE_F64)
+    return OPTIMA_E_UNSUPPORTED;
+  const size_t csz = col_sq_dtype == OPTIMA_DTYPE_F64 ? 8 : 4;
+  if ((reinterpret_cast<uintptr_t>(W0) & 3) || (reinterpret_cast<uintptr_t>(mask) & 3) ||
+      (reinterpret_cast<uintptr_t>(col_sq) % csz))
+    return OPTIMA_E_INVAL;
+  if (pattern == OPTIMA_MASK_2TO4) {
+    if (d % 4) return OPTIMA_E_INVAL;
+  } else if (pattern == OPTIMA_MASK_UNSTRUCTURED) {
+    if (!(sparsity >= 0.0 && sparsity <= 1.0)) return OPTIMA_E_INVAL;
+  } else {
+    return OPTIMA_E_INVAL;
+  }
+  const size_t mbytes = size_t(n_cols) * size_t(d);
+  if (overlaps(mask, mbytes, W0, mbytes * 4) ||
+      overlaps(mask, mbytes, col_sq, (size_t(d - 1) * size_t(col_sq_stride) + 1) * csz))
+    return OPTIMA_E_INVAL;
+  return optima::wanda_mask(W0, n_cols, d, col_sq, col_sq_dtype, col_sq_stride, pattern,
+                            sparsity, mask, stream);
 }
 
 void optima_solver_opts_default(optima_solver_opts* o) {

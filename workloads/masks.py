@@ -5,8 +5,11 @@ the Wanda saliency |W_ij| * ||X_j||_2 (Section 2, related work), either per
 column (unstructured) or 2-of-4 along d_in (semi-structured, Section 4).
 Convention: mask[j, i] = 1 keeps weight i of column QP j, 0 prunes it (Eq. (1)).
 
-Scores are computed in fp64. Ties go to the lower index, so the mask is a pure
-function of W0 and the column norms.
+Scores are computed in fp64 as W_ij^2 * sum_t X_tj^2, the square of the
+saliency (same order; the square of an fp32 weight is exact in fp64 and one
+correctly rounded product leaves no room for rounding differences between
+implementations). Ties go to the lower index, so the mask is a pure function
+of W0 and the column norms.
 """
 from __future__ import annotations
 
@@ -16,8 +19,9 @@ from .configs import LayerConfig
 
 
 def wanda_scores(W0: np.ndarray, col_sq: np.ndarray) -> np.ndarray:
-    return np.abs(np.asarray(W0, dtype=np.float64)) * np.sqrt(
-        np.asarray(col_sq, dtype=np.float64))[None, :]
+    """Squared Wanda saliency (|W_ij| ||X_j||)^2 = W_ij^2 * col_sq_j in fp64."""
+    W = np.asarray(W0, dtype=np.float64)
+    return (W * W) * np.asarray(col_sq, dtype=np.float64)[None, :]
 
 
 def wanda_unstructured(W0: np.ndarray, col_sq: np.ndarray, sparsity: float) -> np.ndarray:
