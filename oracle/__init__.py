@@ -5,9 +5,9 @@ this package. The product library never does.
 """
 from .optima_oracle import (hessian, damp, power_iteration, subspace_iteration, wanda_mask,
                             objective,
-                            closed_form, kkt_solve, rapdhg, check_decision,
+                            closed_form, kkt_solve, cg, rapdhg, check_decision,
                             SolverOptions, SolveResult)
 
 __all__ = ["hessian", "damp", "power_iteration", "subspace_iteration", "wanda_mask", "objective",
            "closed_form",
-           "kkt_solve", "rapdhg", "check_decision", "SolverOptions", "SolveResult"]
+           "kkt_solve", "cg", "rapdhg", "check_decision", "SolverOptions", "SolveResult"]

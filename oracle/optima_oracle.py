@@ -39,6 +39,14 @@ closed_form      Eq. (10)-(11): the unconstrained QP over the kept set I has
 kkt_solve        Eq. (6) solved through its KKT system (stationarity plus the
                  equality constraints of Eq. (5)) with a dense LU solve; used on
                  tiny d only, as an independent check of closed_form.
+cg               Eq. (7)-(11): with the pruned entries fixed at zero the QP of
+                 Eq. (6) becomes unconstrained in the kept entries, and its
+                 stationarity condition is the linear system
+                 H_KK x_K = (H w0)_K (Eq. (11) written for w instead of dw).
+                 The paper describes this form but solves the constrained one;
+                 this is the textbook conjugate-gradient method (Hestenes and
+                 Stiefel) on that system, column by column, from the same start
+                 point and with the same termination test as rapdhg.
 rapdhg           Section 3.3 / 3.4: the batched restarted accelerated
                  primal-dual hybrid gradient solve of Eq. (6), with the pruned
                  entries fixed through equal lower and upper bounds (Section 3.4
@@ -76,7 +84,11 @@ entries beat it), hand-made ties and the keep counts. rapdhg: its fixed point is
 iterates by the invariants (pruned entries exactly +0.0, accepted restarts never
 raise the objective, the accelerated O(1/k^2) bound without restarts); the exact
 trajectory (step schedule, restart constants) is the reading above and is
-"parity unpinned": the paper prints no trajectory to compare against.
+"parity unpinned": the paper prints no trajectory to compare against. cg:
+pinned by finite termination (|K| steps reach the closed form in exact
+arithmetic; fp64 on small systems to 1e-10), the one-step solution of the
+hand-worked 2x2 case, A-conjugacy of the search directions and the monotone
+decrease of the energy error.
 """
 from __future__ import annotations
 
@@ -319,6 +331,89 @@ def check_decision(s_x: dict, s_a: dict, kkt_restart, kkt_prev, f_anchor, k, t,
             | (k >= opts.beta_artificial * t))
     restart = cond & (s_c["f"] <= f_anchor) if opts.restarts else np.zeros_like(cond)
     return use_x, converged, restart, s_c
+
+
+def cg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, opts: SolverOptions | None = None,
+       observer=None) -> SolveResult:
+    """Conjugate gradients on H_KK x_K = (H w0)_K for every row of W0.
+
+    Start x = sel(mask, w0, 0), r = P (H w0 - H x), p = r (P keeps the kept
+    entries). Iteration: q = P H p, alpha = r.r / p.q, x += alpha p,
+    r -= alpha q, beta = r'.r' / r.r, p = r' + beta p (alpha = beta = 0 once
+    r.r = 0). Every `check_every` iterations and at max_iters, x is tested with
+    rapdhg's termination rule (r_d, gap against the Appendix D tolerances).
+    Only max_iters, check_every, fixed_iters, eps_rel and eps_abs of `opts`
+    apply. `observer(t, x, p)` sees the iterates after every iteration.
+    """
+    opts = opts or SolverOptions()
+    H = np.asarray(H, dtype=np.float64)
+    W0 = np.asarray(W0, dtype=np.float64)
+    keep = np.asarray(mask) != 0
+    n, d = W0.shape
+
+    x = np.where(keep, W0, 0.0)
+    Hw0 = W0 @ H
+    c_norm = np.linalg.norm(2.0 * Hw0, axis=1)
+    w0Hw0 = np.sum(W0 * Hw0, axis=1)
+    r = np.where(keep, Hw0 - x @ H, 0.0)
+    p = r.copy()
+    rr = np.sum(r * r, axis=1)
+
+    done = np.zeros(n, dtype=bool)
+    out = {"W": np.zeros_like(W0), "iters": np.zeros(n, dtype=np.int64),
+           "converged": np.zeros(n, dtype=bool), "f_final": np.zeros(n),
+           "kkt_final": np.zeros(n)}
+
+    def test(Z):
+        s = _score(H, W0, keep, Z)
+        P, D = s["f"], -s["zHz"] + w0Hw0
+        conv = ((s["rd"] <= opts.eps_abs + opts.eps_rel * c_norm)
+                & (s["gap"] <= opts.eps_abs + opts.eps_rel * (np.abs(P) + np.abs(D))))
+        return s, conv
+
+    def finish(rows, s, t, conv):
+        out["W"][rows] = x[rows]
+        out["iters"][rows] = t
+        out["converged"][rows] = conv[rows]
+        out["f_final"][rows] = s["f"][rows]
+        out["kkt_final"][rows] = s["kkt"][rows]
+        done[rows] = True
+
+    s0, conv0 = test(x)
+    f_initial = s0["f"].copy()
+    if opts.max_iters <= 0:
+        finish(np.ones(n, dtype=bool), s0, 0, conv0)
+    elif not opts.fixed_iters:
+        finish(conv0, s0, 0, conv0)
+
+    t = 0
+    while t < opts.max_iters and not done.all():
+        act = ~done
+        q = np.where(keep, p @ H, 0.0)
+        pq = np.sum(p * q, axis=1)
+        alpha = np.where(rr > 0.0, rr / np.where(pq > 0.0, pq, 1.0), 0.0)
+        x_new = x + alpha[:, None] * p
+        r_new = r - alpha[:, None] * q
+        rr_new = np.sum(r_new * r_new, axis=1)
+        beta = np.where(rr > 0.0, rr_new / np.where(rr > 0.0, rr, 1.0), 0.0)
+        p_new = r_new + beta[:, None] * p
+        x[act], r[act], p[act], rr[act] = x_new[act], r_new[act], p_new[act], rr_new[act]
+        t += 1
+        if observer is not None:
+            observer(t, x, p)
+        if t % opts.check_every and t != opts.max_iters:
+            continue
+        s, conv = test(x)
+        if not opts.fixed_iters:
+            stop = act & conv
+            finish(stop, s, t, conv)
+            act = act & ~stop
+        if t == opts.max_iters:
+            finish(act, s, t, conv)
+
+    return SolveResult(W=out["W"], iters=out["iters"], restarts=np.zeros(n, dtype=np.int64),
+                       converged=out["converged"], f_initial=f_initial,
+                       f_final=out["f_final"], kkt_final=out["kkt_final"])
 
 
 def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
