@@ -157,6 +157,8 @@ def main() -> int:
     qws = torch.empty(L.optima_qp_workspace_bytes(d, C), dtype=torch.uint8, device=dev)
     iters = torch.zeros(C, dtype=torch.int32, device=dev)
     conv = torch.zeros(C, dtype=torch.uint8, device=dev)
+    f_init = torch.zeros(C, dtype=torch.float32, device=dev)
+    f_fin = torch.zeros(C, dtype=torch.float32, device=dev)
     # Table 8: tol 0.01 / 0.01, 100000 iterations
     opts = L.SolverOpts.default()
     if args.precision is not None:
@@ -175,7 +177,8 @@ def main() -> int:
         L.optima_spectral_norm(H, V0d, lmax, max_iters=1000, tol=1e-6, ws=sws)
         ev[2].record()
         info = L.optima_qp_solve_batched(H, lmax, W0d, Md, Wout, opts=opts, ws=qws,
-                                         stats={"iters": iters, "converged": conv})
+                                         stats={"iters": iters, "converged": conv,
+                                                "f_initial": f_init, "f_final": f_fin})
         ev[3].record()
         return ev, info
 
@@ -203,10 +206,41 @@ def main() -> int:
     achieved = flops / (prod_ms * 1e-3) / 1e12
     avg_launch_us = prod_ms * 1e3 / launches
     per_col_it = iters.cpu().numpy()
+    f_ratio_rapdhg = float(f_fin.double().sum() / f_init.double().sum())
     log(f"step {ms_step:.1f} ms: hessian {hess_ms:.2f} ms, damp+spectral {spec_ms:.2f} ms, "
         f"solve {solve_ms:.1f} ms ({it:.0f} iterations, {conv.sum().item()}/{C} converged, "
         f"per-column iterations {per_col_it.min()}..{per_col_it.max()})")
     log(f"H-product: {launches} launches, avg {avg_launch_us:.1f} us, {achieved:.1f} TFLOP/s")
+
+    # Unconstrained-form leg (Eq. (7)-(11)): conjugate gradients on the same
+    # layer and H at the same tolerances, tested every 8 iterations; no step
+    # size is needed. Not part of the timed step.
+    cg_opts = L.SolverOpts.default(method=L.METHOD_CG, check_every=8)
+    if args.precision is not None:
+        cg_opts.precision = prec
+    cg_ms, cg_it = [], []
+    for rep in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        cinfo = L.optima_qp_solve_batched(H, None, W0d, Md, Wout, opts=cg_opts, ws=qws,
+                                          stats={"iters": iters, "converged": conv,
+                                                 "f_initial": f_init, "f_final": f_fin})
+        b.record()
+        torch.cuda.synchronize()
+        if rep:  # the first run is a warm-up
+            cg_ms.append(a.elapsed_time(b))
+            cg_it.append(cinfo["iterations"])
+    cg_solve_ms = float(np.mean(cg_ms))
+    cg_leg = {"solve_ms": cg_solve_ms, "iterations": float(np.mean(cg_it)), "check_every": 8,
+              "converged": int(conv.sum().item()),
+              "columns_per_s_solve_only": C / (cg_solve_ms * 1e-3),
+              "step_ms_equivalent": hess_ms + cg_solve_ms,
+              "columns_per_s_step_equivalent": C / ((hess_ms + cg_solve_ms) * 1e-3),
+              "f_final_over_f_initial": float(f_fin.double().sum() / f_init.double().sum()),
+              "rapdhg_f_final_over_f_initial": f_ratio_rapdhg}
+    log(f"cg: solve {cg_solve_ms:.2f} ms ({cg_leg['iterations']:.0f} iterations, "
+        f"{cg_leg['converged']}/{C} converged); sum f_final / sum f_initial "
+        f"cg {cg_leg['f_final_over_f_initial']:.4f}, rapdhg {f_ratio_rapdhg:.4f}")
 
     # Full-batch leg: all 4096 columns for a fixed number of iterations, the
     # iteration rate at B = C (not part of the timed step).
@@ -316,6 +350,7 @@ def main() -> int:
         "hessian_tflops": 2.0 * N * d * d / 2 / (hess_ms * 1e-3) / 1e12,
         "fixed_batch": fixed_batch,
         "mask_select": mask_select,
+        "cg_unconstrained": cg_leg,
         "peak_device_memory_gib": torch.cuda.max_memory_allocated(dev) / 2**30,
         "roofline": roofline,
     }

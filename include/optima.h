@@ -62,6 +62,22 @@ typedef int optima_status;
 #define OPTIMA_PREC_FP32 0
 #define OPTIMA_PREC_BF16X3 1
 
+/* Solve method (optima_solver_opts.method).
+ * RAPDHG: the paper's batched restarted accelerated method on the constrained
+ *   form, Eq. (6) (described with optima_qp_solve_batched below).
+ * CG: the unconstrained form of Eq. (7)-(11). With the pruned entries fixed
+ *   at zero the optimum solves H_KK x_K = (H w0)_K for every column, which
+ *   conjugate gradients reach without restarts or a step size: from
+ *   x = sel(mask, w0, +0), r = P (H w0 - H x), p = r, each iteration forms
+ *   q = H p (one batched product), alpha = r.r / p.q_K, x += alpha p,
+ *   r -= alpha q_K, beta = r'.r' / r.r, p = r' + beta p, with x, r and p exactly
+ *   zero off K. Columns are tested every check_every iterations with the same
+ *   rule as RAPDHG, evaluated from the recurrence residual (r_d = 2 ||r_K||,
+ *   gap = 2 |x.r|); lambda_max, the beta_* constants, step_safety and
+ *   restarts are unused (lambda_max may be NULL). */
+#define OPTIMA_METHOD_RAPDHG 0
+#define OPTIMA_METHOD_CG 1
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* optima_status_string(optima_status status);
 
@@ -192,7 +208,9 @@ optima_status optima_wanda_mask(const float* W0, int64_t n_cols, int64_t d,
  * be NULL): per column iterations run, accepted restarts, convergence flag,
  * objective at the start point sel(mask, w0, 0), objective and KKT of W_out
  * (computed on the device from the maintained products). info (host, may be
- * NULL) receives run totals. ws: optima_qp_workspace_bytes(d, n_cols) bytes.
+ * NULL) receives run totals (for CG the timed window of each run of
+ * iterations also covers their CG update kernels). ws:
+ * optima_qp_workspace_bytes(d, n_cols) bytes.
  * Blocking: the call synchronises `stream` once per check to learn how many
  * columns are still active. Non-convergence is not an error; it is reported
  * per column. Returns OPTIMA_E_NONFINITE if H or W0 holds NaN/Inf or
@@ -210,6 +228,7 @@ typedef struct {
   float step_safety;      /* default 1e-3 */
   int32_t restarts;       /* 0 disables restarts; default 1 */
   int32_t precision;      /* OPTIMA_PREC_BF16X3 (default) or OPTIMA_PREC_FP32 */
+  int32_t method;         /* OPTIMA_METHOD_RAPDHG (default) or OPTIMA_METHOD_CG */
 } optima_solver_opts;
 
 typedef struct {

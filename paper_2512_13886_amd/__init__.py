@@ -6,7 +6,8 @@ names match the C entry points. Importing it fails loudly if the library has
 not been built (python -m paper_2512_13886_amd.build).
 """
 from ._lib import (OptimaError, SolverOpts, DTYPE_F32, DTYPE_BF16, DTYPE_F64, PREC_FP32,
-                   PREC_BF16X3, SPECTRAL_MAX_BLOCK, MASK_UNSTRUCTURED, MASK_2TO4, library_path,
+                   PREC_BF16X3, SPECTRAL_MAX_BLOCK, MASK_UNSTRUCTURED, MASK_2TO4, METHOD_RAPDHG,
+                   METHOD_CG, library_path,
                    optima_status_string, optima_abi_version,
                    optima_hessian_workspace_bytes, optima_hessian_accumulate,
                    optima_hessian_damp, optima_spectral_norm_workspace_bytes,
@@ -15,7 +16,8 @@ from ._lib import (OptimaError, SolverOpts, DTYPE_F32, DTYPE_BF16, DTYPE_F64, PR
 
 __all__ = [
     "OptimaError", "SolverOpts", "DTYPE_F32", "DTYPE_BF16", "DTYPE_F64", "PREC_FP32",
-    "PREC_BF16X3", "SPECTRAL_MAX_BLOCK", "MASK_UNSTRUCTURED", "MASK_2TO4", "library_path",
+    "PREC_BF16X3", "SPECTRAL_MAX_BLOCK", "MASK_UNSTRUCTURED", "MASK_2TO4", "METHOD_RAPDHG",
+    "METHOD_CG", "library_path",
     "optima_status_string", "optima_abi_version", "optima_hessian_workspace_bytes",
     "optima_hessian_accumulate", "optima_hessian_damp",
     "optima_spectral_norm_workspace_bytes", "optima_spectral_norm", "optima_wanda_mask",

@@ -24,6 +24,8 @@ OPTIMA_E_UNSUPPORTED = -5
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 DTYPE_F64 = 2
+METHOD_RAPDHG = 0
+METHOD_CG = 1
 PREC_FP32 = 0
 PREC_BF16X3 = 1
 
@@ -48,7 +50,7 @@ class _Opts(ctypes.Structure):
                 ("eps_abs", ctypes.c_float), ("beta_sufficient", ctypes.c_float),
                 ("beta_necessary", ctypes.c_float), ("beta_artificial", ctypes.c_float),
                 ("step_safety", ctypes.c_float), ("restarts", ctypes.c_int32),
-                ("precision", ctypes.c_int32)]
+                ("precision", ctypes.c_int32), ("method", ctypes.c_int32)]
 
 
 class _Stats(ctypes.Structure):
@@ -146,6 +148,7 @@ class SolverOpts:
     step_safety: float = 0.0
     restarts: int = 0
     precision: int = 0
+    method: int = 0
 
     @classmethod
     def default(cls, **overrides) -> "SolverOpts":
@@ -252,17 +255,19 @@ def optima_qp_workspace_bytes(d: int, n_cols: int) -> int:
     return int(_qp_ws(d, n_cols))
 
 
-def optima_qp_solve_batched(H: torch.Tensor, lambda_max: torch.Tensor, W0: torch.Tensor,
+def optima_qp_solve_batched(H: torch.Tensor, lambda_max: torch.Tensor | None, W0: torch.Tensor,
                             mask: torch.Tensor, W_out: torch.Tensor,
                             opts: SolverOpts | None = None, ws: torch.Tensor | None = None,
                             stats: dict | None = None, stream=None) -> dict:
     """Solves every row QP of W0 under `mask`; returns the run totals.
 
-    stats: optional dict of device tensors with keys among iters (int32),
-    restarts (int32), converged (uint8), f_initial, f_final, kkt_final (float32).
+    lambda_max may be None with opts.method == METHOD_CG. stats: optional dict
+    of device tensors with keys among iters (int32), restarts (int32),
+    converged (uint8), f_initial, f_final, kkt_final (float32).
     """
     _need_cuda("H", H, torch.float32)
-    _need_cuda("lambda_max", lambda_max, torch.float32)
+    if lambda_max is not None:
+        _need_cuda("lambda_max", lambda_max, torch.float32)
     _need_cuda("W0", W0, torch.float32)
     _need_cuda("mask", mask, torch.uint8)
     _need_cuda("W_out", W_out, torch.float32)

@@ -46,7 +46,7 @@ const char* optima_status_string(optima_status status) {
   }
 }
 
-int optima_abi_version(void) { return 4; }
+int optima_abi_version(void) { return 5; }
 
 size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
   if (n_tok < 0 || d < 1 || d > kMaxDim) return 0;
@@ -136,6 +136,7 @@ void optima_solver_opts_default(optima_solver_opts* o) {
   o->step_safety = 1e-3f;
   o->restarts = 1;
   o->precision = OPTIMA_PREC_BF16X3;
+  o->method = OPTIMA_METHOD_RAPDHG;
 }
 
 size_t optima_qp_workspace_bytes(int64_t d, int64_t n_cols) {
@@ -151,7 +152,10 @@ optima_status optima_qp_solve_batched(const float* H, int64_t d, const float* la
   if (!opts || d < 1 || d > kMaxDim || n_cols < 0 || n_cols > kMaxCols) return OPTIMA_E_INVAL;
   if (info) *info = optima_solve_info{};
   if (n_cols == 0) return OPTIMA_OK;
-  if (!H || !lambda_max || !W0 || !mask || !W_out) return OPTIMA_E_INVAL;
+  if (opts->method != OPTIMA_METHOD_RAPDHG && opts->method != OPTIMA_METHOD_CG)
+    return OPTIMA_E_INVAL;
+  if (!H || !W0 || !mask || !W_out) return OPTIMA_E_INVAL;
+  if (!lambda_max && opts->method == OPTIMA_METHOD_RAPDHG) return OPTIMA_E_INVAL;
   if (!optima::aligned16(H) || (reinterpret_cast<uintptr_t>(W0) & 3) ||
       (reinterpret_cast<uintptr_t>(W_out) & 3))
     return OPTIMA_E_INVAL;

@@ -499,6 +499,146 @@ __global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Conjugate gradients on the unconstrained form (OPTIMA_METHOD_CG)
+// ---------------------------------------------------------------------------
+// With the pruned entries fixed at zero, Eq. (6) is unconstrained in the kept
+// entries K and its optimum solves H_KK x_K = (H w0)_K (Eq. (11) written for
+// w). Per column: r = P (H w0 - H x0), p = r; each iteration q = H p (one
+// batched product), alpha = r.r / p.q_K, x += alpha p, r -= alpha q_K,
+// beta = r'.r' / r.r, p = r' + beta p. Entries outside K stay exactly 0 in
+// x, r and p. Buffers: x = X0, r = XA, p = X1 (split planes XP0), q = HA,
+// r.r per column in st.kkt_prev (fp64).
+struct CgArgs {
+  const int* rows;
+  int n_rows;
+  int dp, d;
+  float* X;
+  float* R;
+  float* P;
+  uint16_t* PP;      // split planes of p (kPrecBf16x3), else NULL
+  const float* Q;    // H p
+  const float* HX;   // H x0 (initialisation)
+  const float* HW0;
+  const uint8_t* mask;
+  double* rr;
+};
+
+__global__ void __launch_bounds__(kThreads) k_cg_init(CgArgs a) {
+  __shared__ double red[kThreads / 64];
+  const int r = blockIdx.x;
+  if (r >= a.n_rows) return;
+  const int j = a.rows ? a.rows[r] : r;
+  const size_t base = size_t(j) * a.dp;
+  double s = 0.0;
+  for (int n = threadIdx.x; n < a.dp; n += kThreads) {
+    const bool keep = n < a.d && a.mask[size_t(j) * a.d + n] != 0;
+    const float v = keep ? a.HW0[base + n] - a.HX[base + n] : 0.f;
+    a.R[base + n] = v;
+    a.P[base + n] = v;
+    if (a.PP) store_split(a.PP + base * 2, n, v);
+    s += double(v) * double(v);
+  }
+  s = block_sum(s, red);
+  if (threadIdx.x == 0) a.rr[j] = s;
+}
+
+// One CG iteration of one active column (one workgroup per column).
+__global__ void __launch_bounds__(kThreads) k_cg_step(CgArgs a) {
+  __shared__ double red[kThreads / 64];
+  const int r = blockIdx.x;
+  if (r >= a.n_rows) return;
+  const int j = a.rows ? a.rows[r] : r;
+  const size_t base = size_t(j) * a.dp;
+  const uint8_t* m = a.mask + size_t(j) * a.d;
+  double pq = 0.0;
+  for (int n = threadIdx.x; n < a.d; n += kThreads)
+    if (m[n]) pq += double(a.P[base + n]) * double(a.Q[base + n]);
+  pq = block_sum(pq, red);
+  const double rr = a.rr[j];
+  const float alpha = float(rr > 0.0 && pq > 0.0 ? rr / pq : 0.0);
+  double rr2 = 0.0;
+  for (int n = threadIdx.x; n < a.d; n += kThreads) {
+    if (!m[n]) continue;
+    const size_t o = base + n;
+    a.X[o] = a.X[o] + alpha * a.P[o];
+    const float rn = a.R[o] - alpha * a.Q[o];
+    a.R[o] = rn;
+    rr2 += double(rn) * double(rn);
+  }
+  rr2 = block_sum(rr2, red);
+  const float beta = float(rr > 0.0 ? rr2 / rr : 0.0);
+  for (int n = threadIdx.x; n < a.d; n += kThreads) {
+    if (!m[n]) continue;
+    const size_t o = base + n;
+    const float pn = a.R[o] + beta * a.P[o];
+    a.P[o] = pn;
+    if (a.PP) store_split(a.PP + base * 2, n, pn);
+  }
+  if (threadIdx.x == 0) a.rr[j] = rr2;
+}
+
+// Termination test of the CG iterate with the rAPDHG rule. With x = 0 off K:
+// g_K = -2 r_K, so r_d = 2 ||r_K||, gap = 2 |x.r|, x^T H x = x.Hw0 - x.r and
+// f(x) = w0^T H w0 - x.Hw0 - x.r (sums over K).
+struct CgCheckArgs {
+  const int* rows;
+  int n_rows;
+  int dp, d;
+  const float* X;
+  const float* R;
+  const float* HW0;
+  const uint8_t* mask;
+  ColState st;
+  int64_t t;
+  int final_check;
+  optima_solver_opts o;
+  float* W_out;
+  optima_solve_stats stats;
+};
+
+__global__ void __launch_bounds__(kThreads) k_cg_check(CgCheckArgs a) {
+  __shared__ double red[kThreads / 64];
+  __shared__ int stop;
+  const int r = blockIdx.x;
+  if (r >= a.n_rows) return;
+  const int j = a.rows ? a.rows[r] : r;
+  const size_t base = size_t(j) * a.dp;
+  const uint8_t* m = a.mask + size_t(j) * a.d;
+  double rr = 0.0, xr = 0.0, xh = 0.0;
+  for (int n = threadIdx.x; n < a.d; n += kThreads) {
+    if (!m[n]) continue;
+    const double x = a.X[base + n], rv = a.R[base + n];
+    rr += rv * rv;
+    xr += x * rv;
+    xh += x * double(a.HW0[base + n]);
+  }
+  rr = block_sum(rr, red);
+  xr = block_sum(xr, red);
+  xh = block_sum(xh, red);
+  if (threadIdx.x == 0) {
+    const optima_solver_opts& o = a.o;
+    const double rd = 2.0 * sqrt(rr), gap = 2.0 * fabs(xr);
+    const double w0hw0 = a.st.w0hw0[j];
+    const double f = w0hw0 - xh - xr, D = w0hw0 - (xh - xr);
+    const bool conv = rd <= double(o.eps_abs) + double(o.eps_rel) * a.st.c_norm[j] &&
+                      gap <= double(o.eps_abs) + double(o.eps_rel) * (fabs(f) + fabs(D));
+    const bool st_ = (conv && !o.fixed_iters) || a.final_check;
+    if (st_) {
+      a.st.done[j] = 1;
+      if (a.stats.iters) a.stats.iters[j] = int(a.t);
+      if (a.stats.restarts) a.stats.restarts[j] = 0;
+      if (a.stats.converged) a.stats.converged[j] = conv ? 1 : 0;
+      if (a.stats.f_final) a.stats.f_final[j] = float(f);
+      if (a.stats.kkt_final) a.stats.kkt_final[j] = float(sqrt(rd * rd + gap * gap));
+    }
+    stop = st_ ? 1 : 0;
+  }
+  __syncthreads();
+  if (stop)
+    for (int n = threadIdx.x; n < a.d; n += kThreads) a.W_out[size_t(j) * a.d + n] = a.X[base + n];
+}
+
 // Stable compaction of the active list: keeps the columns not yet done.
 __global__ void __launch_bounds__(1024) k_compact(const int* rows_in, int n_in, const int* done,
                                                   int* rows_out, int* n_out) {
@@ -645,6 +785,85 @@ optima_status launch_product(const ProductArgs& p, const Layout& l, int prec, hi
                              : launch_product<MODE, kPrecF32>(p, l, s);
 }
 
+
+// The CG iteration loop (after setup, the initial check and compaction).
+optima_status cg_loop(const Layout& l, ProductArgs p, int dp, int di, const uint8_t* mask,
+                      const optima_solver_opts& o, float* W_out,
+                      const optima_solve_stats& stats, optima_solve_info& inf, hipEvent_t* ev,
+                      bool timed, int n_act, hipStream_t s) {
+  const bool split = o.precision == kPrecBf16x3;
+  CgArgs cg{};
+  cg.dp = dp;
+  cg.d = di;
+  cg.X = l.X0;
+  cg.R = l.XA;
+  cg.P = l.X1;
+  cg.PP = split ? l.XP0 : nullptr;
+  cg.Q = l.HA;
+  cg.HX = l.HX;
+  cg.HW0 = l.HW0;
+  cg.mask = mask;
+  cg.rr = l.st.kkt_prev;
+  CgCheckArgs ck{};
+  ck.dp = dp;
+  ck.d = di;
+  ck.X = l.X0;
+  ck.R = l.XA;
+  ck.HW0 = l.HW0;
+  ck.mask = mask;
+  ck.st = l.st;
+  ck.o = o;
+  ck.W_out = W_out;
+  ck.stats = stats;
+  p.A = l.X1;
+  p.Ap = l.XP0;
+  p.out1 = l.HA;
+  int* rows = l.rows0;
+  int* rows_next = l.rows1;
+  int64_t t = 0;
+  const int64_t ce = o.check_every;
+  while (t < o.max_iters && n_act > 0) {
+    const int64_t t_next = std::min<int64_t>((t / ce + 1) * ce, o.max_iters);
+    const int n = int(t_next - t);
+    p.rows = rows;
+    p.n_rows = n_act;
+    cg.rows = rows;
+    cg.n_rows = n_act;
+    if (timed) OPTIMA_HIP_TRY(hipEventRecord(ev[0], s));
+    for (int i = 0; i < n; ++i) {
+      if (auto e = launch_product<kPlain>(p, l, o.precision, s)) return e;
+      hipLaunchKernelGGL(k_cg_step, dim3(unsigned(n_act)), dim3(kThreads), 0, s, cg);
+      OPTIMA_LAUNCH_CHECK();
+    }
+    if (timed) OPTIMA_HIP_TRY(hipEventRecord(ev[1], s));
+    inf.gemm_calls += n;
+    inf.row_products += int64_t(n) * n_act;
+    inf.timed_launches += n;
+    inf.timed_row_products += int64_t(n) * n_act;
+    t = t_next;
+    ck.rows = rows;
+    ck.n_rows = n_act;
+    ck.t = t;
+    ck.final_check = t == o.max_iters;
+    hipLaunchKernelGGL(k_cg_check, dim3(unsigned(n_act)), dim3(kThreads), 0, s, ck);
+    OPTIMA_LAUNCH_CHECK();
+    inf.checks += 1;
+    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, rows, n_act, l.st.done, rows_next,
+                       l.n_active);
+    OPTIMA_LAUNCH_CHECK();
+    std::swap(rows, rows_next);
+    OPTIMA_HIP_TRY(hipMemcpyAsync(&n_act, l.n_active, sizeof(int), hipMemcpyDeviceToHost, s));
+    OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+    if (timed) {
+      float ms = 0.f;
+      OPTIMA_HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));
+      inf.timed_product_ms += ms;
+    }
+  }
+  inf.iterations = t;
+  return OPTIMA_OK;
+}
+
 }  // namespace
 
 size_t qp_workspace_bytes(int64_t d, int64_t n_cols) {
@@ -671,8 +890,12 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     OPTIMA_LAUNCH_CHECK();
     if (l.pad_h) Hm = l.Hp;
   }
-  hipLaunchKernelGGL(k_step_constant, dim3(1), dim3(1), 0, s, lambda_max, o.step_safety, l.L, l.flags);
-  OPTIMA_LAUNCH_CHECK();
+  const bool use_cg = o.method == OPTIMA_METHOD_CG;
+  if (!use_cg) {  // CG needs no step size
+    hipLaunchKernelGGL(k_step_constant, dim3(1), dim3(1), 0, s, lambda_max, o.step_safety, l.L,
+                       l.flags);
+    OPTIMA_LAUNCH_CHECK();
+  }
   const dim3 vec_grid(unsigned(nc), unsigned(ceil_div(dp, 4 * kThreads)));
   // W0 padded copy goes to HX first; Hw0 = H w0, then Hx = Hx_ag = H x0.
   const bool split = o.precision == kPrecBf16x3;
@@ -740,6 +963,22 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   hipLaunchKernelGGL(k_check, dim3(nc), dim3(kThreads), 0, s, ca);
   OPTIMA_LAUNCH_CHECK();
   inf.checks += 1;
+  if (use_cg) {
+    CgArgs ci{};
+    ci.rows = nullptr;
+    ci.n_rows = nc;
+    ci.dp = dp;
+    ci.d = di;
+    ci.R = l.XA;
+    ci.P = l.X1;
+    ci.PP = split ? l.XP0 : nullptr;
+    ci.HX = l.HX;
+    ci.HW0 = l.HW0;
+    ci.mask = mask;
+    ci.rr = l.st.kkt_prev;
+    hipLaunchKernelGGL(k_cg_init, dim3(unsigned(nc)), dim3(kThreads), 0, s, ci);
+    OPTIMA_LAUNCH_CHECK();
+  }
   hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, (const int*)nullptr, nc, l.st.done,
                      l.rows0, l.n_active);
   OPTIMA_LAUNCH_CHECK();
@@ -763,6 +1002,14 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
       if (e[1]) (void)hipEventDestroy(e[1]);
     }
   } guard{ev};
+
+  if (use_cg) {
+    const optima_status e = cg_loop(l, p, dp, di, mask, o, W_out, stats, inf, ev, info != nullptr,
+                                    n_act, s);
+    if (e) return e;
+    if (info) *info = inf;
+    return OPTIMA_OK;
+  }
 
   int* rows = l.rows0;
   int* rows_next = l.rows1;

@@ -52,6 +52,7 @@ def test_default_options_follow_table_8():
     assert o.eps_rel == pytest.approx(0.01) and o.eps_abs == pytest.approx(0.01)
     assert o.restarts == 1 and o.fixed_iters == 0
     assert o.precision == L.PREC_BF16X3
+    assert o.method == L.METHOD_RAPDHG
 
 
 def test_workspace_queries():
