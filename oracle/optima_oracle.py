@@ -32,6 +32,13 @@ wanda_mask       The mask the weight update starts from (Algorithm 1 takes M fro
                  (the square of the saliency |w0_ji| sqrt(c_i), same order), per
                  row the d - floor(s d) highest scores, or the two highest of
                  every group of 4; ties go to the lower index, NaN scores last.
+jacobi_scale     Shared diagonal preconditioning (not in the paper; a reading,
+                 usual for PDLP-family solvers): D = diag(H)^(-1/2) and
+                 H' = D H D. The column QPs in y = D^-1 w have Hessian H' and
+                 anchors D^-1 w0, the same zero pattern, the same objective
+                 values and optima y* = D^-1 w*. rapdhg and cg take D as
+                 `scale`: they iterate on the scaled problem, test termination
+                 in the original coordinates and return w = D y.
 objective        Eq. (4)/(6): f_j = dw_j^T H dw_j with dw_j = w_j - w0_j.
 closed_form      Eq. (10)-(11): the unconstrained QP over the kept set I has
                  Q = H_II, c = -2 H_IS w_S, so dw_I = H_II^{-1} H_IS w_S and
@@ -88,7 +95,9 @@ trajectory (step schedule, restart constants) is the reading above and is
 pinned by finite termination (|K| steps reach the closed form in exact
 arithmetic; fp64 on small systems to 1e-10), the one-step solution of the
 hand-worked 2x2 case, A-conjugacy of the search directions and the monotone
-decrease of the energy error.
+decrease of the energy error. jacobi_scale: pinned by the unit diagonal of
+D H D, and by the closed form of the original problem reached through the
+scaled solve.
 """
 from __future__ import annotations
 
@@ -120,6 +129,14 @@ def damp(H: np.ndarray, rel: float = 0.01):
     H = np.asarray(H, dtype=np.float64)
     lam = rel * np.trace(H) / H.shape[0]
     return H + lam * np.eye(H.shape[0]), lam
+
+
+def jacobi_scale(H: np.ndarray):
+    """Return (D H D, D) with D = diag(H)^(-1/2) (entries of H_ii <= 0 get 1)."""
+    H = np.asarray(H, dtype=np.float64)
+    h = np.diag(H)
+    D = np.where(h > 0.0, 1.0 / np.sqrt(np.where(h > 0.0, h, 1.0)), 1.0)
+    return H * np.outer(D, D), D
 
 
 def power_iteration(H: np.ndarray, v0: np.ndarray, max_iters: int = 1000,
@@ -301,12 +318,18 @@ class SolveResult:
     anchors: list = field(default_factory=list)  # per column: f at each accepted restart
 
 
-def _score(H, W0, keep, Z):
-    """Per-row r_d, gap, KKT, f and z^T H z of candidate rows Z."""
+def _score(H, W0, keep, Z, D=None):
+    """Per-row r_d, gap, KKT, f and z^T H z of candidate rows Z.
+
+    With a diagonal scaling D (H, W0 and Z in scaled coordinates), r_d is the
+    norm of the gradient in the original coordinates, D^-1 g; gap, f and
+    z^T H z are the same in both coordinates.
+    """
     dZ = Z - W0
     HdZ = dZ @ H                      # rows of H (z - w0); H is symmetric
     G = 2.0 * HdZ
-    rd = np.sqrt(np.sum(np.where(keep, G, 0.0) ** 2, axis=1))
+    Go = G if D is None else G / D[None, :]
+    rd = np.sqrt(np.sum(np.where(keep, Go, 0.0) ** 2, axis=1))
     gap = np.abs(np.sum(Z * G, axis=1))
     f = np.sum(dZ * HdZ, axis=1)
     zHz = np.sum(Z * (Z @ H), axis=1)
@@ -334,7 +357,7 @@ def check_decision(s_x: dict, s_a: dict, kkt_restart, kkt_prev, f_anchor, k, t,
 
 
 def cg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, opts: SolverOptions | None = None,
-       observer=None) -> SolveResult:
+       observer=None, scale=None) -> SolveResult:
     """Conjugate gradients on H_KK x_K = (H w0)_K for every row of W0.
 
     Start x = sel(mask, w0, 0), r = P (H w0 - H x), p = r (P keeps the kept
@@ -343,17 +366,21 @@ def cg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, opts: SolverOptions | No
     r.r = 0). Every `check_every` iterations and at max_iters, x is tested with
     rapdhg's termination rule (r_d, gap against the Appendix D tolerances).
     Only max_iters, check_every, fixed_iters, eps_rel and eps_abs of `opts`
-    apply. `observer(t, x, p)` sees the iterates after every iteration.
+    apply. `observer(t, x, p)` sees the iterates after every iteration. `scale`
+    works as in rapdhg.
     """
     opts = opts or SolverOptions()
     H = np.asarray(H, dtype=np.float64)
+    D = None if scale is None else np.asarray(scale, dtype=np.float64)
     W0 = np.asarray(W0, dtype=np.float64)
+    if D is not None:
+        W0 = W0 / D[None, :]
     keep = np.asarray(mask) != 0
     n, d = W0.shape
 
     x = np.where(keep, W0, 0.0)
     Hw0 = W0 @ H
-    c_norm = np.linalg.norm(2.0 * Hw0, axis=1)
+    c_norm = np.linalg.norm(2.0 * (Hw0 if D is None else Hw0 / D[None, :]), axis=1)
     w0Hw0 = np.sum(W0 * Hw0, axis=1)
     r = np.where(keep, Hw0 - x @ H, 0.0)
     p = r.copy()
@@ -365,14 +392,14 @@ def cg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, opts: SolverOptions | No
            "kkt_final": np.zeros(n)}
 
     def test(Z):
-        s = _score(H, W0, keep, Z)
-        P, D = s["f"], -s["zHz"] + w0Hw0
+        s = _score(H, W0, keep, Z, D)
+        primal, dual = s["f"], -s["zHz"] + w0Hw0
         conv = ((s["rd"] <= opts.eps_abs + opts.eps_rel * c_norm)
-                & (s["gap"] <= opts.eps_abs + opts.eps_rel * (np.abs(P) + np.abs(D))))
+                & (s["gap"] <= opts.eps_abs + opts.eps_rel * (np.abs(primal) + np.abs(dual))))
         return s, conv
 
     def finish(rows, s, t, conv):
-        out["W"][rows] = x[rows]
+        out["W"][rows] = (x if D is None else x * D[None, :])[rows]
         out["iters"][rows] = t
         out["converged"][rows] = conv[rows]
         out["f_final"][rows] = s["f"][rows]
@@ -417,15 +444,19 @@ def cg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, opts: SolverOptions | No
 
 
 def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
-           opts: SolverOptions | None = None, observer=None) -> SolveResult:
+           opts: SolverOptions | None = None, observer=None, scale=None) -> SolveResult:
     """Solve all column QPs of Eq. (6) side by side (one row of W0 per QP).
 
     `observer(t, x, x_ag)`, if given, sees the iterates after every iteration
-    (before that iteration's check); it must not modify them.
+    (before that iteration's check); it must not modify them. With `scale` = D
+    (see jacobi_scale), H is the scaled D H0 D, lambda_max its largest
+    eigenvalue, W0 and the result stay in the original coordinates.
     """
     opts = opts or SolverOptions()
     H = np.asarray(H, dtype=np.float64)
-    W0 = np.asarray(W0, dtype=np.float64)
+    D = None if scale is None else np.asarray(scale, dtype=np.float64)
+    W0_orig = np.asarray(W0, dtype=np.float64)
+    W0 = W0_orig if D is None else W0_orig / D[None, :]
     keep = np.asarray(mask) != 0
     n, d = W0.shape
     L = 2.0 * float(lambda_max) * (1.0 + opts.step_safety)
@@ -436,7 +467,7 @@ def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
     x = sel(W0)
     xa = x.copy()
     Hw0 = W0 @ H
-    c_norm = np.linalg.norm(2.0 * Hw0, axis=1)
+    c_norm = np.linalg.norm(2.0 * (Hw0 if D is None else Hw0 / D[None, :]), axis=1)
     w0Hw0 = np.sum(W0 * Hw0, axis=1)
 
     k = np.zeros(n, dtype=np.int64)
@@ -447,14 +478,14 @@ def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
            "kkt_final": np.zeros(n)}
     anchors = [[] for _ in range(n)]
 
-    s0 = _score(H, W0, keep, x)
+    s0 = _score(H, W0, keep, x, D)
     f_initial = s0["f"].copy()
     kkt_restart = s0["kkt"].copy()
     kkt_prev = s0["kkt"].copy()
     f_anchor = s0["f"].copy()
 
     def finish(rows, Z, s, t, conv):
-        out["W"][rows] = Z[rows]
+        out["W"][rows] = (Z if D is None else Z * D[None, :])[rows]
         out["iters"][rows] = t
         out["converged"][rows] = conv[rows]
         out["f_final"][rows] = s["f"][rows]
@@ -487,8 +518,8 @@ def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
             observer(t, x, xa)
         if t % opts.check_every and t != opts.max_iters:
             continue
-        s_x = _score(H, W0, keep, x)
-        s_a = _score(H, W0, keep, xa)
+        s_x = _score(H, W0, keep, x, D)
+        s_a = _score(H, W0, keep, xa, D)
         use_x, conv, restart, s_c = check_decision(
             s_x, s_a, kkt_restart, kkt_prev, f_anchor, k, t, c_norm, w0Hw0, opts)
         cand = np.where(use_x[:, None], x, xa)
