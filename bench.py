@@ -242,6 +242,61 @@ def main() -> int:
         f"{cg_leg['converged']}/{C} converged); sum f_final / sum f_initial "
         f"cg {cg_leg['f_final_over_f_initial']:.4f}, rapdhg {f_ratio_rapdhg:.4f}")
 
+    # Preconditioned leg: Jacobi scaling of (a copy of) H, the spectral norm of
+    # D H D and both solvers with the column scaling, at the paper's
+    # tolerances and at a tight one (eps_rel 1e-4, eps_abs 0) beside the
+    # unscaled solves. Not part of the timed step.
+    Hs = torch.empty_like(H)
+    Hs.copy_(H)
+    Ds = torch.empty(d, dtype=torch.float32, device=dev)
+    lmax_s = torch.empty(1, dtype=torch.float32, device=dev)
+    sp_it = torch.zeros(1, dtype=torch.int32, device=dev)
+    stats_d = {"iters": iters, "converged": conv, "f_initial": f_init, "f_final": f_fin}
+
+    def timed_solve(Hm, lm, o):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        inf = L.optima_qp_solve_batched(Hm, lm, W0d, Md, Wout, opts=o, ws=qws, stats=stats_d)
+        b.record()
+        torch.cuda.synchronize()
+        return {"ms": a.elapsed_time(b), "iterations": inf["iterations"],
+                "converged": int(conv.sum().item()),
+                "f_final_over_f_initial": (f_fin.double().sum() / f_init.double().sum()).item()}
+
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e[0].record()
+    L.optima_hessian_jacobi(Hs, Ds)
+    e[1].record()
+    L.optima_spectral_norm(Hs, V0d, lmax_s, max_iters=1000, tol=1e-6, ws=sws, iters=sp_it)
+    e[2].record()
+    torch.cuda.synchronize()
+
+    def o_(**kw):
+        o = L.SolverOpts.default(**kw)
+        if args.precision is not None:
+            o.precision = prec
+        return o
+
+    tight = dict(eps_rel=1e-4, eps_abs=0.0, max_iters=20000)
+    pre = {"scale_ms": e[0].elapsed_time(e[1]), "spectral_ms": e[1].elapsed_time(e[2]),
+           "spectral_passes": int(sp_it.item()),
+           "paper_tolerance": {
+               "rapdhg_scaled": timed_solve(Hs, lmax_s, o_(col_scale=Ds)),
+               "cg_scaled": timed_solve(Hs, None, o_(method=L.METHOD_CG, check_every=8,
+                                                      col_scale=Ds))},
+           "tight_tolerance_eps_rel_1e-4": {
+               "rapdhg": timed_solve(H, lmax, o_(**tight)),
+               "rapdhg_scaled": timed_solve(Hs, lmax_s, o_(col_scale=Ds, **tight)),
+               "cg": timed_solve(H, None, o_(method=L.METHOD_CG, check_every=8, **tight)),
+               "cg_scaled": timed_solve(Hs, None, o_(method=L.METHOD_CG, check_every=8,
+                                                     col_scale=Ds, **tight))}}
+    tt = pre["tight_tolerance_eps_rel_1e-4"]
+    log(f"jacobi-preconditioned: scale {pre['scale_ms']:.2f} ms, spectral {pre['spectral_ms']:.2f} ms "
+        f"({pre['spectral_passes']} passes); tight: rapdhg {tt['rapdhg']['iterations']} -> "
+        f"{tt['rapdhg_scaled']['iterations']} it ({tt['rapdhg']['ms']:.1f} -> "
+        f"{tt['rapdhg_scaled']['ms']:.1f} ms), cg {tt['cg']['iterations']} -> "
+        f"{tt['cg_scaled']['iterations']} it ({tt['cg']['ms']:.1f} -> {tt['cg_scaled']['ms']:.1f} ms)")
+
     # Full-batch leg: all 4096 columns for a fixed number of iterations, the
     # iteration rate at B = C (not part of the timed step).
     fixed_batch = None
@@ -351,6 +406,7 @@ def main() -> int:
         "fixed_batch": fixed_batch,
         "mask_select": mask_select,
         "cg_unconstrained": cg_leg,
+        "jacobi_preconditioned": pre,
         "peak_device_memory_gib": torch.cuda.max_memory_allocated(dev) / 2**30,
         "roofline": roofline,
     }

@@ -118,6 +118,27 @@ optima_status optima_hessian_damp(float* H, int64_t d, float rel_damp,
                                   float* lambda_out, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * Shared diagonal preconditioning (Jacobi). Not in the paper; a reading usual
+ * for PDLP-family first-order solvers. One scaling serves all columns, so the
+ * batching of Algorithm 1 is unchanged.
+ *
+ * H[d][d] fp32 (symmetric, damped) is replaced in place by D H D with
+ * D_i = H_ii^(-1/2) (computed in fp64, rounded to fp32; 1 where H_ii is not
+ * positive and finite), and scale_out[d] (device) receives D. The factor of
+ * entry (i, j) is the fp32 product D_i D_j, so exact symmetry is kept. In the
+ * coordinates y = D^-1 w every column QP of Eq. (6) keeps its zero pattern and
+ * objective values, and its optimum is D^-1 w*. The outlier channels of
+ * transformer layers make H badly scaled (condition numbers of 10^3 - 10^4);
+ * D H D is well conditioned and the solvers need far fewer iterations.
+ * Workflow: damp, optima_hessian_jacobi, optima_spectral_norm on the scaled H,
+ * then optima_qp_solve_batched with opts.col_scale = scale_out: the solver
+ * iterates on the scaled problem, tests termination with the gradient in the
+ * original coordinates and writes W_out in the original coordinates.
+ * ------------------------------------------------------------------------- */
+optima_status optima_hessian_jacobi(float* H, int64_t d, float* scale_out,
+                                    hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Spectral norm of H for the solver's step size (Section 3.3: the first-order
  * method's bottleneck is products with H; its step needs ||Q|| = 2 lambda_max).
  * H must be symmetric positive semi-definite (X^T X + lambda I is), [d][d]
@@ -213,8 +234,9 @@ optima_status optima_wanda_mask(const float* W0, int64_t n_cols, int64_t d,
  * optima_qp_workspace_bytes(d, n_cols) bytes.
  * Blocking: the call synchronises `stream` once per check to learn how many
  * columns are still active. Non-convergence is not an error; it is reported
- * per column. Returns OPTIMA_E_NONFINITE if H or W0 holds NaN/Inf or
- * lambda_max is not a positive finite number.
+ * per column. Returns OPTIMA_E_NONFINITE if H or W0 holds NaN/Inf,
+ * lambda_max is not a positive finite number, or opts.col_scale holds an
+ * entry that is not positive and finite.
  * ------------------------------------------------------------------------- */
 typedef struct {
   int64_t max_iters;      /* >= 0; the paper uses 100000 (Table 8) */
@@ -229,6 +251,9 @@ typedef struct {
   int32_t restarts;       /* 0 disables restarts; default 1 */
   int32_t precision;      /* OPTIMA_PREC_BF16X3 (default) or OPTIMA_PREC_FP32 */
   int32_t method;         /* OPTIMA_METHOD_RAPDHG (default) or OPTIMA_METHOD_CG */
+  const float* col_scale; /* NULL (default), or the [d] device diagonal D of a
+                             preconditioned H = D H0 D (optima_hessian_jacobi);
+                             see "Shared diagonal preconditioning" */
 } optima_solver_opts;
 
 typedef struct {

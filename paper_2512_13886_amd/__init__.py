@@ -10,7 +10,8 @@ from ._lib import (OptimaError, SolverOpts, DTYPE_F32, DTYPE_BF16, DTYPE_F64, PR
                    METHOD_CG, library_path,
                    optima_status_string, optima_abi_version,
                    optima_hessian_workspace_bytes, optima_hessian_accumulate,
-                   optima_hessian_damp, optima_spectral_norm_workspace_bytes,
+                   optima_hessian_damp, optima_hessian_jacobi,
+                   optima_spectral_norm_workspace_bytes,
                    optima_spectral_norm, optima_wanda_mask, optima_qp_workspace_bytes,
                    optima_qp_solve_batched)
 
@@ -19,7 +20,7 @@ __all__ = [
     "PREC_BF16X3", "SPECTRAL_MAX_BLOCK", "MASK_UNSTRUCTURED", "MASK_2TO4", "METHOD_RAPDHG",
     "METHOD_CG", "library_path",
     "optima_status_string", "optima_abi_version", "optima_hessian_workspace_bytes",
-    "optima_hessian_accumulate", "optima_hessian_damp",
+    "optima_hessian_accumulate", "optima_hessian_damp", "optima_hessian_jacobi",
     "optima_spectral_norm_workspace_bytes", "optima_spectral_norm", "optima_wanda_mask",
     "optima_qp_workspace_bytes", "optima_qp_solve_batched",
 ]

@@ -50,7 +50,8 @@ class _Opts(ctypes.Structure):
                 ("eps_abs", ctypes.c_float), ("beta_sufficient", ctypes.c_float),
                 ("beta_necessary", ctypes.c_float), ("beta_artificial", ctypes.c_float),
                 ("step_safety", ctypes.c_float), ("restarts", ctypes.c_int32),
-                ("precision", ctypes.c_int32), ("method", ctypes.c_int32)]
+                ("precision", ctypes.c_int32), ("method", ctypes.c_int32),
+                ("col_scale", ctypes.c_void_p)]
 
 
 class _Stats(ctypes.Structure):
@@ -78,6 +79,7 @@ _hess_ws = _sig("optima_hessian_workspace_bytes", _sz, [_i64, _i64, _i32])
 _hess_acc = _sig("optima_hessian_accumulate", _i32,
                  [_vp, _i32, _i64, _i64, _vp, _i32, _vp, _sz, _vp])
 _damp = _sig("optima_hessian_damp", _i32, [_vp, _i64, _f32, _vp, _vp])
+_jacobi = _sig("optima_hessian_jacobi", _i32, [_vp, _i64, _vp, _vp])
 _spec_ws = _sig("optima_spectral_norm_workspace_bytes", _sz, [_i64, _i32])
 _spec = _sig("optima_spectral_norm", _i32,
              [_vp, _i64, _vp, _i32, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
@@ -149,6 +151,7 @@ class SolverOpts:
     restarts: int = 0
     precision: int = 0
     method: int = 0
+    col_scale: "torch.Tensor | None" = None  # [d] float32 device scaling D, or None
 
     @classmethod
     def default(cls, **overrides) -> "SolverOpts":
@@ -162,7 +165,11 @@ class SolverOpts:
         return o
 
     def _c(self) -> _Opts:
-        return _Opts(**{f.name: getattr(self, f.name) for f in fields(self)})
+        vals = {f.name: getattr(self, f.name) for f in fields(self)}
+        scale = vals.pop("col_scale")
+        c = _Opts(**vals)
+        c.col_scale = None if scale is None else scale.data_ptr()
+        return c
 
 
 def optima_hessian_workspace_bytes(n_tok: int, d: int, dtype: int) -> int:
@@ -193,6 +200,15 @@ def optima_hessian_damp(H: torch.Tensor, rel_damp: float, lambda_out: torch.Tens
 
 
 SPECTRAL_MAX_BLOCK = 16
+
+
+def optima_hessian_jacobi(H: torch.Tensor, scale_out: torch.Tensor, stream=None) -> None:
+    """H <- D H D in place with D = diag(H)^(-1/2); scale_out [d] receives D."""
+    _need_cuda("H", H, torch.float32)
+    _need_cuda("scale_out", scale_out, torch.float32)
+    if H.dim() != 2 or H.shape[0] != H.shape[1] or scale_out.numel() != H.shape[0]:
+        raise ValueError("H must be [d, d] and scale_out [d]")
+    _check(_jacobi(_ptr(H), H.shape[0], _ptr(scale_out), _stream(stream)))
 
 
 def optima_spectral_norm_workspace_bytes(d: int, block: int = 1) -> int:
@@ -275,6 +291,10 @@ def optima_qp_solve_batched(H: torch.Tensor, lambda_max: torch.Tensor | None, W0
     if H.shape != (d, d) or mask.shape != W0.shape or W_out.shape != W0.shape:
         raise ValueError("shape mismatch between H, W0, mask and W_out")
     opts = opts or SolverOpts.default()
+    if opts.col_scale is not None:
+        _need_cuda("opts.col_scale", opts.col_scale, torch.float32)
+        if opts.col_scale.numel() != d:
+            raise ValueError("opts.col_scale must have d entries")
     ws, nbytes = _workspace(optima_qp_workspace_bytes(d, n_cols), ws, W0.device)
     st = _Stats()
     kinds = {"iters": torch.int32, "restarts": torch.int32, "converged": torch.uint8,

@@ -7,6 +7,7 @@ size_t hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype);
 optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_t d, float* H,
                                  int accumulate, void* ws, hipStream_t s);
 optima_status hessian_damp(float* H, int64_t d, float rel, float* lambda_out, hipStream_t s);
+optima_status hessian_jacobi(float* H, int64_t d, float* D, hipStream_t s);
 size_t spectral_norm_workspace_bytes(int64_t d, int block);
 optima_status spectral_norm(const float* H, int64_t d, const float* V0, int block, int max_iters,
                             float tol, void* ws, float* lambda_max, int32_t* iters,
@@ -46,7 +47,7 @@ const char* optima_status_string(optima_status status) {
   }
 }
 
-int optima_abi_version(void) { return 5; }
+int optima_abi_version(void) { return 6; }
 
 size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
   if (n_tok < 0 || d < 1 || d > kMaxDim) return 0;
@@ -76,6 +77,14 @@ optima_status optima_hessian_damp(float* H, int64_t d, float rel_damp, float* la
   if (!H || !lambda_out || d < 1 || d > kMaxDim) return OPTIMA_E_INVAL;
   if (!(rel_damp >= 0.f)) return OPTIMA_E_INVAL;
   return optima::hessian_damp(H, d, rel_damp, lambda_out, stream);
+}
+
+optima_status optima_hessian_jacobi(float* H, int64_t d, float* scale_out, hipStream_t stream) {
+  if (!H || !scale_out || d < 1 || d > kMaxDim) return OPTIMA_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(H) & 3) || (reinterpret_cast<uintptr_t>(scale_out) & 3))
+    return OPTIMA_E_INVAL;
+  if (overlaps(H, size_t(d) * size_t(d) * 4, scale_out, size_t(d) * 4)) return OPTIMA_E_INVAL;
+  return optima::hessian_jacobi(H, d, scale_out, stream);
 }
 
 size_t optima_spectral_norm_workspace_bytes(int64_t d, int block) {
@@ -137,6 +146,7 @@ void optima_solver_opts_default(optima_solver_opts* o) {
   o->restarts = 1;
   o->precision = OPTIMA_PREC_BF16X3;
   o->method = OPTIMA_METHOD_RAPDHG;
+  o->col_scale = nullptr;
 }
 
 size_t optima_qp_workspace_bytes(int64_t d, int64_t n_cols) {
@@ -157,7 +167,8 @@ optima_status optima_qp_solve_batched(const float* H, int64_t d, const float* la
   if (!H || !W0 || !mask || !W_out) return OPTIMA_E_INVAL;
   if (!lambda_max && opts->method == OPTIMA_METHOD_RAPDHG) return OPTIMA_E_INVAL;
   if (!optima::aligned16(H) || (reinterpret_cast<uintptr_t>(W0) & 3) ||
-      (reinterpret_cast<uintptr_t>(W_out) & 3))
+      (reinterpret_cast<uintptr_t>(W_out) & 3) ||
+      (reinterpret_cast<uintptr_t>(opts->col_scale) & 3))
     return OPTIMA_E_INVAL;
   const size_t wbytes = size_t(n_cols) * size_t(d) * sizeof(float);
   if (overlaps(W0, wbytes, W_out, wbytes) || overlaps(H, size_t(d) * d * 4, W_out, wbytes) ||

@@ -146,6 +146,26 @@ __global__ void __launch_bounds__(kThreads) k_hess_reduce(const float* part, int
   }
 }
 
+// Shared diagonal preconditioning: D_i = diag(H)_i^(-1/2) (computed in fp64,
+// 1 where the diagonal is not positive and finite).
+__global__ void __launch_bounds__(kThreads) k_jacobi_d(const float* H, int64_t d, float* D) {
+  const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (i >= d) return;
+  const double h = H[i * d + i];
+  D[i] = (h > 0.0 && isfinite(h)) ? float(1.0 / sqrt(h)) : 1.f;
+}
+
+// H_ij <- H_ij (D_i D_j): the factor is the same product for (i, j) and
+// (j, i), so an exactly symmetric H stays exactly symmetric.
+__global__ void __launch_bounds__(kThreads) k_jacobi_scale(float* H, int64_t d, const float* D) {
+  const int64_t total = d * d;
+  for (int64_t e = int64_t(blockIdx.x) * kThreads + threadIdx.x; e < total;
+       e += int64_t(gridDim.x) * kThreads) {
+    const int64_t i = e / d, j = e - i * d;
+    H[e] = H[e] * (D[i] * D[j]);
+  }
+}
+
 __global__ void __launch_bounds__(1024) k_damp(float* H, int64_t d, float rel, float* lambda_out) {
   __shared__ double red[16];
   double s = 0.0;
@@ -506,6 +526,16 @@ optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_
   const int64_t B = ceil_div(d, 64);
   hipLaunchKernelGGL(k_hess_reduce, dim3(unsigned(B * (B + 1) / 2)), dim3(kThreads), 0, s, part,
                      p.splits, p.dp, d, H, accumulate);
+  OPTIMA_LAUNCH_CHECK();
+  return OPTIMA_OK;
+}
+
+optima_status hessian_jacobi(float* H, int64_t d, float* D, hipStream_t s) {
+  hipLaunchKernelGGL(k_jacobi_d, dim3(unsigned(ceil_div(d, kThreads))), dim3(kThreads), 0, s, H, d,
+                     D);
+  OPTIMA_LAUNCH_CHECK();
+  const int64_t blocks = std::min<int64_t>(8192, ceil_div(d * d, kThreads));
+  hipLaunchKernelGGL(k_jacobi_scale, dim3(unsigned(blocks)), dim3(kThreads), 0, s, H, d, D);
   OPTIMA_LAUNCH_CHECK();
   return OPTIMA_OK;
 }

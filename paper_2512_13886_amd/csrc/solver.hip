@@ -269,9 +269,12 @@ __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows
 }
 
 // Copies W0 into padded rows and forms the start point x = x_ag = sel(m, w0, 0).
+// Padded copy of the anchors (divided by the column scaling D when given),
+// the start point sel(mask, w0, +0), its average and split planes.
 __global__ void __launch_bounds__(kThreads) k_prep(const float* W0, const uint8_t* mask, int n_cols,
                                                    int d, int dp, float* W0P, float* X, float* XA,
-                                                   uint16_t* XP, uint16_t* WP, int* flags) {
+                                                   uint16_t* XP, uint16_t* WP,
+                                                   const float* scale, int* flags) {
   const int j = blockIdx.x;
   const size_t base = size_t(j) * dp;
   bool bad = false;
@@ -282,6 +285,11 @@ __global__ void __launch_bounds__(kThreads) k_prep(const float* W0, const uint8_
       w = W0[size_t(j) * d + n];
       keep = mask[size_t(j) * d + n] != 0;
       bad |= !isfinite(w);
+      if (scale) {
+        const float sc = scale[n];
+        bad |= !(sc > 0.f) || !isfinite(sc);
+        w = w / sc;
+      }
     }
     W0P[base + n] = w;
     const float x = keep ? w : 0.f;
@@ -352,6 +360,7 @@ struct CheckArgs {
   const float* HW0;
   const float* W0;     // [n_cols][d]
   const uint8_t* mask;
+  const float* scale;  // column scaling D of a preconditioned H, or NULL
   ColState st;
   int n_block;         // iterations run since the last check
   int64_t t;           // total iterations run
@@ -372,25 +381,29 @@ __global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
   const int j = a.rows ? a.rows[r] : r;
   const size_t base = size_t(j) * a.dp;
 
+  // With a column scaling D the iterates live in y = D^-1 w; r_d and ||2 H w0||
+  // are taken with the gradient in the original coordinates (divided by D),
+  // gap, f and z^T H z are the same in both.
   double rdx = 0, gpx = 0, fx = 0, qx = 0, rda = 0, gpa = 0, fa = 0, qa = 0, cn = 0, wq = 0;
   for (int n = threadIdx.x; n < a.d; n += kThreads) {
     const size_t o = base + n;
     const double hw = a.HW0[o];
-    const double w0 = a.W0[size_t(j) * a.d + n];
+    const double inv = a.scale ? 1.0 / double(a.scale[n]) : 1.0;
+    const double w0 = double(a.W0[size_t(j) * a.d + n]) * inv;
     const bool keep = a.mask[size_t(j) * a.d + n] != 0;
     const double x = a.X[o], hx = a.HX[o];
     const double gx = 2.0 * (hx - hw);
-    rdx += keep ? gx * gx : 0.0;
+    rdx += keep ? (gx * inv) * (gx * inv) : 0.0;
     gpx += x * gx;
     fx += (x - w0) * (hx - hw);
     qx += x * hx;
     if (a.initial) {
-      cn += 4.0 * hw * hw;
+      cn += 4.0 * (hw * inv) * (hw * inv);
       wq += w0 * hw;
     } else {
       const double xa = a.XA[o], ha = a.HA[o];
       const double ga = 2.0 * (ha - hw);
-      rda += keep ? ga * ga : 0.0;
+      rda += keep ? (ga * inv) * (ga * inv) : 0.0;
       gpa += xa * ga;
       fa += (xa - w0) * (ha - hw);
       qa += xa * ha;
@@ -485,7 +498,8 @@ __global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
   const int dec = decision;
   if (dec & 1) {
     const float* src = (dec & 4) ? a.X : a.XA;
-    for (int n = threadIdx.x; n < a.d; n += kThreads) a.W_out[size_t(j) * a.d + n] = src[base + n];
+    for (int n = threadIdx.x; n < a.d; n += kThreads)
+      a.W_out[size_t(j) * a.d + n] = a.scale ? src[base + n] * a.scale[n] : src[base + n];
   } else if (dec & 2) {
     float* xd = (dec & 4) ? a.XA : a.X;
     float* hd = (dec & 4) ? a.HA : a.HX;
@@ -589,6 +603,7 @@ struct CgCheckArgs {
   const float* R;
   const float* HW0;
   const uint8_t* mask;
+  const float* scale;
   ColState st;
   int64_t t;
   int final_check;
@@ -609,7 +624,8 @@ __global__ void __launch_bounds__(kThreads) k_cg_check(CgCheckArgs a) {
   for (int n = threadIdx.x; n < a.d; n += kThreads) {
     if (!m[n]) continue;
     const double x = a.X[base + n], rv = a.R[base + n];
-    rr += rv * rv;
+    const double ro = a.scale ? rv / double(a.scale[n]) : rv;  // original coordinates
+    rr += ro * ro;
     xr += x * rv;
     xh += x * double(a.HW0[base + n]);
   }
@@ -636,7 +652,8 @@ __global__ void __launch_bounds__(kThreads) k_cg_check(CgCheckArgs a) {
   }
   __syncthreads();
   if (stop)
-    for (int n = threadIdx.x; n < a.d; n += kThreads) a.W_out[size_t(j) * a.d + n] = a.X[base + n];
+    for (int n = threadIdx.x; n < a.d; n += kThreads)
+      a.W_out[size_t(j) * a.d + n] = a.scale ? a.X[base + n] * a.scale[n] : a.X[base + n];
 }
 
 // Stable compaction of the active list: keeps the columns not yet done.
@@ -811,6 +828,7 @@ optima_status cg_loop(const Layout& l, ProductArgs p, int dp, int di, const uint
   ck.R = l.XA;
   ck.HW0 = l.HW0;
   ck.mask = mask;
+  ck.scale = o.col_scale;
   ck.st = l.st;
   ck.o = o;
   ck.W_out = W_out;
@@ -901,7 +919,8 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   const bool split = o.precision == kPrecBf16x3;
   // Split planes: x0 into XP0, W0 into XP1 (free until the first update).
   hipLaunchKernelGGL(k_prep, vec_grid, dim3(kThreads), 0, s, W0, mask, nc, di, dp, l.HX, l.X0,
-                     l.XA, split ? l.XP0 : nullptr, split ? l.XP1 : nullptr, l.flags);
+                     l.XA, split ? l.XP0 : nullptr, split ? l.XP1 : nullptr, o.col_scale,
+                     l.flags);
   OPTIMA_LAUNCH_CHECK();
   if (split) {
     hipLaunchKernelGGL(k_split_h, dim3(unsigned(dp), unsigned(ceil_div(dp, 4 * kThreads))),
@@ -947,6 +966,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   ca.HW0 = l.HW0;
   ca.W0 = W0;
   ca.mask = mask;
+  ca.scale = o.col_scale;
   ca.st = l.st;
   ca.o = o;
   ca.W_out = W_out;

@@ -293,6 +293,16 @@ __global__ void __launch_bounds__(kSubThreads) k_subspace_pass(const float* H, i
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, y.w, acc, 0, 0, 0);
   };
   int64_t c = ks;
+  for (; c + 28 < nch; c += 32) {  // eight 16-byte loads per operand in flight
+    float4 a[8], y[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      a[u] = load_a(c + 4 * u);
+      y[u] = *reinterpret_cast<const float4*>(yrow + (c + 4 * u) * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) mfma4(a[u], y[u]);
+  }
   for (; c + 12 < nch; c += 16) {
     const float4 a0 = load_a(c), a1 = load_a(c + 4), a2 = load_a(c + 8), a3 = load_a(c + 12);
     const float4 y0 = *reinterpret_cast<const float4*>(yrow + c * 16);
@@ -374,10 +384,34 @@ __global__ void __launch_bounds__(kSubThreads) k_subspace_init(const float* V0, 
   }
 }
 
+// Sums the per-workgroup partials of G, T and S (kPart entries each row of
+// `part`, nblk rows) into tot[kPart]: workgroup b takes 32 entries, its 8
+// thread groups sum 8 contiguous ranges of rows, then the 8 range sums are
+// added in order (a fixed order: deterministic).
+constexpr int kRedEntries = 32, kRedSegs = 8;
+__global__ void __launch_bounds__(256) k_subspace_reduce(const double* part, int nblk,
+                                                         double* tot, const SubState* st) {
+  if (st->conv) return;
+  __shared__ double seg[kRedSegs][kRedEntries];
+  const int el = threadIdx.x % kRedEntries, sg = threadIdx.x / kRedEntries;
+  const int e = blockIdx.x * kRedEntries + el;
+  const int per = (nblk + kRedSegs - 1) / kRedSegs;
+  const int k0 = sg * per, k1 = min(nblk, k0 + per);
+  double a = 0.0;
+  for (int k = k0; k < k1; ++k) a += part[size_t(k) * kPart + e];
+  seg[sg][el] = a;
+  __syncthreads();
+  if (sg == 0) {
+    double t = 0.0;
+    for (int q = 0; q < kRedSegs; ++q) t += seg[q][el];
+    tot[e] = t;
+  }
+}
+
 // Finish of pass `it` (0: the start block only). One workgroup of 256.
-__global__ void __launch_bounds__(256) k_subspace_finish(const double* part, int nblk, int b,
-                                                         int it, float tol, double* Rinv,
-                                                         SubState* st, float* lambda_out) {
+__global__ void __launch_bounds__(256) k_subspace_finish(const double* tot, int b, int it,
+                                                         float tol, double* Rinv, SubState* st,
+                                                         float* lambda_out) {
   if (st->conv) return;
   __shared__ double G[kMaxBlock][kPitch], T[kMaxBlock][kPitch], S[kMaxBlock][kPitch];
   __shared__ double L[kMaxBlock][kPitch], X[kMaxBlock][kPitch], W[kMaxBlock][kPitch];
@@ -388,13 +422,7 @@ __global__ void __launch_bounds__(256) k_subspace_finish(const double* part, int
   if (t == 0) bad = 0;
   __syncthreads();
   {
-    double g = 0.0, tt = 0.0, ss = 0.0;
-    for (int k = 0; k < nblk; ++k) {
-      const double* P = part + size_t(k) * kPart;
-      g += P[t];
-      tt += P[kGram + t];
-      ss += P[2 * kGram + t];
-    }
+    const double g = tot[t], tt = tot[kGram + t], ss = tot[2 * kGram + t];
     G[i][j] = g;
     T[i][j] = tt;
     S[i][j] = ss;
@@ -488,6 +516,7 @@ size_t spectral_norm_workspace_bytes(int64_t d, int block) {
     c.take<float>(size_t(kMaxBlock) * size_t(dpp));
     c.take<float>(size_t(kMaxBlock) * size_t(dpp));
     c.take<double>(size_t(dpp / kSubRows) * kPart);
+    c.take<double>(kPart);
     c.take<double>(kGram);
     c.take<SubState>(1);
   }
@@ -546,13 +575,17 @@ optima_status subspace_iteration(const float* H, int64_t d, const float* V0, int
   float* Y[2] = {c.take<float>(size_t(kMaxBlock) * size_t(dpp)),
                  c.take<float>(size_t(kMaxBlock) * size_t(dpp))};
   double* part = c.take<double>(size_t(nblk) * kPart);
+  double* tot = c.take<double>(kPart);
   double* Rinv = c.take<double>(kGram);
   SubState* st = c.take<SubState>(1);
+  const dim3 rg(unsigned(kPart / kRedEntries));
   hipLaunchKernelGGL(k_subspace_init, dim3(unsigned(nblk)), dim3(kSubThreads), 0, s, V0, b, d,
                      dpp, Y[0], part, st);
   OPTIMA_LAUNCH_CHECK();
-  hipLaunchKernelGGL(k_subspace_finish, dim3(1), dim3(256), 0, s, part, nblk, b, 0, tol, Rinv,
-                     st, lambda_max);
+  hipLaunchKernelGGL(k_subspace_reduce, rg, dim3(256), 0, s, part, nblk, tot, st);
+  OPTIMA_LAUNCH_CHECK();
+  hipLaunchKernelGGL(k_subspace_finish, dim3(1), dim3(256), 0, s, tot, b, 0, tol, Rinv, st,
+                     lambda_max);
   OPTIMA_LAUNCH_CHECK();
   const bool vec4 = (d % 4) == 0 && aligned16(H);
   constexpr int kPoll = 4;
@@ -564,8 +597,10 @@ optima_status subspace_iteration(const float* H, int64_t d, const float* V0, int
       hipLaunchKernelGGL(k_subspace_pass<false>, dim3(unsigned(nblk)), dim3(kSubThreads), 0, s, H,
                          d, dpp, Y[(it - 1) & 1], Y[it & 1], Rinv, part, st);
     OPTIMA_LAUNCH_CHECK();
-    hipLaunchKernelGGL(k_subspace_finish, dim3(1), dim3(256), 0, s, part, nblk, b, it, tol, Rinv,
-                       st, lambda_max);
+    hipLaunchKernelGGL(k_subspace_reduce, rg, dim3(256), 0, s, part, nblk, tot, st);
+    OPTIMA_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_subspace_finish, dim3(1), dim3(256), 0, s, tot, b, it, tol, Rinv, st,
+                       lambda_max);
     OPTIMA_LAUNCH_CHECK();
     if (it % kPoll == 0 && it < max_iters) {
       int conv = 0;
