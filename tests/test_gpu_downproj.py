@@ -1,0 +1,94 @@
+"""Parity at the down_proj shape (d_in = 14336, 4096 columns, SiLU-gated
+bf16 tokens, 60 % unstructured mask).
+
+The Hessian runs on all 262144 tokens (the direct path over 56 x 56 blocks of
+256, split along the tokens) and is checked on sampled features; the block
+spectral norm runs on that device matrix; both solvers run at the full width
+on a Hessian from 8192 tokens and are checked against the closed form on
+sampled columns.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from gpu_util import dev, to_dev, to_dev_x, gpu_spectral, gpu_solve, rel_fro, f32_exact, log
+from test_gpu_solver import _assert_w_and_f, _assert_zero_pattern
+
+pytestmark = pytest.mark.gpu
+
+CFG = workloads.DOWN_PROJ
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2512_13886_amd as lib_mod  # fails loudly when the library is missing
+    return lib_mod
+
+
+def test_downproj_hessian_and_spectral_full_size(L):
+    log("down_proj: generating 262144 x 14336 bf16 tokens")
+    X = workloads.x_all(CFG)
+    Xd = to_dev_x(X)
+    H = torch.empty((CFG.d, CFG.d), dtype=torch.float32, device=dev())
+    L.optima_hessian_accumulate(Xd, H)
+    torch.cuda.synchronize()
+    del Xd
+    rng = np.random.default_rng(1)
+    cols = np.sort(np.unique(np.concatenate([rng.choice(CFG.d, 254, replace=False),
+                                             [0, CFG.d - 1]])))
+    log(f"  oracle on {cols.size} features")
+    Ho = oracle.hessian(workloads.x_to_f64(X[c * CFG.chunk:(c + 1) * CFG.chunk][:, cols])
+                        for c in range(CFG.n_chunks))
+    del X
+    Hg = H.cpu().numpy().astype(np.float64)
+    assert np.array_equal(Hg, Hg.T), "H must be exactly symmetric"
+    sub = Hg[np.ix_(cols, cols)]
+    r = rel_fro(sub, Ho)
+    dg = np.sqrt(np.outer(np.diag(Ho), np.diag(Ho)))
+    worst = float(np.max(np.abs(sub - Ho) / dg))
+    log(f"  H rel_fro={r:.3e} worst_entry={worst:.3e}")
+    assert r <= 1e-5 and worst <= 2e-5
+    # Damping and the block-16 spectral norm of the device matrix.
+    lam = torch.empty(1, dtype=torch.float32, device=dev())
+    L.optima_hessian_damp(H, CFG.rel_damp, lam)
+    Hd = H.cpu().numpy().astype(np.float64)
+    V0 = workloads.power_start_block(CFG.d, 16)
+    lm, it = gpu_spectral(L, H, V0, max_iters=1000, tol=1e-6)
+    th, it_o = oracle.subspace_iteration(Hd, V0, 1000, 1e-6)
+    log(f"  lambda_max gpu {float(lm.item()):.8e} ({it} it) oracle {th:.8e} ({it_o} it)")
+    assert float(lm.item()) == pytest.approx(th, rel=2e-5)
+
+
+@pytest.fixture(scope="module")
+def small_layer():
+    # Full width, 8192 tokens for the oracle's Hessian, 384 columns.
+    cfg = CFG.with_tokens(4 * 2048).with_cols(384)
+    log("down_proj: oracle Hessian over 8192 tokens")
+    X = workloads.x_all(cfg)
+    H, _ = oracle.damp(oracle.hessian([workloads.x_to_f64(X)]), cfg.rel_damp)
+    H = f32_exact(H)
+    W0 = workloads.w0(cfg)
+    M = workloads.layer_mask(cfg, W0, workloads.col_sq_norms(cfg, X))
+    return cfg, H, W0, M
+
+
+@pytest.mark.parametrize("method", ["rapdhg", "cg"])
+def test_downproj_solve_full_width(L, small_layer, method):
+    cfg, H, W0, M = small_layer
+    assert np.all(M.sum(axis=1) == cfg.d - int(np.floor(cfg.sparsity * cfg.d)))
+    Hd = to_dev(H)
+    if method == "rapdhg":
+        lm, _ = gpu_spectral(L, Hd, workloads.power_start_block(cfg.d, 16))
+        opts = L.SolverOpts.default(max_iters=800, fixed_iters=1)
+    else:
+        lm = None
+        opts = L.SolverOpts.default(method=L.METHOD_CG, max_iters=150, fixed_iters=1)
+    Wg, st, info = gpu_solve(L, Hd, lm, W0, M, opts)
+    Wg = Wg.cpu().numpy()
+    _assert_zero_pattern(Wg, M)
+    cols = np.arange(0, cfg.n_cols, cfg.n_cols // 12)
+    log(f"  closed form on {cols.size} columns")
+    ref = oracle.closed_form(H, W0[cols], M[cols])
+    _assert_w_and_f(H, W0[cols], M[cols], Wg[cols], ref, label=f"down_proj {method}")
