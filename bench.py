@@ -98,6 +98,77 @@ def cpu_baseline(cfg, X, W0, mask, sample_cols: int, sample_chunks: int) -> dict
     }
 
 
+def block_leg(L, torch, dev, precision) -> dict:
+    """The streamed decoder block (Llama-3-8B shapes): for each calibration
+    stream the Hessian, the Wanda masks of its matrices (from the undamped
+    Hessian's diagonal, on the device), damping, the step size and the paper-
+    mode solves. Tokens and weights are moved to the device before timing;
+    the reported time is the device time of all of that work."""
+    import workloads
+    total_ms = 0.0
+    layers = {}
+    streams = {}
+    for sname, scfg in workloads.BLOCK_STREAMS.items():
+        mats = [lc for lc, st in workloads.BLOCK_LAYERS if st == sname]
+        X = workloads.x_all(scfg)
+        Xd = torch.from_numpy(X.view(np.int16)).view(torch.bfloat16).to(dev)
+        del X
+        d = scfg.d
+        W0s = [torch.from_numpy(workloads.w0(lc)).to(dev) for lc in mats]
+        H = torch.empty((d, d), dtype=torch.float32, device=dev)
+        lam = torch.empty(1, dtype=torch.float32, device=dev)
+        lmax = torch.empty(1, dtype=torch.float32, device=dev)
+        sp_it = torch.zeros(1, dtype=torch.int32, device=dev)
+        V0 = torch.from_numpy(workloads.power_start_block(d, SPECTRAL_BLOCK)).to(dev)
+        masks = [torch.empty((lc.n_cols, d), dtype=torch.uint8, device=dev) for lc in mats]
+        outs = [torch.empty_like(w) for w in W0s]
+        stats = [{"iters": torch.zeros(lc.n_cols, dtype=torch.int32, device=dev),
+                  "converged": torch.zeros(lc.n_cols, dtype=torch.uint8, device=dev),
+                  "f_initial": torch.zeros(lc.n_cols, dtype=torch.float32, device=dev),
+                  "f_final": torch.zeros(lc.n_cols, dtype=torch.float32, device=dev)}
+                 for lc in mats]
+        hws = torch.empty(L.optima_hessian_workspace_bytes(scfg.n_tok, d, L.DTYPE_BF16),
+                          dtype=torch.uint8, device=dev)
+        opts = L.SolverOpts.default()
+        if precision is not None:
+            opts.precision = precision
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 + len(mats))]
+        ev[0].record()
+        L.optima_hessian_accumulate(Xd, H, ws=hws)
+        for lc, W0d, M in zip(mats, W0s, masks):
+            L.optima_wanda_mask(W0d, H, M, L.MASK_UNSTRUCTURED, lc.sparsity, col_sq_stride=d + 1)
+        ev[1].record()
+        L.optima_hessian_damp(H, scfg.rel_damp, lam)
+        L.optima_spectral_norm(H, V0, lmax, max_iters=1000, tol=1e-6, iters=sp_it)
+        ev[2].record()
+        infos = []
+        for i, (lc, W0d, M, out, st) in enumerate(zip(mats, W0s, masks, outs, stats)):
+            infos.append(L.optima_qp_solve_batched(H, lmax, W0d, M, out, opts=opts, stats=st))
+            ev[3 + i].record()
+        torch.cuda.synchronize()
+        s_ms = ev[0].elapsed_time(ev[-1])
+        total_ms += s_ms
+        streams[sname] = {"d": d, "hessian_and_masks_ms": ev[0].elapsed_time(ev[1]),
+                          "damp_spectral_ms": ev[1].elapsed_time(ev[2]),
+                          "spectral_passes": int(sp_it.item()), "ms": s_ms}
+        prev = ev[2]
+        for i, (lc, st, inf) in enumerate(zip(mats, stats, infos)):
+            layers[lc.name[len("block_"):]] = {
+                "d": d, "columns": lc.n_cols, "solve_ms": prev.elapsed_time(ev[3 + i]),
+                "iterations": inf["iterations"], "converged": int(st["converged"].sum().item()),
+                "f_final_over_f_initial":
+                    (st["f_final"].double().sum() / st["f_initial"].double().sum()).item()}
+            prev = ev[3 + i]
+        log(f"block stream {sname}: {s_ms:.1f} ms ({streams[sname]['spectral_passes']} "
+            f"spectral passes)")
+        del Xd, H, hws, W0s, outs, masks, stats
+        torch.cuda.empty_cache()
+    cols = sum(v["columns"] for v in layers.values())
+    return {"block_prune_ms": total_ms, "columns": cols,
+            "columns_per_s": cols / (total_ms * 1e-3), "streams": streams, "layers": layers}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -111,6 +182,9 @@ def main() -> int:
     ap.add_argument("--precision", choices=["fp32", "bf16x3"], default=None,
                     help="arithmetic of the per-iteration H-products (default: the "
                          "library's, bf16x3)")
+    ap.add_argument("--block-config", action="store_true",
+                    help="also prune the streamed Llama-3-8B-shaped decoder block (7 matrices, "
+                         "4 calibration streams) and report its end-to-end device time")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="first run one 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -346,6 +420,11 @@ def main() -> int:
     log(f"mask selection: 2:4 {m24_ms * 1e3:.1f} us, unstructured {mun_ms * 1e3:.1f} us, "
         f"2:4 equals the host mask: {m24_same}")
 
+    block = None
+    if args.block_config:
+        block = block_leg(L, torch, dev, None if args.precision is None else prec)
+        log(f"block prune: {block['block_prune_ms']:.1f} ms for {block['columns']} columns")
+
     traffic = None  # the counter passes were taken on the bf16x3 kernels
     if (TRAFFIC and prec == L.PREC_BF16X3
             and TRAFFIC.get("sources_sha1") == kernel_sources_sha1()):
@@ -407,6 +486,7 @@ def main() -> int:
         "mask_select": mask_select,
         "cg_unconstrained": cg_leg,
         "jacobi_preconditioned": pre,
+        "decoder_block": block,
         "peak_device_memory_gib": torch.cuda.max_memory_allocated(dev) / 2**30,
         "roofline": roofline,
     }

@@ -74,6 +74,35 @@ DOWN_PROJ = LayerConfig(
 
 CONFIGS = {c.name: c for c in (TINY, GPT2_FC, Q_PROJ, DOWN_PROJ)}
 
+# The Llama-3-8B-shaped decoder block, streamed layer by layer: four
+# calibration streams (the inputs of q/k/v, of o, of gate/up and of down; the
+# first three follow the q_proj recipe, the last the down_proj recipe), 128 x
+# 2048 tokens each, and seven weight matrices with 50 % unstructured masks.
+# Streams draw their tokens under cfg_id 4 with tensor ids offset by 10 k;
+# each matrix draws its W0 with an offset of its own (40, 50, ...).
+_BLOCK_STREAM_RECIPES = (
+    ("qkv_in", 4096, "student_t_outliers"),
+    ("o_in", 4096, "student_t_outliers"),
+    ("gate_up_in", 4096, "student_t_outliers"),
+    ("down_in", 14336, "silu_gated"),
+)
+BLOCK_STREAMS = {
+    name: LayerConfig(
+        name=f"block_{name}", cfg_id=4, d=d, n_cols=0, n_tok=128 * 2048, chunk=2048,
+        x_dtype="bf16", w_dtype="bf16", w_std=0.015, x_recipe=recipe,
+        mask_kind="unstructured", sparsity=0.5, tensor_offset=10 * k)
+    for k, (name, d, recipe) in enumerate(_BLOCK_STREAM_RECIPES)
+}
+# (matrix, stream, output columns)
+_BLOCK_MATRICES = (("q_proj", "qkv_in", 4096), ("k_proj", "qkv_in", 1024),
+                   ("v_proj", "qkv_in", 1024), ("o_proj", "o_in", 4096),
+                   ("gate_proj", "gate_up_in", 14336), ("up_proj", "gate_up_in", 14336),
+                   ("down_proj", "down_in", 4096))
+BLOCK_LAYERS = tuple(
+    (replace(BLOCK_STREAMS[stream], name=f"block_{name}", n_cols=cols,
+             tensor_offset=40 + 10 * i), stream)
+    for i, (name, stream, cols) in enumerate(_BLOCK_MATRICES))
+
 
 @dataclass(frozen=True)
 class SolverSettings:
