@@ -40,6 +40,9 @@ METRIC = "QP columns solved/sec + rAPDHG iters/sec on 4096×4096 layer; MFMA % o
 # Published dense MFMA peaks of MI355X.
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0
+# Rate of the 2:4-sparse bf16 instruction counted in the flops of the dense
+# product it stands for (twice the dense instruction's).
+BF16_SPARSE_MFMA_PEAK_TFLOPS = 5000.0
 HBM_PEAK_GBS = 8000.0
 # Start vectors of the subspace iteration that sets the step size.
 SPECTRAL_BLOCK = 16
@@ -276,6 +279,7 @@ def main() -> int:
     launches = sum(i["timed_launches"] for _, i in recs)
     rows = sum(i["timed_row_products"] for _, i in recs)
     prod_ms = sum(i["timed_product_ms"] for _, i in recs)
+    sparse_products = all(i["sparse_products"] == 1 for _, i in recs)
     flops = 2.0 * d * d * rows
     achieved = flops / (prod_ms * 1e-3) / 1e12
     avg_launch_us = prod_ms * 1e3 / launches
@@ -432,7 +436,28 @@ def main() -> int:
 
     # Roofline of the dominant kernel over the timed steps: algorithmic flops
     # (2 d^2 per column per iteration) over the device time of its launches.
-    if prec == L.PREC_BF16X3:
+    if prec == L.PREC_BF16X3 and sparse_products:
+        # The 2:4 mask lets x travel compressed: each of the three bf16
+        # products runs on v_smfmac_f32_16x16x64_bf16 and skips the pruned
+        # half of K. achieved keeps the algorithmic count of the dense
+        # product (2 d^2 per column and iteration) and frac compares it with
+        # the dense bf16 peak; mfma_issued_frac compares the issued products
+        # (3 x achieved) with the sparse instruction's own peak.
+        roofline = {
+            "kernel": "k_product_sparse<fused>: H-product x H over the active columns "
+                      "(M = active columns, N = K = 4096), x 2:4-compressed, three bf16 "
+                      "products per fp32 product on v_smfmac_f32_16x16x64_bf16 (256 x 128 "
+                      "tiles), fused rAPDHG update in the epilogue",
+            "bound": "mfma", "achieved": achieved, "peak": BF16_MFMA_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": achieved / BF16_MFMA_PEAK_TFLOPS,
+            "traffic": traffic,
+            "sparse_products": True,
+            "mfma_issued_tflops": 3.0 * achieved,
+            "mfma_issued_peak": BF16_SPARSE_MFMA_PEAK_TFLOPS,
+            "mfma_issued_frac": 3.0 * achieved / BF16_SPARSE_MFMA_PEAK_TFLOPS,
+            "fp32_equivalent_frac": achieved / FP32_MFMA_PEAK_TFLOPS,
+        }
+    elif prec == L.PREC_BF16X3:
         roofline = {
             "kernel": "k_product<fused, bf16x3>: H-product x H over the active columns "
                       "(M = active columns, N = K = 4096) on v_mfma_f32_16x16x32_bf16, three "

@@ -254,6 +254,14 @@ typedef struct {
   const float* col_scale; /* NULL (default), or the [d] device diagonal D of a
                              preconditioned H = D H0 D (optima_hessian_jacobi);
                              see "Shared diagonal preconditioning" */
+  int32_t sparse;         /* 1 (default): when precision is BF16X3, method is
+                             RAPDHG and no mask row keeps more than 2 entries
+                             of any group of 4 consecutive columns (a 2:4 mask,
+                             Section 4), the iteration products take x
+                             2:4-compressed and multiply on the sparse MFMA
+                             (v_smfmac_f32_16x16x64_bf16), skipping the pruned
+                             entries; the same products are formed, summed in
+                             another order. 0: dense products always. */
 } optima_solver_opts;
 
 typedef struct {
@@ -274,6 +282,7 @@ typedef struct {
   int64_t timed_row_products; /* columns multiplied by those launches */
   double timed_product_ms;    /* their device time, from HIP events recorded on `stream`
                                  around each run of back-to-back product launches */
+  int64_t sparse_products;    /* 1 if the iteration products ran 2:4-sparse (opts.sparse) */
 } optima_solve_info;
 
 void optima_solver_opts_default(optima_solver_opts* opts);

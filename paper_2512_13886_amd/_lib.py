@@ -51,7 +51,7 @@ class _Opts(ctypes.Structure):
                 ("beta_necessary", ctypes.c_float), ("beta_artificial", ctypes.c_float),
                 ("step_safety", ctypes.c_float), ("restarts", ctypes.c_int32),
                 ("precision", ctypes.c_int32), ("method", ctypes.c_int32),
-                ("col_scale", ctypes.c_void_p)]
+                ("col_scale", ctypes.c_void_p), ("sparse", ctypes.c_int32)]
 
 
 class _Stats(ctypes.Structure):
@@ -63,7 +63,7 @@ class _Info(ctypes.Structure):
     _fields_ = [("iterations", ctypes.c_int64), ("gemm_calls", ctypes.c_int64),
                 ("row_products", ctypes.c_int64), ("checks", ctypes.c_int64),
                 ("timed_launches", ctypes.c_int64), ("timed_row_products", ctypes.c_int64),
-                ("timed_product_ms", ctypes.c_double)]
+                ("timed_product_ms", ctypes.c_double), ("sparse_products", ctypes.c_int64)]
 
 
 def _sig(name, res, args):
@@ -152,6 +152,7 @@ class SolverOpts:
     precision: int = 0
     method: int = 0
     col_scale: "torch.Tensor | None" = None  # [d] float32 device scaling D, or None
+    sparse: int = 0
 
     @classmethod
     def default(cls, **overrides) -> "SolverOpts":

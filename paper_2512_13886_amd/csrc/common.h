@@ -15,6 +15,7 @@ namespace optima {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x16 __attribute__((ext_vector_type(16)));
 
 // Output tile of the MFMA GEMM core and the padding unit of every matrix the
 // core reads (rows and the contraction dimension are padded to it).

@@ -311,6 +311,263 @@ __device__ inline void gemm_tile_mainloop(f4 (&acc)[Cfg::MB][Cfg::NB], const Ope
   __syncthreads();
 }
 
+// ---------------------------------------------------------------------------
+// 2:4-sparse A operand on v_smfmac_f32_16x16x64_bf16
+// ---------------------------------------------------------------------------
+// When every group of 4 consecutive K values of every A row has at most 2
+// nonzeros (a 2:4 pruning mask applied to the multiplied vectors), A is kept
+// compressed: per group 2 stored values, the entries at 2 positions p0 < p1
+// that cover the group's nonzeros (padded with the lowest free positions),
+// and per stored value its 2-bit position. One sparse MFMA multiplies a
+// 16 x 64 block of A (16 x 32 stored values) by a dense 64 x 16 block of B,
+// in the time of a dense 16 x 16 x 32 one, so it skips the products with
+// the zeros.
+//
+// Operand layout of the instruction (checked on gfx950 against a reference
+// product for every lane and value slot): lane l supplies A row l % 16 and
+// the 8 stored values of logical K [16 g, 16 g + 16), g = l / 16, two per
+// group of 4 in group order; bits 2 i..2 i + 1 of its 16-bit index give the
+// position of stored value i within its group. Lane l supplies B column
+// l % 16 at K [8 g, 8 g + 8) (values 0-7) and [32 + 8 g, 32 + 8 g + 8)
+// (values 8-15). The result has the layout of the dense 16 x 16 MFMA.
+//
+// Storage of A: per row and 64-column block of K, 128 bytes: the 32 stored
+// hi values (64 B), then the 32 stored lo values; lane group g's 16 bytes
+// sit at byte 16 g of each plane. Indices: per row and block four 16-bit
+// words (8 bytes), word g for lane group g.
+//
+// Work split: a 256 x 128 output tile per workgroup of 8 waves (4 x 2, each
+// 64 x 64). The operand loads from L2, not the MFMAs, bound these products
+// (about 25 bytes per clock and CU were measured for both the direct loads
+// and plain 16-byte loads), so the tile is the largest whose double-
+// buffered stages fit the LDS: per 64-column stage the stored A rows
+// (256 x 128 B), their index words (256 x 8 B) and the split planes of B
+// (128 x 256 B), 66 KiB, all fetched once per workgroup by direct loads.
+// That is 64 algorithmic flops per loaded byte, twice the dense bf16x3
+// 128 x 128 tile's 32.
+struct SpTile {
+  static constexpr int BM = 256, BN = 128, WGM = 4, WGN = 2, KSPLIT = 1;
+  static constexpr int kTileWaves = 8, kWaves = 8, kThreads = 512;
+  static constexpr int MB = 4, NB = 4;
+  static constexpr int kKPerStage = 64;
+  static constexpr int kARowBytes = 128;  // stored A bytes per row and stage
+  static constexpr int kBRowBytes = 256;  // B bytes per row and stage (both planes)
+  static constexpr int kASegs = kARowBytes / 16, kBSegs = kBRowBytes / 16;
+  static constexpr int kLoadsA = BM * kARowBytes / 1024 / kWaves;  // 1-KiB wave loads
+  static constexpr int kLoadsB = BN * kBRowBytes / 1024 / kWaves;
+  static constexpr int kIdxOff = BM * kARowBytes + BN * kBRowBytes;  // index words
+  static constexpr int kBufBytes = kIdxOff + BM * 8;
+  static_assert(BM * 8 == kWaves * 256, "one 4-byte-per-lane index load per wave");
+};
+
+struct SpOperands {
+  const char* a[SpTile::kLoadsA];  // A segment of this thread's direct loads at stage 0
+  const char* b[SpTile::kLoadsB];  // B segment of this thread's direct loads at stage 0
+  const char* ai;                  // its 4 bytes of index words at stage 0
+  const char* pf;                  // the 128-byte line it touches ahead (see sp_prefetch_line)
+  int pf_stride;                   // that line's advance per stage (128 for A, 256 for B)
+};
+
+// Tile rows fetched by this thread's direct loads and the byte offset of the
+// fetched 16-byte segment in the row's stage. A rows take 128 bytes (8
+// segments, physical segment g ^ (r % 8)), B rows 256 bytes (16 segments,
+// g ^ (r % 16)); index row r takes 8 bytes, 2 lanes per row.
+__device__ inline int sp_a_row(int i) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  return (i * SpTile::kWaves + wave) * (1024 / SpTile::kARowBytes) + lane / SpTile::kASegs;
+}
+__device__ inline int sp_a_seg_bytes(int i) {
+  const int lane = threadIdx.x & 63;
+  return ((lane % SpTile::kASegs) ^ (sp_a_row(i) % SpTile::kASegs)) * 16;
+}
+__device__ inline int sp_b_row(int i) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  return (i * SpTile::kWaves + wave) * (1024 / SpTile::kBRowBytes) + lane / SpTile::kBSegs;
+}
+__device__ inline int sp_b_seg_bytes(int i) {
+  const int lane = threadIdx.x & 63;
+  return ((lane % SpTile::kBSegs) ^ (sp_b_row(i) % SpTile::kBSegs)) * 16;
+}
+__device__ inline int sp_idx_row() { return (threadIdx.x >> 6) * 32 + (threadIdx.x & 63) / 2; }
+__device__ inline int sp_idx_bytes() { return (threadIdx.x & 1) * 4; }
+
+// L2 prefetch one stage further ahead. A stage's operands are 512 lines of
+// 128 bytes (one per A row, two per B row); every lane touches one of them
+// with a 4-byte direct load into a scratch LDS area nobody reads: lanes
+// 0-31 of wave w take A rows 32 w .. 32 w + 31, lanes 32-63 the two lines of
+// B rows 16 w .. 16 w + 15. The stage loop waits on these one stage later
+// than on the real loads, so two stages of operands are in flight with LDS
+// room for only two.
+__device__ inline int sp_pf_a_row() { return (threadIdx.x >> 6) * 32 + (threadIdx.x & 31); }
+__device__ inline int sp_pf_b_row() { return (threadIdx.x >> 6) * 16 + ((threadIdx.x & 31) >> 1); }
+__device__ inline int sp_pf_b_line() { return (threadIdx.x & 1) * 128; }
+__device__ inline bool sp_pf_is_a() { return (threadIdx.x & 63) < 32; }
+
+__device__ inline void sp_prefetch_line(const SpOperands& src, int s, char* scratch) {
+  __builtin_amdgcn_global_load_lds(
+      (const __attribute__((address_space(1))) void*)(src.pf + size_t(s) * src.pf_stride),
+      (__attribute__((address_space(3))) void*)(scratch), 4, 0, 0);
+}
+
+__device__ inline void sp_issue_stage(const SpOperands& src, int s, char* buf) {
+  const int wave = threadIdx.x >> 6;
+  const size_t oa = size_t(s) * SpTile::kARowBytes, ob = size_t(s) * SpTile::kBRowBytes;
+#pragma unroll
+  for (int i = 0; i < SpTile::kLoadsA; ++i)
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(src.a[i] + oa),
+        (__attribute__((address_space(3))) void*)(buf + (i * SpTile::kWaves + wave) * 1024), 16,
+        0, 0);
+#pragma unroll
+  for (int i = 0; i < SpTile::kLoadsB; ++i)
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(src.b[i] + ob),
+        (__attribute__((address_space(3))) void*)(buf + SpTile::BM * SpTile::kARowBytes +
+                                                  (i * SpTile::kWaves + wave) * 1024),
+        16, 0, 0);
+  __builtin_amdgcn_global_load_lds(
+      (const __attribute__((address_space(1))) void*)(src.ai + size_t(s) * 8),
+      (__attribute__((address_space(3))) void*)(buf + SpTile::kIdxOff + wave * 256), 4, 0, 0);
+}
+
+// Fragment reads load ext-vector values straight from the stage buffer: a
+// 16-byte struct load would be split and re-merged by the backend, which
+// drops the LDS alias scope and makes every such read wait for the direct
+// loads in flight.
+__device__ inline bf16x8 sp_a_frag(const char* buf, int r, int seg) {
+  return *reinterpret_cast<const bf16x8*>(buf + r * SpTile::kARowBytes +
+                                          ((seg ^ (r % SpTile::kASegs)) * 16));
+}
+__device__ inline bf16x8 sp_b_frag16(const char* buf, int r, int seg) {
+  return *reinterpret_cast<const bf16x8*>(buf + SpTile::BM * SpTile::kARowBytes +
+                                          r * SpTile::kBRowBytes +
+                                          ((seg ^ (r % SpTile::kBSegs)) * 16));
+}
+__device__ inline bf16x16 sp_b_pair(bf16x8 k0, bf16x8 k1) {
+  return __builtin_shufflevector(k0, k1, 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+}
+
+__device__ inline void sp_compute_stage(f4 (&acc)[SpTile::MB][SpTile::NB], const char* buf) {
+  constexpr int MB = SpTile::MB, NB = SpTile::NB;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ra = (wave / SpTile::WGN) * MB * 16 + (lane & 15);
+  const int rb = (wave % SpTile::WGN) * NB * 16 + (lane & 15);
+  const int g = lane >> 4;
+  bf16x8 ah[MB], al[MB];
+  int ix[MB];
+#pragma unroll
+  for (int mi = 0; mi < MB; ++mi) {
+    ah[mi] = sp_a_frag(buf, ra + mi * 16, g);
+    al[mi] = sp_a_frag(buf, ra + mi * 16, 4 + g);
+    ix[mi] = *reinterpret_cast<const uint16_t*>(buf + SpTile::kIdxOff + (ra + mi * 16) * 8 + 2 * g);
+  }
+  // B row segments: hi planes of K [0, 32) at 0-3 and [32, 64) at 8-11, lo
+  // planes at 4-7 and 12-15. Consecutive MFMAs use different accumulators.
+#pragma unroll
+  for (int ni = 0; ni < NB; ++ni) {
+    const int r = rb + ni * 16;
+    const bf16x16 bh = sp_b_pair(sp_b_frag16(buf, r, g), sp_b_frag16(buf, r, 8 + g));
+    const bf16x16 bl = sp_b_pair(sp_b_frag16(buf, r, 4 + g), sp_b_frag16(buf, r, 12 + g));
+#pragma unroll
+    for (int mi = 0; mi < MB; ++mi)
+      acc[mi][ni] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(ah[mi],
+                                                              bh, acc[mi][ni], ix[mi], 0, 0);
+#pragma unroll
+    for (int mi = 0; mi < MB; ++mi)
+      acc[mi][ni] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(ah[mi],
+                                                              bl, acc[mi][ni], ix[mi], 0, 0);
+#pragma unroll
+    for (int mi = 0; mi < MB; ++mi)
+      acc[mi][ni] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(al[mi],
+                                                              bh, acc[mi][ni], ix[mi], 0, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x020, SpTile::kLoadsA + SpTile::kLoadsB + 2, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, 3 * MB + 8, 0);
+#pragma unroll
+  for (int ni = 0; ni < NB - 2; ++ni) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 3 * MB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 6 * MB, 0);
+}
+
+// n stages (of 64 K values) of the sparse product, starting at the stage the
+// operand addresses point to; lds0 / lds1 are distinct __shared__ arrays of
+// SpTile::kBufBytes.
+// Stage barrier of the sparse loop: this wave's direct loads except the
+// newest one (the prefetch touch) and its LDS reads are complete, then all
+// waves meet. __syncthreads() would also drain the prefetch (its release
+// fence waits for every outstanding load). The empty asm statements keep
+// the compiler from moving memory accesses across the barrier.
+__device__ inline void sp_stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(1 | 0x70);  // vmcnt(1) lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+__device__ inline void gemm_sparse_mainloop(f4 (&acc)[SpTile::MB][SpTile::NB],
+                                            const SpOperands& src, int n, char* lds0,
+                                            char* lds1, char* scratch) {
+#pragma unroll
+  for (int mi = 0; mi < SpTile::MB; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < SpTile::NB; ++ni) acc[mi][ni] = f4{0.f, 0.f, 0.f, 0.f};
+  if (n <= 0) return;
+  auto cl = [n](int s) { return s < n ? s : n - 1; };
+  sp_issue_stage(src, 0, lds0);
+  sp_prefetch_line(src, cl(1), scratch);
+  int s = 0;
+  for (; s + 1 < n; s += 2) {
+    sp_stage_barrier();
+    sp_issue_stage(src, s + 1, lds1);
+    sp_prefetch_line(src, cl(s + 2), scratch);
+    sp_compute_stage(acc, lds0);
+    sp_stage_barrier();
+    sp_issue_stage(src, cl(s + 2), lds0);
+    sp_prefetch_line(src, cl(s + 3), scratch);
+    sp_compute_stage(acc, lds1);
+  }
+  if (s < n) {  // odd count: the last stage is in lds0
+    sp_stage_barrier();
+    sp_compute_stage(acc, lds0);
+  }
+  // No direct load may still be writing LDS when the workgroup moves on.
+  wait_vmcnt<0>();
+  __syncthreads();
+}
+
+// Epilogue staging of the 256 x 128 accumulator tile through the stage
+// buffers: tile rows 64 q .. 64 q + 63 go to region q (lds0, lds0 + 32 KiB,
+// lds1, lds1 + 32 KiB), 512 bytes per row, 16-byte column chunk c of row r at
+// physical chunk c ^ (r & 31) (conflict-free as in stage_tile).
+__device__ inline char* sp_stage_region(char* lds0, char* lds1, int r) {
+  const int q = r >> 6;
+  return (q < 2 ? lds0 : lds1) + (q & 1) * 32768 + (r & 63) * 512;
+}
+__device__ inline void sp_stage_tile(const f4 (&acc)[SpTile::MB][SpTile::NB], char* lds0,
+                                     char* lds1) {
+  static_assert(SpTile::kBufBytes >= 2 * 64 * 512, "stage buffers too small for the tile");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / SpTile::WGN, wn = wave % SpTile::WGN;
+#pragma unroll
+  for (int mi = 0; mi < SpTile::MB; ++mi)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = wm * SpTile::MB * 16 + mi * 16 + 4 * (lane >> 4) + e;
+      char* row = sp_stage_region(lds0, lds1, r);
+#pragma unroll
+      for (int ni = 0; ni < SpTile::NB; ++ni) {
+        const int col = wn * SpTile::NB * 16 + ni * 16 + (lane & 15);
+        *reinterpret_cast<float*>(row + ((col >> 2) ^ (r & 31)) * 16 + (col & 3) * 4) =
+            acc[mi][ni][e];
+      }
+    }
+}
+__device__ inline float4 sp_staged_chunk(char* lds0, char* lds1, int r, int c) {
+  return *reinterpret_cast<const float4*>(sp_stage_region(lds0, lds1, r) + ((c ^ (r & 31)) * 16));
+}
+
 // Epilogue staging of a 128 x 128 fp32 accumulator tile through the (then
 // idle) stage buffers: tile rows 0-63 go to buf0 and 64-127 to buf1, 512
 // bytes per row, 16-byte column chunk c of row r at physical chunk

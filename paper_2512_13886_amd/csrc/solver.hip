@@ -21,7 +21,9 @@ namespace optima {
 namespace {
 
 enum GemmMode { kPlain = 0, kPlain2 = 1, kStore = 2, kFused = 3 };
-enum Prec { kPrecF32 = OPTIMA_PREC_FP32, kPrecBf16x3 = OPTIMA_PREC_BF16X3 };
+// kPrecSparse: bf16x3 with the multiplied vectors stored 2:4-compressed (the
+// iteration products of a solve whose mask keeps at most 2 of every 4).
+enum Prec { kPrecF32 = OPTIMA_PREC_FP32, kPrecBf16x3 = OPTIMA_PREC_BF16X3, kPrecSparse = 2 };
 
 struct ProductArgs {
   const float* A;      // rows of the multiplied vectors, pitch dp
@@ -41,9 +43,11 @@ struct ProductArgs {
   const int* kbase;    // iterations since restart, per column, at the last check
   int s;               // iterations since the last check before this product
   const float* Lp;     // step constant L
-  const uint16_t* Ap;  // kPrecBf16x3: split planes of A (same rows as A)
-  const uint16_t* Bp;  // kPrecBf16x3: split planes of H
-  uint16_t* XoutP;     // kPrecBf16x3, kFused: split planes of the next x
+  const uint16_t* Ap;  // kPrecBf16x3: split planes of A (same rows as A);
+                       // kPrecSparse: their 2:4-compressed form
+  const uint16_t* Aidx;  // kPrecSparse: index words of the compressed rows
+  const uint16_t* Bp;  // kPrecBf16x3, kPrecSparse: split planes of H
+  uint16_t* XoutP;     // kFused: split (or compressed) planes of the next x
 };
 
 struct RowCoef {
@@ -94,6 +98,50 @@ __device__ inline void store_split4(uint16_t* row_planes, int n, const float (&v
   *reinterpret_cast<uint2*>(b + 32) = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
 }
 
+// 2:4-compressed storage of a group of 4 (the layout of the sparse product):
+// the group is stored at two positions p0 < p1, its kept positions padded
+// with the lowest free ones. kSparsePairs packs p0 | p1 << 2 for each 4-bit
+// keep pattern (patterns keeping 3 or 4 never reach a sparse solve).
+constexpr uint64_t sparse_pair_table() {
+  uint64_t t = 0;
+  for (int k = 0; k < 16; ++k) {
+    int q[2] = {0, 0}, c = 0;
+    for (int e = 0; e < 4; ++e)
+      if (((k >> e) & 1) && c < 2) q[c++] = e;
+    for (int e = 0; e < 4; ++e)
+      if (!((k >> e) & 1) && c < 2) q[c++] = e;
+    const int p0 = q[0] < q[1] ? q[0] : q[1], p1 = q[0] < q[1] ? q[1] : q[0];
+    t |= uint64_t(p0 | (p1 << 2)) << (4 * k);
+  }
+  return t;
+}
+constexpr uint64_t kSparsePairs = sparse_pair_table();
+
+__device__ inline uint32_t sparse_pair_code(const bool (&keep)[4]) {
+  const int k = int(keep[0]) | (int(keep[1]) << 1) | (int(keep[2]) << 2) | (int(keep[3]) << 3);
+  return uint32_t(kSparsePairs >> (4 * k)) & 15u;
+}
+
+// Compressed planes of the group of 4 values at column n (a multiple of 4)
+// of a row (dp / 2 stored values per plane, 2 dp bytes per row): the values
+// at the group's two stored positions (pruned values are +0), hi and lo.
+__device__ inline void store_sparse4(uint16_t* row, int n, const bool (&keep)[4],
+                                     const float (&v)[4]) {
+  const uint32_t code = sparse_pair_code(keep);
+  const int p0 = int(code & 3u), p1 = int(code >> 2);
+  float a = v[0], b = v[0];
+#pragma unroll
+  for (int e = 1; e < 4; ++e) {
+    a = e == p0 ? v[e] : a;
+    b = e == p1 ? v[e] : b;
+  }
+  const uint32_t ha = bf16_rne_bits(a), hb = bf16_rne_bits(b);
+  const uint32_t la = bf16_rne_bits(a - bf16_bits_value(ha)), lb = bf16_rne_bits(b - bf16_bits_value(hb));
+  uint16_t* blk = row + (n >> 6) * 64 + ((n & 63) >> 2) * 2;
+  *reinterpret_cast<uint32_t*>(blk) = ha | (hb << 16);
+  *reinterpret_cast<uint32_t*>(blk + 32) = la | (lb << 16);
+}
+
 // Consumes y = (H x)[j][n..n+3] for column j (n a multiple of 4).
 template <int MODE, int PREC>
 __device__ inline void epilogue4(const ProductArgs& p, int j, int n, float4 y4, const RowCoef& c) {
@@ -133,6 +181,7 @@ __device__ inline void epilogue4(const ProductArgs& p, int j, int n, float4 y4, 
     st4(p.HA + o, make_float4(ha[0], ha[1], ha[2], ha[3]));
     st4(p.Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
     if (PREC == kPrecBf16x3) store_split4(p.XoutP + size_t(j) * p.dp * 2, n, xn);
+    if (PREC == kPrecSparse) store_sparse4(p.XoutP + size_t(j) * p.dp, n, keep, xn);
   }
 }
 
@@ -208,15 +257,86 @@ __global__ void __launch_bounds__(ProductTile::kThreads) k_product(ProductArgs p
   }
 }
 
+// The iteration products with x 2:4-compressed (kPrecSparse): 256 x 128
+// tiles of 8 waves on the sparse MFMA, one workgroup per CU (132 KiB of
+// LDS). Split ranges, partial sums and the epilogue work as in k_product,
+// with partial rows padded to the 256-row tile.
+template <int MODE>
+__global__ void __launch_bounds__(SpTile::kThreads) k_product_sparse(ProductArgs p, int splits,
+                                                                     float* part) {
+  __shared__ __attribute__((aligned(1024))) char lds0[SpTile::kBufBytes];
+  __shared__ __attribute__((aligned(1024))) char lds1[SpTile::kBufBytes];
+  __shared__ __attribute__((aligned(256))) char lds_pf[256];
+  const int tiles_m = (p.n_rows + SpTile::BM - 1) / SpTile::BM;
+  const int tiles_n = p.dp / SpTile::BN;
+  const int n_tiles = tiles_m * tiles_n;
+  const int lin = blockIdx.x % n_tiles;
+  const int sp = blockIdx.x / n_tiles;
+  int tm, tn;
+  tile_of_block(lin, n_tiles, tiles_m, tiles_n, &tm, &tn);
+  const int m0 = tm * SpTile::BM, n0 = tn * SpTile::BN;
+  const int stages = p.dp / SpTile::kKPerStage;
+  const int s0 = int(int64_t(stages) * sp / splits);
+  const int s1 = int(int64_t(stages) * (sp + 1) / splits);
+
+  auto col_of = [&](int r) {
+    r = m0 + r;
+    r = r < p.n_rows ? r : p.n_rows - 1;
+    return p.rows ? p.rows[r] : r;
+  };
+  SpOperands src;
+  const char* ap = reinterpret_cast<const char*>(p.Ap);
+#pragma unroll
+  for (int i = 0; i < SpTile::kLoadsA; ++i)
+    src.a[i] = ap + size_t(col_of(sp_a_row(i))) * p.dp * 2 + size_t(s0) * SpTile::kARowBytes +
+               sp_a_seg_bytes(i);
+#pragma unroll
+  for (int i = 0; i < SpTile::kLoadsB; ++i)
+    src.b[i] = reinterpret_cast<const char*>(p.Bp) + size_t(n0 + sp_b_row(i)) * p.dp * 4 +
+               size_t(s0) * SpTile::kBRowBytes + sp_b_seg_bytes(i);
+  src.ai = reinterpret_cast<const char*>(p.Aidx) + size_t(col_of(sp_idx_row())) * (p.dp / 8) +
+           size_t(s0) * 8 + sp_idx_bytes();
+  if (sp_pf_is_a()) {
+    src.pf = ap + size_t(col_of(sp_pf_a_row())) * p.dp * 2 + size_t(s0) * SpTile::kARowBytes;
+    src.pf_stride = SpTile::kARowBytes;
+  } else {
+    src.pf = reinterpret_cast<const char*>(p.Bp) + size_t(n0 + sp_pf_b_row()) * p.dp * 4 +
+             size_t(s0) * SpTile::kBRowBytes + sp_pf_b_line();
+    src.pf_stride = SpTile::kBRowBytes;
+  }
+  f4 acc[SpTile::MB][SpTile::NB];
+  gemm_sparse_mainloop(acc, src, s1 - s0, lds0, lds1, lds_pf);
+
+  sp_stage_tile(acc, lds0, lds1);
+  __syncthreads();
+  const float L = (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f;
+  float* P = part + size_t(sp) * size_t(tiles_m) * SpTile::BM * size_t(p.dp);
+  constexpr int kChunks = SpTile::BM * SpTile::BN / 4;
+#pragma unroll 4
+  for (int q = 0; q < kChunks / SpTile::kThreads; ++q) {
+    const int c = threadIdx.x + SpTile::kThreads * q;  // 16-byte chunk of the tile
+    const int r = c >> 5, ch = c & 31;
+    const int rg = m0 + r;
+    if (rg >= p.n_rows) continue;
+    const float4 y = sp_staged_chunk(lds0, lds1, r, ch);
+    const int n = n0 + 4 * ch;
+    if (splits > 1) {
+      st4(P + size_t(rg) * p.dp + n, y);
+      continue;
+    }
+    const int j = p.rows ? p.rows[rg] : rg;
+    epilogue4<MODE, kPrecSparse>(p, j, n, y, row_coef<MODE>(p, j, L));
+  }
+}
+
 // Sums the split partials in split order and applies the product epilogue.
 template <int MODE, int PREC>
 __global__ void __launch_bounds__(kThreads) k_split_epilogue(ProductArgs p, int splits,
-                                                             const float* part) {
+                                                             int rows_pad, const float* part) {
   const int r = blockIdx.x;
   if (r >= p.n_rows) return;
   const int j = p.rows ? p.rows[r] : r;
-  const int tiles_m = (p.n_rows + kTile - 1) / kTile;
-  const size_t split_stride = size_t(tiles_m) * kTile * size_t(p.dp);
+  const size_t split_stride = size_t(rows_pad) * size_t(p.dp);
   const RowCoef c = row_coef<MODE>(p, j, (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f);
   for (int n = 4 * (blockIdx.y * kThreads + threadIdx.x); n < p.dp; n += 4 * gridDim.y * kThreads) {
     const float* q = part + size_t(r) * p.dp + n;
@@ -238,7 +358,7 @@ __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows
                                                      const float* HX, const float* HA,
                                                      const float* HW0, const uint8_t* mask,
                                                      const int* kbase, const float* Lp,
-                                                     uint16_t* XoutP) {
+                                                     uint16_t* XoutP, int sparse) {
   const int r = blockIdx.x;
   if (r >= n_rows) return;
   const int j = rows ? rows[r] : r;
@@ -264,7 +384,12 @@ __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows
     }
     st4(XA + o, make_float4(xa[0], xa[1], xa[2], xa[3]));
     st4(Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
-    if (XoutP) store_split4(XoutP + base * 2, n, xn);
+    if (XoutP) {
+      if (sparse)
+        store_sparse4(XoutP + base, n, keep, xn);
+      else
+        store_split4(XoutP + base * 2, n, xn);
+    }
   }
 }
 
@@ -306,6 +431,29 @@ __global__ void __launch_bounds__(kThreads) k_split_h(const float* Hm, int dp, u
   const int i = blockIdx.x;
   for (int n = blockIdx.y * kThreads + threadIdx.x; n < dp; n += gridDim.y * kThreads)
     store_split(HP + size_t(i) * dp * 2, n, Hm[size_t(i) * dp + n]);
+}
+
+// Index words of the 2:4-compressed layout, one thread per row, 64-column
+// block and lane group (dp / 16 words per row; word w covers columns
+// 16 w .. 16 w + 15 of the row), and flags[1] = 1 if some group of 4 keeps
+// more than 2 (the mask then has no compressed form).
+__global__ void __launch_bounds__(kThreads) k_sparse_index(const uint8_t* mask, int n_cols, int d,
+                                                           int dp, uint16_t* idx, int* flags) {
+  const int words = dp / 16;
+  const int64_t t = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (t >= int64_t(n_cols) * words) return;
+  const int j = int(t / words), w = int(t % words);
+  uint32_t word = 0;
+  bool bad = false;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    bool keep[4];
+    mask4(mask, d, j, 16 * w + 4 * q, keep);
+    bad |= int(keep[0]) + int(keep[1]) + int(keep[2]) + int(keep[3]) > 2;
+    word |= sparse_pair_code(keep) << (4 * q);
+  }
+  idx[size_t(j) * words + w] = uint16_t(word);
+  if (bad) atomicOr(flags + 1, 1);
 }
 
 // Zero-padded copy of H (used when d is not a multiple of the tile) with a
@@ -354,6 +502,7 @@ struct CheckArgs {
   int dp, d;
   float* X;            // current x
   uint16_t* XP;        // its split planes (kPrecBf16x3), else NULL
+  int sparse;          // XP holds the 2:4-compressed planes
   float* XA;
   float* HX;
   float* HA;
@@ -508,7 +657,15 @@ __global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
     for (int n = threadIdx.x; n < a.dp; n += kThreads) {
       xd[base + n] = xs[base + n];
       hd[base + n] = hs[base + n];
-      if (!(dec & 4) && a.XP) store_split(a.XP + base * 2, n, xs[base + n]);
+      if (!(dec & 4) && a.XP && !a.sparse) store_split(a.XP + base * 2, n, xs[base + n]);
+    }
+    if (!(dec & 4) && a.XP && a.sparse) {
+      for (int n = 4 * threadIdx.x; n < a.dp; n += 4 * kThreads) {
+        bool keep[4];
+        mask4(a.mask, a.d, j, n, keep);
+        const float v[4] = {xs[base + n], xs[base + n + 1], xs[base + n + 2], xs[base + n + 3]};
+        store_sparse4(a.XP + base, n, keep, v);
+      }
     }
   }
 }
@@ -698,6 +855,7 @@ struct Layout {
   float* part;
   float *X0, *X1, *XA, *HX, *HA, *HW0, *Hp, *L;
   uint16_t *XP0, *XP1, *HP;  // split planes for kPrecBf16x3
+  uint16_t* XIDX;            // index words of the 2:4-compressed x planes
   int *rows0, *rows1, *n_active, *flags;
   ColState st;
 };
@@ -721,6 +879,7 @@ Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
   l.XP0 = c.take<uint16_t>(2 * vec);
   l.XP1 = c.take<uint16_t>(2 * vec);
   l.HP = c.take<uint16_t>(2 * size_t(l.dp) * size_t(l.dp));
+  l.XIDX = c.take<uint16_t>(size_t(n_cols) * size_t(l.dp / 16));
   l.rows0 = c.take<int>(n_cols);
   l.rows1 = c.take<int>(n_cols);
   l.st.kbase = c.take<int>(n_cols);
@@ -778,18 +937,49 @@ int choose_splits(int tiles, int stages, int tiles_m, int dp, size_t part_cap) {
   return best;
 }
 
+// Number of K ranges for a tile that fills a CU with one workgroup: the
+// fewest CU rounds per unit of work, charging 5% per extra range for the
+// partial sums and their epilogue.
+int choose_splits_one_per_cu(int tiles, int stages, int rows_pad, int dp, size_t part_cap) {
+  const int n_cu = device_cu_count();
+  auto cost = [&](int S) {
+    return double(ceil_div(int64_t(tiles) * S, n_cu)) / S * (1.0 + 0.05 * (S - 1));
+  };
+  int best = 1;
+  double best_cost = cost(1);
+  for (int S = 2; S <= kMaxSplits && S <= stages; ++S) {
+    if (int64_t(tiles) * S > kMaxSplitTiles) break;
+    if (size_t(S) * size_t(rows_pad) * size_t(dp) > part_cap) break;
+    const double c = cost(S);
+    if (c < best_cost - 1e-9) {
+      best = S;
+      best_cost = c;
+    }
+  }
+  return best;
+}
+
 template <int MODE, int PREC>
 optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t s) {
-  const int tiles_m = int(ceil_div(p.n_rows, kTile));
+  const bool sparse = PREC == kPrecSparse;
+  const int bm = sparse ? SpTile::BM : kTile;
+  const int tiles_m = int(ceil_div(p.n_rows, bm));
   const int tiles_n = p.dp / kTile;
-  const int stages = p.dp * 4 / ProductTile::SRB;
-  const int S = choose_splits(tiles_m * tiles_n, stages, tiles_m, p.dp, l.part_elems);
-  hipLaunchKernelGGL((k_product<MODE, PREC>), dim3(tiles_m * tiles_n * S),
-                     dim3(ProductTile::kThreads), 0, s, p, S, l.part);
+  const int stages = sparse ? p.dp / SpTile::kKPerStage : p.dp * 4 / ProductTile::SRB;
+  const int rows_pad = tiles_m * bm;
+  const int S = sparse ? choose_splits_one_per_cu(tiles_m * tiles_n, stages, rows_pad, p.dp,
+                                                  l.part_elems)
+                       : choose_splits(tiles_m * tiles_n, stages, tiles_m, p.dp, l.part_elems);
+  if constexpr (PREC == kPrecSparse)
+    hipLaunchKernelGGL((k_product_sparse<MODE>), dim3(tiles_m * tiles_n * S),
+                       dim3(SpTile::kThreads), 0, s, p, S, l.part);
+  else
+    hipLaunchKernelGGL((k_product<MODE, PREC>), dim3(tiles_m * tiles_n * S),
+                       dim3(ProductTile::kThreads), 0, s, p, S, l.part);
   OPTIMA_LAUNCH_CHECK();
   if (S > 1) {
     const dim3 g(unsigned(p.n_rows), unsigned(ceil_div(p.dp, 4 * kThreads)));
-    hipLaunchKernelGGL((k_split_epilogue<MODE, PREC>), g, dim3(kThreads), 0, s, p, S,
+    hipLaunchKernelGGL((k_split_epilogue<MODE, PREC>), g, dim3(kThreads), 0, s, p, S, rows_pad,
                        static_cast<const float*>(l.part));
     OPTIMA_LAUNCH_CHECK();
   }
@@ -798,6 +988,7 @@ optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t 
 
 template <int MODE>
 optima_status launch_product(const ProductArgs& p, const Layout& l, int prec, hipStream_t s) {
+  if (prec == kPrecSparse) return launch_product<MODE, kPrecSparse>(p, l, s);
   return prec == kPrecBf16x3 ? launch_product<MODE, kPrecBf16x3>(p, l, s)
                              : launch_product<MODE, kPrecF32>(p, l, s);
 }
@@ -927,10 +1118,22 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
                        dim3(kThreads), 0, s, Hm, dp, l.HP);
     OPTIMA_LAUNCH_CHECK();
   }
-  int flags = 0;
-  OPTIMA_HIP_TRY(hipMemcpyAsync(&flags, l.flags, sizeof(int), hipMemcpyDeviceToHost, s));
+  // The rAPDHG iteration products skip the pruned entries on the 2:4 sparse
+  // MFMA when every group of 4 of every mask row keeps at most 2.
+  const bool try_sparse = split && !use_cg && o.sparse;
+  if (try_sparse) {
+    const int64_t words = int64_t(nc) * (dp / 16);
+    hipLaunchKernelGGL(k_sparse_index, dim3(unsigned(ceil_div(words, kThreads))), dim3(kThreads),
+                       0, s, mask, nc, di, dp, l.XIDX, l.flags);
+    OPTIMA_LAUNCH_CHECK();
+  }
+  int flags[2] = {0, 0};
+  OPTIMA_HIP_TRY(hipMemcpyAsync(flags, l.flags, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
   OPTIMA_HIP_TRY(hipStreamSynchronize(s));
-  if (flags) return OPTIMA_E_NONFINITE;
+  if (flags[0]) return OPTIMA_E_NONFINITE;
+  const bool sparse = try_sparse && !flags[1];
+  const int iprec = sparse ? int(kPrecSparse) : o.precision;
+  inf.sparse_products = sparse ? 1 : 0;
 
   ProductArgs p{};
   p.B = Hm;
@@ -942,6 +1145,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   p.rows = nullptr;
   p.n_rows = nc;
   p.Bp = l.HP;
+  p.Aidx = l.XIDX;
   // The setup products use the solve's precision too: H w0 and H x0 then
   // agree bit for bit wherever w0 and x0 do (all-kept columns start at
   // their optimum with a zero gradient).
@@ -967,6 +1171,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   ca.W0 = W0;
   ca.mask = mask;
   ca.scale = o.col_scale;
+  ca.sparse = sparse ? 1 : 0;
   ca.st = l.st;
   ca.o = o;
   ca.W_out = W_out;
@@ -1044,7 +1249,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     const dim3 ug(unsigned(n_act), unsigned(ceil_div(dp, 4 * kThreads)));
     hipLaunchKernelGGL(k_update, ug, dim3(kThreads), 0, s, rows, n_act, dp, di, xbuf[cur],
                        xbuf[cur ^ 1], l.XA, l.HX, l.HA, l.HW0, mask, l.st.kbase, l.L,
-                       split ? xpl[cur ^ 1] : nullptr);
+                       split ? xpl[cur ^ 1] : nullptr, sparse ? 1 : 0);
     OPTIMA_LAUNCH_CHECK();
     cur ^= 1;
     p.rows = rows;
@@ -1060,14 +1265,14 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
       p.Xout = xbuf[cur ^ 1];
       p.XoutP = xpl[cur ^ 1];
       p.s = i;
-      if (auto e = launch_product<kFused>(p, l, o.precision, s)) return e;
+      if (auto e = launch_product<kFused>(p, l, iprec, s)) return e;
       cur ^= 1;
     }
     p.A = xbuf[cur];
     p.Ap = xpl[cur];
     p.out1 = l.HX;
     p.s = n - 1;
-    if (auto e = launch_product<kStore>(p, l, o.precision, s)) return e;
+    if (auto e = launch_product<kStore>(p, l, iprec, s)) return e;
     if (info) OPTIMA_HIP_TRY(hipEventRecord(ev[1], s));
     inf.gemm_calls += n;
     inf.row_products += int64_t(n) * n_act;

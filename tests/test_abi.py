@@ -53,6 +53,7 @@ def test_default_options_follow_table_8():
     assert o.restarts == 1 and o.fixed_iters == 0
     assert o.precision == L.PREC_BF16X3
     assert o.method == L.METHOD_RAPDHG
+    assert o.sparse == 1
 
 
 def test_workspace_queries():
