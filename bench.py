@@ -49,8 +49,8 @@ SPECTRAL_BLOCK = 16
 
 # HBM traffic of the product kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (profiles/), valid only for the kernel sources they were taken on.
-TRAFFIC = {"sources_sha1": "b078b7a920f185dbd31db0aa772b92ac9fb206b5",
-           "bytes_per_launch": 420727 * 1024}
+TRAFFIC = {"sources_sha1": "b06fc4ceafdd0c568dbd4c46f83407cefaa77866",
+           "bytes_per_launch": 219021 * 1024}
 
 
 def log(msg: str):
