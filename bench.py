@@ -172,6 +172,46 @@ def block_leg(L, torch, dev, precision) -> dict:
             "columns_per_s": cols / (total_ms * 1e-3), "streams": streams, "layers": layers}
 
 
+def chain_leg(L, torch, dev, precision) -> dict:
+    """The layer loop of Algorithm 1 on the chain of four 4096 x 4096 layers
+    (SiLU between them) over 262144 bf16 tokens: per layer the Hessian of its
+    (pruned) inputs, the device Wanda mask, the step size, the paper-mode solve,
+    the skip rule, the layer-wise errors and the forward pass that feeds the
+    next layer. Reported: device time per layer and the error ratios."""
+    import workloads
+    from paper_2512_13886_amd.pipeline import prune_chain
+    X = workloads.x_all(workloads.CHAIN_STREAM)
+    Xd = torch.from_numpy(X.view(np.int16)).view(torch.bfloat16).to(dev)
+    del X
+    W0s = [torch.from_numpy(workloads.w0(lc)).to(dev) for lc in workloads.CHAIN_LAYERS]
+    starts = {}
+
+    def start(d):
+        if d not in starts:
+            starts[d] = torch.from_numpy(workloads.power_start_block(d, SPECTRAL_BLOCK)).to(dev)
+        return starts[d]
+
+    opts = L.SolverOpts.default()
+    if precision is not None:
+        opts.precision = precision
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    _, _, reps, _ = prune_chain(Xd, W0s, start, sparsity=0.5, rel_damp=0.01, opts=opts,
+                                timed=True)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3
+    layers = []
+    for r in reps:
+        layers.append({"d_in": r.d_in, "d_out": r.d_out, "iterations": r.iterations,
+                       "converged": r.converged, "skipped": r.skipped,
+                       "error_ratio_vs_wanda": r.error_ratio, "ms": r.ms})
+        log(f"chain layer: {r.iterations} iterations, {r.converged}/{r.d_out} converged, "
+            f"skipped {r.skipped}, error ratio {r.error_ratio:.4f}, {r.ms['total']:.1f} ms")
+    dev_ms = sum(r.ms["total"] for r in reps)
+    return {"layers": layers, "device_ms": dev_ms, "wall_ms": wall,
+            "tokens": int(Xd.shape[0]), "columns": sum(r.d_out for r in reps)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -188,6 +228,10 @@ def main() -> int:
     ap.add_argument("--block-config", action="store_true",
                     help="also prune the streamed Llama-3-8B-shaped decoder block (7 matrices, "
                          "4 calibration streams) and report its end-to-end device time")
+    ap.add_argument("--chain-config", action="store_true",
+                    help="also run the layer loop of Algorithm 1 on a chain of four 4096 x 4096 "
+                         "layers (forward propagation of the pruned activations, skip rule, "
+                         "layer-wise error ratios)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="first run one 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -429,6 +473,11 @@ def main() -> int:
         block = block_leg(L, torch, dev, None if args.precision is None else prec)
         log(f"block prune: {block['block_prune_ms']:.1f} ms for {block['columns']} columns")
 
+    chain = None
+    if args.chain_config:
+        chain = chain_leg(L, torch, dev, None if args.precision is None else prec)
+        log(f"chain: {chain['device_ms']:.1f} ms device time for {len(chain['layers'])} layers")
+
     traffic = None  # the counter passes were taken on the bf16x3 kernels
     if (TRAFFIC and prec == L.PREC_BF16X3
             and TRAFFIC.get("sources_sha1") == kernel_sources_sha1()):
@@ -512,6 +561,7 @@ def main() -> int:
         "cg_unconstrained": cg_leg,
         "jacobi_preconditioned": pre,
         "decoder_block": block,
+        "layer_chain": chain,
         "peak_device_memory_gib": torch.cuda.max_memory_allocated(dev) / 2**30,
         "roofline": roofline,
     }

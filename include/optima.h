@@ -199,6 +199,39 @@ optima_status optima_wanda_mask(const float* W0, int64_t n_cols, int64_t d,
                                 hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * Layer forward pass -- Algorithm 1: the layer outputs y = L(x) on the
+ * calibration tokens, and the activations X <- L(X) handed to the next layer
+ * once L is pruned. Also the squared output error between two weight sets.
+ * The layer-wise error of Section 4 (MSE against the dense layer's outputs,
+ * OPTIMA's over another method's) is a ratio of two such errors.
+ *
+ * Z[n_tok][d_out] = X W^T with X [n_tok][d_in] bf16 (row-major, 16-byte
+ * aligned, d_in a multiple of 64) and W [d_out][d_in] fp32 rounded to bf16
+ * on the device (round to nearest even), products exact, sums in fp32.
+ * d_out must be a multiple of 4.
+ * Y (nullable): act(Z), act OPTIMA_ACT_NONE or OPTIMA_ACT_SILU (z / (1 +
+ *   e^-z) in fp32), stored as y_dtype OPTIMA_DTYPE_BF16 (round to nearest
+ *   even, 8-byte aligned) or OPTIMA_DTYPE_F32 (16-byte aligned).
+ * err_out (nullable, device double): receives the sum over all outputs of
+ *   (Z - Y_ref)^2, accumulated in fp64 in a fixed order; Y_ref (fp32
+ *   [n_tok][d_out], 16-byte aligned) is then required when n_tok > 0: a
+ *   reference Z, e.g. the dense layer's from an earlier call with act NONE
+ *   and fp32 Y. Y_ref without err_out, or neither Y nor err_out, is
+ *   OPTIMA_E_INVAL. With n_tok = 0, X, Y and Y_ref are not read and
+ *   err_out receives 0.
+ * ws: optima_linear_forward_workspace_bytes(n_tok, d_in, d_out) bytes
+ * (the bf16 weights and per-tile partial sums). The call synchronises the
+ * stream once. It returns OPTIMA_E_NONFINITE if W holds a NaN or Inf.
+ * ------------------------------------------------------------------------- */
+#define OPTIMA_ACT_NONE 0
+#define OPTIMA_ACT_SILU 1
+size_t optima_linear_forward_workspace_bytes(int64_t n_tok, int64_t d_in, int64_t d_out);
+optima_status optima_linear_forward(const void* X, int64_t n_tok, int64_t d_in,
+                                    const float* W, int64_t d_out, int act, void* Y,
+                                    int y_dtype, const float* Y_ref, double* err_out,
+                                    void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Batched column-QP solve -- Eq. (6), Algorithm 1, Section 3.3-3.4.
  *
  * For every row j < n_cols of W0 (fp32 values) and mask (uint8), writes

@@ -85,6 +85,9 @@ _spec = _sig("optima_spectral_norm", _i32,
              [_vp, _i64, _vp, _i32, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
 _mask = _sig("optima_wanda_mask", _i32,
              [_vp, _i64, _i64, _vp, _i32, _i64, _i32, ctypes.c_double, _vp, _vp])
+_fwd_ws = _sig("optima_linear_forward_workspace_bytes", _sz, [_i64, _i64, _i64])
+_fwd = _sig("optima_linear_forward", _i32,
+            [_vp, _i64, _i64, _vp, _i64, _i32, _vp, _i32, _vp, _vp, _vp, _sz, _vp])
 _opts_default = _sig("optima_solver_opts_default", None, [ctypes.POINTER(_Opts)])
 _qp_ws = _sig("optima_qp_workspace_bytes", _sz, [_i64, _i64])
 _qp_solve = _sig("optima_qp_solve_batched", _i32,
@@ -239,6 +242,50 @@ def optima_spectral_norm(H: torch.Tensor, V0: torch.Tensor, lambda_max: torch.Te
     ws, nbytes = _workspace(optima_spectral_norm_workspace_bytes(d, block), ws, H.device)
     _check(_spec(_ptr(H), d, _ptr(V0), int(block), int(max_iters), float(tol), _ptr(ws), nbytes,
                  _ptr(lambda_max), _ptr(iters), _stream(stream)))
+
+
+ACT_NONE = 0
+ACT_SILU = 1
+
+
+def optima_linear_forward_workspace_bytes(n_tok: int, d_in: int, d_out: int) -> int:
+    return int(_fwd_ws(n_tok, d_in, d_out))
+
+
+def optima_linear_forward(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor | None = None,
+                          act: int = ACT_NONE, Y_ref: torch.Tensor | None = None,
+                          err_out: torch.Tensor | None = None, ws: torch.Tensor | None = None,
+                          stream=None) -> None:
+    """Y = act(X W^T) for X [n_tok, d_in] bfloat16 and W [d_out, d_in] float32
+    (rounded to bf16 on the device); Y bfloat16 or float32 [n_tok, d_out].
+    With Y_ref (float32 [n_tok, d_out]) err_out (float64 [1]) receives the sum
+    of (X W^T - Y_ref)^2."""
+    _need_cuda("X", X, torch.bfloat16)
+    _need_cuda("W", W, torch.float32)
+    if X.dim() != 2 or W.dim() != 2 or W.shape[1] != X.shape[1]:
+        raise ValueError("X must be [n_tok, d_in] and W [d_out, d_in]")
+    n_tok, d_in = X.shape
+    d_out = W.shape[0]
+    y_dtype = -1
+    if Y is not None:
+        _need_cuda("Y", Y)
+        y_dtype = {torch.bfloat16: DTYPE_BF16, torch.float32: DTYPE_F32}.get(Y.dtype, -1)
+        if y_dtype < 0 or Y.shape != (n_tok, d_out):
+            raise ValueError("Y must be bfloat16 or float32 [n_tok, d_out]")
+    if Y_ref is not None:
+        _need_cuda("Y_ref", Y_ref, torch.float32)
+        if Y_ref.shape != (n_tok, d_out):
+            raise ValueError("Y_ref must be [n_tok, d_out]")
+    if (Y_ref is None) != (err_out is None):
+        raise ValueError("Y_ref and err_out go together")
+    if err_out is not None:
+        _need_cuda("err_out", err_out, torch.float64)
+    ws, nbytes = _workspace(optima_linear_forward_workspace_bytes(n_tok, d_in, d_out), ws,
+                            W.device)
+    empty = n_tok == 0  # an empty tensor may report a null address
+    _check(_fwd(None if empty else _ptr(X), n_tok, d_in, _ptr(W), d_out, int(act),
+                None if empty else _ptr(Y), y_dtype, None if empty else _ptr(Y_ref),
+                _ptr(err_out), _ptr(ws), nbytes, _stream(stream)))
 
 
 MASK_UNSTRUCTURED = 0

@@ -16,6 +16,10 @@ optima_status wanda_mask(const float* W0, int64_t n_cols, int64_t d, const void*
                          int col_dtype, int64_t col_stride, int pattern, double sparsity,
                          uint8_t* mask, hipStream_t s);
 size_t qp_workspace_bytes(int64_t d, int64_t n_cols);
+size_t linear_forward_workspace_bytes(int64_t n_tok, int64_t d_in, int64_t d_out);
+optima_status linear_forward(const void* X, int64_t n_tok, int64_t d_in, const float* W,
+                             int64_t d_out, int act, void* Y, int y_dtype, const float* Y_ref,
+                             double* err_out, void* ws, hipStream_t s);
 optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const float* W0,
                        const uint8_t* mask, int64_t n_cols, const optima_solver_opts& o, void* ws,
                        float* W_out, const optima_solve_stats& stats, optima_solve_info* info,
@@ -47,7 +51,7 @@ const char* optima_status_string(optima_status status) {
   }
 }
 
-int optima_abi_version(void) { return 7; }
+int optima_abi_version(void) { return 8; }
 
 size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
   if (n_tok < 0 || d < 1 || d > kMaxDim) return 0;
@@ -130,6 +134,42 @@ optima_status optima_wanda_mask(const float* W0, int64_t n_cols, int64_t d, cons
     return OPTIMA_E_INVAL;
   return optima::wanda_mask(W0, n_cols, d, col_sq, col_sq_dtype, col_sq_stride, pattern,
                             sparsity, mask, stream);
+}
+
+size_t optima_linear_forward_workspace_bytes(int64_t n_tok, int64_t d_in, int64_t d_out) {
+  if (n_tok < 0 || d_in < 64 || d_in > kMaxDim || d_in % 64 || d_out < 4 || d_out > kMaxDim ||
+      d_out % 4)
+    return 0;
+  // one workgroup per 128 x 128 output tile; the grid stays below 2^31
+  if ((n_tok + 127) / 128 * ((d_out + 127) / 128) >= (int64_t(1) << 31)) return 0;
+  return optima::linear_forward_workspace_bytes(n_tok, d_in, d_out);
+}
+
+optima_status optima_linear_forward(const void* X, int64_t n_tok, int64_t d_in, const float* W,
+                                    int64_t d_out, int act, void* Y, int y_dtype,
+                                    const float* Y_ref, double* err_out, void* ws,
+                                    size_t ws_bytes, hipStream_t stream) {
+  const size_t need = optima_linear_forward_workspace_bytes(n_tok, d_in, d_out);
+  if (!need) return OPTIMA_E_INVAL;
+  // Nothing to do without Y or err_out; an error needs its reference (no
+  // pointer is read when n_tok == 0).
+  if (!W || (n_tok > 0 && !X) || (!Y && !err_out)) return OPTIMA_E_INVAL;
+  if ((Y_ref && !err_out) || (err_out && n_tok > 0 && !Y_ref)) return OPTIMA_E_INVAL;
+  if (act != OPTIMA_ACT_NONE && act != OPTIMA_ACT_SILU) return OPTIMA_E_INVAL;
+  if (Y && y_dtype != OPTIMA_DTYPE_BF16 && y_dtype != OPTIMA_DTYPE_F32) return OPTIMA_E_INVAL;
+  if ((X && !optima::aligned16(X)) || (reinterpret_cast<uintptr_t>(W) & 3)) return OPTIMA_E_INVAL;
+  if (Y && (reinterpret_cast<uintptr_t>(Y) & (y_dtype == OPTIMA_DTYPE_F32 ? 15 : 7)))
+    return OPTIMA_E_INVAL;
+  if (Y_ref && !optima::aligned16(Y_ref)) return OPTIMA_E_INVAL;
+  if (err_out && (reinterpret_cast<uintptr_t>(err_out) & 7)) return OPTIMA_E_INVAL;
+  const size_t ybytes = size_t(n_tok) * size_t(d_out) * (Y && y_dtype == OPTIMA_DTYPE_BF16 ? 2 : 4);
+  if (Y && (overlaps(Y, ybytes, X, size_t(n_tok) * size_t(d_in) * 2) ||
+            overlaps(Y, ybytes, W, size_t(d_out) * size_t(d_in) * 4) ||
+            (Y_ref && overlaps(Y, ybytes, Y_ref, size_t(n_tok) * size_t(d_out) * 4))))
+    return OPTIMA_E_INVAL;
+  if (!ws || ws_bytes < need) return OPTIMA_E_WORKSPACE;
+  return optima::linear_forward(X, n_tok, d_in, W, d_out, act, Y, y_dtype, Y_ref, err_out, ws,
+                                stream);
 }
 
 void optima_solver_opts_default(optima_solver_opts* o) {

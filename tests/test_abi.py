@@ -93,3 +93,26 @@ def test_validation_returns_before_launch(lib):
     assert g(vp(256), 8, vp(512), 0, 10, 1e-6, None, 0, vp(1024), None, None) == -1  # block
     assert g(vp(256), 8, vp(512), 17, 10, 1e-6, None, 0, vp(1024), None, None) == -1
     assert g(vp(256), 8, vp(512), 4, 10, 1e-6, None, 0, vp(1024), None, None) == -4  # ws
+
+
+def test_forward_queries_and_validation(lib):
+    import paper_2512_13886_amd as L
+    assert L.ACT_NONE == 0 and L.ACT_SILU == 1
+    b = L.optima_linear_forward_workspace_bytes(1000, 128, 100)
+    assert b >= 128 * 128 * 2  # bf16 weights, rows padded to the tile
+    assert L.optima_linear_forward_workspace_bytes(1000, 100, 100) == 0   # d_in % 64
+    assert L.optima_linear_forward_workspace_bytes(1000, 128, 102) == 0   # d_out % 4
+    assert L.optima_linear_forward_workspace_bytes(-1, 128, 100) == 0
+    i64, vp, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    f = lib.optima_linear_forward
+    f.restype = ctypes.c_int
+    f.argtypes = [vp, i64, i64, vp, i64, i32, vp, i32, vp, vp, vp, ctypes.c_size_t, vp]
+    X, W, Y = vp(1 << 20), vp(2 << 20), vp(4 << 20)
+    assert f(X, 10, 128, None, 8, 0, Y, 1, None, None, None, 0, None) == -1   # W is NULL
+    assert f(X, 10, 128, W, 8, 0, None, 1, None, None, None, 0, None) == -1   # nothing to do
+    assert f(X, 10, 128, W, 8, 5, Y, 1, None, None, None, 0, None) == -1      # act
+    assert f(X, 10, 128, W, 8, 0, Y, 7, None, None, None, 0, None) == -1      # y_dtype
+    assert f(X, 10, 128, W, 8, 0, None, 1, Y, None, None, 0, None) == -1      # Y_ref w/o err
+    assert f(X, 10, 128, W, 8, 0, None, 1, None, Y, None, 0, None) == -1      # err w/o Y_ref
+    assert f(vp((1 << 20) + 8), 10, 128, W, 8, 0, Y, 1, None, None, None, 0, None) == -1  # align
+    assert f(X, 10, 128, W, 8, 0, Y, 1, None, None, None, 0, None) == -4      # no workspace

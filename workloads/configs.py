@@ -111,3 +111,17 @@ class SolverSettings:
     paper_max_iters: int = 100_000
     check_every: int = 64
     tiny_fixed_iters: int = 1000
+
+# A chain of four 4096 x 4096 linear layers with SiLU between them, for the
+# layer loop of Algorithm 1 (each layer is pruned on the pruned outputs of the
+# one before). Its input stream follows the q_proj recipe (128 x 2048 bf16
+# tokens, seeds of its own); the weights are N(0, 0.015^2) with 50 %
+# unstructured masks.
+CHAIN_STREAM = LayerConfig(
+    name="chain_in", cfg_id=5, d=4096, n_cols=0, n_tok=128 * 2048, chunk=2048,
+    x_dtype="bf16", w_dtype="bf16", w_std=0.015, x_recipe="student_t_outliers",
+    mask_kind="unstructured", sparsity=0.5)
+
+CHAIN_LAYERS = tuple(
+    replace(CHAIN_STREAM, name=f"chain_l{i}", n_cols=4096, tensor_offset=10 * (i + 1))
+    for i in range(4))
