@@ -55,7 +55,9 @@ typedef int optima_status;
  *   lo = rne(v - hi), and a*b is formed as hi*hi + hi*lo + lo*hi on
  *   v_mfma_f32_16x16x32_bf16 with fp32 accumulation; the dropped terms are
  *   below 3 * 2^-16 |a b| per product. The precision applies to every
- *   product of a solve, the setup products H w0 and H x0 included. BF16X3 is
+ *   product of a solve, the setup products H w0 and H x0 included (with at
+ *   most 8 active columns the iteration products stream H once per
+ *   iteration through a 16-column MFMA kernel, with the same products). BF16X3 is
  *   the default: on the 4096-wide outlier layer its
  *   solutions differ from FP32's by under 1e-5 relative (Frobenius) and it
  *   runs the iteration about 2.5x faster. */

@@ -329,6 +329,113 @@ __global__ void __launch_bounds__(SpTile::kThreads) k_product_sparse(ProductArgs
   }
 }
 
+// The iteration products when at most kSkinnyRows columns are still active
+// (the last columns of a paper-mode solve). H is streamed once from HBM as
+// its split planes: each workgroup takes 16 rows and its 8 waves split the
+// contraction into 8 ranges. A wave computes the 16 x 16 block (active
+// vectors padded to 16) x (H rows) over its range on
+// v_mfma_f32_16x16x32_bf16 as hi*hi + hi*lo + lo*hi, the bf16x3 products of
+// the MFMA tiles; it splits the active vectors' fp32 values into hi =
+// rne(v) and lo = rne(v - hi) as it loads them. Loads of 8 K steps are in
+// flight at a time. The eight partial blocks are added in wave order, then
+// the product epilogue runs with the solve's plane layout. fp32 solves keep
+// the fp32 MFMA tiles.
+constexpr int kSkinnyRows = 8;
+constexpr int kSkinnyHRows = 16;     // H rows per workgroup
+constexpr int kSkinnyWaves = 8;      // contraction ranges per workgroup
+constexpr int kSkinnyBatch = 8;      // K steps of 32 whose loads are in flight together
+
+__device__ inline uint32_t split_pair_hi(float a, float b, uint32_t& lo) {
+  const uint32_t ha = bf16_rne_bits(a), hb = bf16_rne_bits(b);
+  const uint32_t la = bf16_rne_bits(a - bf16_bits_value(ha));
+  const uint32_t lb = bf16_rne_bits(b - bf16_bits_value(hb));
+  lo = la | (lb << 16);
+  return ha | (hb << 16);
+}
+
+// hi and lo bf16 planes of 8 consecutive fp32 values.
+__device__ inline void split8(float4 v0, float4 v1, bf16x8& hi, bf16x8& lo) {
+  uint4 h, l;
+  h.x = split_pair_hi(v0.x, v0.y, l.x);
+  h.y = split_pair_hi(v0.z, v0.w, l.y);
+  h.z = split_pair_hi(v1.x, v1.y, l.z);
+  h.w = split_pair_hi(v1.z, v1.w, l.w);
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
+template <int MODE, int PREC>
+__global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny(ProductArgs p) {
+  static_assert(PREC != kPrecF32, "bf16x3 products only");
+  __shared__ float red[kSkinnyWaves][kSkinnyHRows][kSkinnyHRows + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * kSkinnyHRows;
+  const int nr = p.n_rows;
+  const int r = lane & 15, g = lane >> 4;
+  // This lane's A row (active vector r; lanes of rows r >= nr read column
+  // rows[0] and zero what they read) and B row (the planes of H row n0 + r:
+  // per 32 columns 64 bytes of hi, then of lo).
+  const bool has_x = r < nr;
+  const float* xrow = p.A + size_t(p.rows ? p.rows[has_x ? r : 0] : (has_x ? r : 0)) * p.dp;
+  const char* hrow = reinterpret_cast<const char*>(p.Bp) + size_t(n0 + r) * p.dp * 4 + 16 * g;
+  const int steps = p.dp / 32, per = steps / kSkinnyWaves;  // dp % 256 == 0
+  const int s0 = wave * per, s1 = s0 + per;
+  f4 acc = {0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](uint4 bh4, uint4 bl4, float4 x0, float4 x1) {
+    bf16x8 ah, al;
+    split8(x0, x1, ah, al);
+    if (!has_x) ah = al = bf16x8{};
+    const bf16x8 bh = __builtin_bit_cast(bf16x8, bh4), bl = __builtin_bit_cast(bf16x8, bl4);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, acc, 0, 0, 0);
+  };
+  int st = s0;
+  for (; st + kSkinnyBatch <= s1; st += kSkinnyBatch) {
+    uint4 hh[kSkinnyBatch], hl[kSkinnyBatch];
+    float4 xv[kSkinnyBatch][2];
+#pragma unroll
+    for (int b = 0; b < kSkinnyBatch; ++b) {
+      hh[b] = *reinterpret_cast<const uint4*>(hrow + size_t(st + b) * 128);
+      hl[b] = *reinterpret_cast<const uint4*>(hrow + size_t(st + b) * 128 + 64);
+      const int k = (st + b) * 32 + 8 * g;
+      xv[b][0] = ld4(xrow + k);
+      xv[b][1] = ld4(xrow + k + 4);
+    }
+    // Keep the scheduler from sinking the loads toward their uses: all of
+    // the batch's loads go out before the first MFMA waits for data.
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int b = 0; b < kSkinnyBatch; ++b) mma(hh[b], hl[b], xv[b][0], xv[b][1]);
+  }
+  for (; st < s1; ++st) {
+    const int k = st * 32 + 8 * g;
+    mma(*reinterpret_cast<const uint4*>(hrow + size_t(st) * 128),
+        *reinterpret_cast<const uint4*>(hrow + size_t(st) * 128 + 64), ld4(xrow + k),
+        ld4(xrow + k + 4));
+  }
+  // Output (lane, e): vector 4 g + e, H row n0 + r (the dense 16 x 16 layout).
+#pragma unroll
+  for (int e = 0; e < 4; ++e) red[wave][4 * g + e][r] = acc[e];
+  __syncthreads();
+  const float L = (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f;
+  const int t = threadIdx.x;
+  if (t < 4 * nr) {
+    const int v = t >> 2, q = t & 3;
+    float y[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float a = red[0][v][4 * q + e];
+#pragma unroll
+      for (int w = 1; w < kSkinnyWaves; ++w) a += red[w][v][4 * q + e];
+      y[e] = a;
+    }
+    const int j = p.rows ? p.rows[v] : v;
+    epilogue4<MODE, PREC>(p, j, n0 + 4 * q, make_float4(y[0], y[1], y[2], y[3]),
+                          row_coef<MODE>(p, j, L));
+  }
+}
+
 // Sums the split partials in split order and applies the product epilogue.
 template <int MODE, int PREC>
 __global__ void __launch_bounds__(kThreads) k_split_epilogue(ProductArgs p, int splits,
@@ -961,6 +1068,14 @@ int choose_splits_one_per_cu(int tiles, int stages, int rows_pad, int dp, size_t
 
 template <int MODE, int PREC>
 optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t s) {
+  if constexpr ((MODE == kFused || MODE == kStore) && PREC != kPrecF32) {
+    if (p.n_rows <= kSkinnyRows && p.dp % (32 * kSkinnyWaves) == 0) {
+      hipLaunchKernelGGL((k_product_skinny<MODE, PREC>), dim3(unsigned(p.dp / kSkinnyHRows)),
+                         dim3(64 * kSkinnyWaves), 0, s, p);
+      OPTIMA_LAUNCH_CHECK();
+      return OPTIMA_OK;
+    }
+  }
   const bool sparse = PREC == kPrecSparse;
   const int bm = sparse ? SpTile::BM : kTile;
   const int tiles_m = int(ceil_div(p.n_rows, bm));
