@@ -14,6 +14,18 @@
 // epilogue, element by element, so between checks each iteration is one
 // launch. Columns that terminate leave the active list; the products then run
 // over the active rows only.
+//
+// Solves whose iteration products run on the 2:4-sparse MFMA pack every
+// per-column vector after the initial check. Group g (columns 4g..4g+3) has
+// two stored positions p0 < p1, its kept columns padded with the lowest
+// pruned ones; slot 2g + t holds the entry at position p_t. An iteration
+// never needs the entries at pruned positions: x and x_ag are zero there and
+// the gradient there is discarded. So the update moves half the bytes. A
+// slot whose position is pruned holds x = x_ag = +0 throughout. The checks
+// take f on the kept entries as
+//   f(x) = f(x0) + (x - x0)^T (H x + H x0 - 2 H w0)
+// (x - x0 vanishes off the kept set), with g0 = H x0 - H w0 packed into the
+// second half of Hx_ag's row.
 #include "common.h"
 #include "gemm_core.h"
 
@@ -48,6 +60,7 @@ struct ProductArgs {
   const uint16_t* Aidx;  // kPrecSparse: index words of the compressed rows
   const uint16_t* Bp;  // kPrecBf16x3, kPrecSparse: split planes of H
   uint16_t* XoutP;     // kFused: split (or compressed) planes of the next x
+  const uint8_t* slot; // kPrecSparse: stored positions and keep flags per group (slot_code)
 };
 
 struct RowCoef {
@@ -68,6 +81,8 @@ __device__ inline RowCoef row_coef(const ProductArgs& p, int j, float L) {
 
 __device__ inline float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 __device__ inline void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ inline float2 ld2(const float* p) { return *reinterpret_cast<const float2*>(p); }
+__device__ inline void st2(float* p, float2 v) { *reinterpret_cast<float2*>(p) = v; }
 
 // Keep flags of columns n..n+3 (n a multiple of 4) of mask row j.
 __device__ inline void mask4(const uint8_t* mask, int d, int j, int n, bool (&keep)[4]) {
@@ -122,29 +137,94 @@ __device__ inline uint32_t sparse_pair_code(const bool (&keep)[4]) {
   return uint32_t(kSparsePairs >> (4 * k)) & 15u;
 }
 
-// Compressed planes of the group of 4 values at column n (a multiple of 4)
-// of a row (dp / 2 stored values per plane, 2 dp bytes per row): the values
-// at the group's two stored positions (pruned values are +0), hi and lo.
-__device__ inline void store_sparse4(uint16_t* row, int n, const bool (&keep)[4],
-                                     const float (&v)[4]) {
+// Slot code of a group: its stored positions p0 < p1 and whether each is
+// kept, packed as p0 | p1 << 2 | kept(p0) << 4 | kept(p1) << 5.
+struct SlotCode {
+  int p0, p1;
+  bool k0, k1;
+};
+__device__ inline uint32_t slot_code_bits(const bool (&keep)[4]) {
   const uint32_t code = sparse_pair_code(keep);
   const int p0 = int(code & 3u), p1 = int(code >> 2);
+  bool k0 = keep[0], k1 = keep[0];
+#pragma unroll
+  for (int e = 1; e < 4; ++e) {
+    k0 = e == p0 ? keep[e] : k0;
+    k1 = e == p1 ? keep[e] : k1;
+  }
+  return code | (uint32_t(k0) << 4) | (uint32_t(k1) << 5);
+}
+__device__ inline SlotCode slot_code(uint32_t c) {
+  return SlotCode{int(c & 3u), int((c >> 2) & 3u), (c & 16u) != 0, (c & 32u) != 0};
+}
+// The values at positions p0 and p1 of a group of 4.
+__device__ inline float2 pick_pair(const float (&v)[4], const SlotCode& c) {
   float a = v[0], b = v[0];
 #pragma unroll
   for (int e = 1; e < 4; ++e) {
-    a = e == p0 ? v[e] : a;
-    b = e == p1 ? v[e] : b;
+    a = e == c.p0 ? v[e] : a;
+    b = e == c.p1 ? v[e] : b;
   }
+  return make_float2(a, b);
+}
+
+// Compressed planes of group g of a row (dp / 2 stored values per plane,
+// 2 dp bytes per row; per 64 columns 32 hi values, then 32 lo): the values a
+// and b at its two stored positions, hi and lo.
+__device__ inline void store_pair_planes(uint16_t* row, int g, float a, float b) {
   const uint32_t ha = bf16_rne_bits(a), hb = bf16_rne_bits(b);
   const uint32_t la = bf16_rne_bits(a - bf16_bits_value(ha)), lb = bf16_rne_bits(b - bf16_bits_value(hb));
-  uint16_t* blk = row + (n >> 6) * 64 + ((n & 63) >> 2) * 2;
+  uint16_t* blk = row + (g >> 4) * 64 + (g & 15) * 2;
   *reinterpret_cast<uint32_t*>(blk) = ha | (hb << 16);
   *reinterpret_cast<uint32_t*>(blk + 32) = la | (lb << 16);
 }
 
-// Consumes y = (H x)[j][n..n+3] for column j (n a multiple of 4).
+// Consumes y = (H x)[j][n..n+3] for column j (n a multiple of 4); the
+// iteration products of a sparse solve update the packed vectors.
+template <int MODE>
+__device__ inline void epilogue_packed(const ProductArgs& p, int j, int n, float4 y4,
+                                       const RowCoef& c) {
+  const int g = n >> 2;
+  const size_t o = size_t(j) * p.dp + 2 * g;
+  const SlotCode sc = slot_code(p.slot[size_t(j) * (p.dp >> 2) + g]);
+  const float yv[4] = {y4.x, y4.y, y4.z, y4.w};
+  const float2 y2 = pick_pair(yv, sc);
+  const float y[2] = {y2.x, y2.y};
+  const bool keep[2] = {sc.k0, sc.k1};
+  if (MODE == kStore) {
+    const float2 ha2 = ld2(p.HA + o);
+    const float hav[2] = {ha2.x, ha2.y};
+    float ha[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) ha[e] = (1.f - c.alpha) * hav[e] + c.alpha * y[e];
+    st2(p.HA + o, make_float2(ha[0], ha[1]));
+    st2(p.out1 + o, y2);
+  } else {
+    const float2 ha2 = ld2(p.HA + o), hw2 = ld2(p.HW0 + o), xi2 = ld2(p.Xin + o),
+                 xa2 = ld2(p.XA + o);
+    const float hav[2] = {ha2.x, ha2.y}, hwv[2] = {hw2.x, hw2.y};
+    const float xiv[2] = {xi2.x, xi2.y}, xav[2] = {xa2.x, xa2.y};
+    float ha[2], xn[2], xa[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      ha[e] = (1.f - c.alpha) * hav[e] + c.alpha * y[e];
+      const float gr = 2.f * ((1.f - c.alpha1) * ha[e] + c.alpha1 * y[e] - hwv[e]);
+      xn[e] = keep[e] ? xiv[e] - c.eta1 * gr : 0.f;
+      xa[e] = (1.f - c.alpha1) * xav[e] + c.alpha1 * xn[e];
+    }
+    st2(p.XA + o, make_float2(xa[0], xa[1]));
+    st2(p.HA + o, make_float2(ha[0], ha[1]));
+    st2(p.Xout + o, make_float2(xn[0], xn[1]));
+    store_pair_planes(p.XoutP + size_t(j) * p.dp, g, xn[0], xn[1]);
+  }
+}
+
 template <int MODE, int PREC>
 __device__ inline void epilogue4(const ProductArgs& p, int j, int n, float4 y4, const RowCoef& c) {
+  if (PREC == kPrecSparse && (MODE == kFused || MODE == kStore)) {
+    epilogue_packed<MODE>(p, j, n, y4, c);
+    return;
+  }
   const size_t o = size_t(j) * p.dp + n;
   if (MODE == kPlain) {
     st4(p.out1 + o, y4);
@@ -181,7 +261,6 @@ __device__ inline void epilogue4(const ProductArgs& p, int j, int n, float4 y4, 
     st4(p.HA + o, make_float4(ha[0], ha[1], ha[2], ha[3]));
     st4(p.Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
     if (PREC == kPrecBf16x3) store_split4(p.XoutP + size_t(j) * p.dp * 2, n, xn);
-    if (PREC == kPrecSparse) store_sparse4(p.XoutP + size_t(j) * p.dp, n, keep, xn);
   }
 }
 
@@ -366,7 +445,7 @@ __device__ inline void split8(float4 v0, float4 v1, bf16x8& hi, bf16x8& lo) {
 
 template <int MODE, int PREC>
 __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny(ProductArgs p) {
-  static_assert(PREC != kPrecF32, "bf16x3 products only");
+  static_assert(PREC == kPrecBf16x3, "split-plane bf16x3 products only");
   __shared__ float red[kSkinnyWaves][kSkinnyHRows][kSkinnyHRows + 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * kSkinnyHRows;
@@ -436,6 +515,91 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny(ProductArg
   }
 }
 
+// The same for sparse solves: the A operand is x's compressed planes and
+// index words, as in k_product_sparse, on v_smfmac_f32_16x16x64_bf16 (hi*hi,
+// hi*lo, lo*hi), one 64-column step per instruction. Each lane reads its 16
+// bytes of hi and of lo (the 8 stored values of columns 16 g .. 16 g + 15
+// of its vector), its 2-byte index word, and H's hi and lo planes of
+// columns 8 g .. 8 g + 7 and 32 + 8 g .. 32 + 8 g + 7. The 8 waves take
+// contiguous step ranges of near-equal length.
+constexpr int kSkinnySparseBatch = 4;  // 64-column steps whose loads are in flight together
+
+template <int MODE>
+__global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny_sparse(ProductArgs p) {
+  __shared__ float red[kSkinnyWaves][kSkinnyHRows][kSkinnyHRows + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * kSkinnyHRows;
+  const int nr = p.n_rows;
+  const int r = lane & 15, g = lane >> 4;
+  const bool has_x = r < nr;
+  const int jx = p.rows ? p.rows[has_x ? r : 0] : (has_x ? r : 0);
+  // Per 64 columns: x's planes take 128 bytes (64 hi, 64 lo), its index
+  // words 8 bytes, H's planes 256 bytes (hi, lo of the first 32 columns,
+  // then of the next 32).
+  const char* arow = reinterpret_cast<const char*>(p.Ap) + size_t(jx) * p.dp * 2 + 16 * g;
+  const char* irow = reinterpret_cast<const char*>(p.Aidx) + size_t(jx) * (p.dp / 8) + 2 * g;
+  const char* hrow = reinterpret_cast<const char*>(p.Bp) + size_t(n0 + r) * p.dp * 4 + 16 * g;
+  const int steps = p.dp / 64;
+  const int s0 = steps * wave / kSkinnyWaves, s1 = steps * (wave + 1) / kSkinnyWaves;
+  f4 acc = {0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](uint4 ah4, uint4 al4, int ix, uint4 h0, uint4 l0, uint4 h1, uint4 l1) {
+    bf16x8 ah = __builtin_bit_cast(bf16x8, ah4), al = __builtin_bit_cast(bf16x8, al4);
+    if (!has_x) ah = al = bf16x8{};
+    const bf16x16 bh = sp_b_pair(__builtin_bit_cast(bf16x8, h0), __builtin_bit_cast(bf16x8, h1));
+    const bf16x16 bl = sp_b_pair(__builtin_bit_cast(bf16x8, l0), __builtin_bit_cast(bf16x8, l1));
+    acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(ah, bh, acc, ix, 0, 0);
+    acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(ah, bl, acc, ix, 0, 0);
+    acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(al, bh, acc, ix, 0, 0);
+  };
+  auto ld16 = [](const char* q) { return *reinterpret_cast<const uint4*>(q); };
+  int st = s0;
+  for (; st + kSkinnySparseBatch <= s1; st += kSkinnySparseBatch) {
+    uint4 ah[kSkinnySparseBatch], al[kSkinnySparseBatch], h0[kSkinnySparseBatch],
+        l0[kSkinnySparseBatch], h1[kSkinnySparseBatch], l1[kSkinnySparseBatch];
+    int ix[kSkinnySparseBatch];
+#pragma unroll
+    for (int b = 0; b < kSkinnySparseBatch; ++b) {
+      const char* a = arow + size_t(st + b) * 128;
+      const char* h = hrow + size_t(st + b) * 256;
+      ah[b] = ld16(a);
+      al[b] = ld16(a + 64);
+      ix[b] = *reinterpret_cast<const uint16_t*>(irow + size_t(st + b) * 8);
+      h0[b] = ld16(h);
+      l0[b] = ld16(h + 64);
+      h1[b] = ld16(h + 128);
+      l1[b] = ld16(h + 192);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int b = 0; b < kSkinnySparseBatch; ++b) mma(ah[b], al[b], ix[b], h0[b], l0[b], h1[b], l1[b]);
+  }
+  for (; st < s1; ++st) {
+    const char* a = arow + size_t(st) * 128;
+    const char* h = hrow + size_t(st) * 256;
+    mma(ld16(a), ld16(a + 64), *reinterpret_cast<const uint16_t*>(irow + size_t(st) * 8), ld16(h),
+        ld16(h + 64), ld16(h + 128), ld16(h + 192));
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) red[wave][4 * g + e][r] = acc[e];
+  __syncthreads();
+  const float L = *p.Lp;
+  const int t = threadIdx.x;
+  if (t < 4 * nr) {
+    const int v = t >> 2, q = t & 3;
+    float y[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float a = red[0][v][4 * q + e];
+#pragma unroll
+      for (int w = 1; w < kSkinnyWaves; ++w) a += red[w][v][4 * q + e];
+      y[e] = a;
+    }
+    const int j = p.rows ? p.rows[v] : v;
+    epilogue_packed<MODE>(p, j, n0 + 4 * q, make_float4(y[0], y[1], y[2], y[3]),
+                          row_coef<MODE>(p, j, L));
+  }
+}
+
 // Sums the split partials in split order and applies the product epilogue.
 template <int MODE, int PREC>
 __global__ void __launch_bounds__(kThreads) k_split_epilogue(ProductArgs p, int splits,
@@ -460,12 +624,14 @@ __global__ void __launch_bounds__(kThreads) k_split_epilogue(ProductArgs p, int 
 }
 
 // Iteration update from the stored products (first iteration after a check).
+// With `sparse` the vectors are packed and slot gives each group's code.
 __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows, int dp, int d,
                                                      const float* X, float* Xout, float* XA,
                                                      const float* HX, const float* HA,
                                                      const float* HW0, const uint8_t* mask,
                                                      const int* kbase, const float* Lp,
-                                                     uint16_t* XoutP, int sparse) {
+                                                     uint16_t* XoutP, int sparse,
+                                                     const uint8_t* slot) {
   const int r = blockIdx.x;
   if (r >= n_rows) return;
   const int j = rows ? rows[r] : r;
@@ -473,6 +639,29 @@ __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows
   const float alpha = 2.f / (k + 2.f);
   const float eta = (k + 1.f) / (2.f * *Lp);
   const size_t base = size_t(j) * dp;
+  if (sparse) {
+    const int groups = dp / 4;
+    for (int g = blockIdx.y * kThreads + threadIdx.x; g < groups; g += gridDim.y * kThreads) {
+      const size_t o = base + 2 * g;
+      const SlotCode c = slot_code(slot[size_t(j) * groups + g]);
+      const float2 ha2 = ld2(HA + o), hx2 = ld2(HX + o), hw2 = ld2(HW0 + o), x2 = ld2(X + o),
+                   xa2 = ld2(XA + o);
+      const float hav[2] = {ha2.x, ha2.y}, hxv[2] = {hx2.x, hx2.y}, hwv[2] = {hw2.x, hw2.y};
+      const float xv[2] = {x2.x, x2.y}, xav[2] = {xa2.x, xa2.y};
+      const bool keep[2] = {c.k0, c.k1};
+      float xn[2], xa[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const float gr = 2.f * ((1.f - alpha) * hav[e] + alpha * hxv[e] - hwv[e]);
+        xn[e] = keep[e] ? xv[e] - eta * gr : 0.f;
+        xa[e] = (1.f - alpha) * xav[e] + alpha * xn[e];
+      }
+      st2(XA + o, make_float2(xa[0], xa[1]));
+      st2(Xout + o, make_float2(xn[0], xn[1]));
+      store_pair_planes(XoutP + base, g, xn[0], xn[1]);
+    }
+    return;
+  }
   for (int n = 4 * (blockIdx.y * kThreads + threadIdx.x); n < dp; n += 4 * gridDim.y * kThreads) {
     const size_t o = base + n;
     const float4 ha4 = ld4(HA + o), hx4 = ld4(HX + o), hw4 = ld4(HW0 + o), x4 = ld4(X + o),
@@ -491,11 +680,49 @@ __global__ void __launch_bounds__(kThreads) k_update(const int* rows, int n_rows
     }
     st4(XA + o, make_float4(xa[0], xa[1], xa[2], xa[3]));
     st4(Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
-    if (XoutP) {
-      if (sparse)
-        store_sparse4(XoutP + base, n, keep, xn);
-      else
-        store_split4(XoutP + base * 2, n, xn);
+    if (XoutP) store_split4(XoutP + base * 2, n, xn);
+  }
+}
+
+// Packs the state of the active columns of a sparse solve after the initial
+// check: x (X, in place) and x_ag (XA) from x0, Hx (HX, in place) and Hx_ag
+// (HA) from H x0, Hw0 (HW0, in place), and g0 = H x0 - H w0 into the second
+// half of HA's row. Slot 2g + t comes from position 4g + p_t >= 2g + t, so
+// in place a write never lands beyond its source. Chunks of kThreads groups
+// go in order with a barrier between a chunk's reads and its writes: chunk c
+// reads positions from 4 kThreads c on and writes slots below
+// 2 kThreads (c + 1), so only the chunk's own reads can be overwritten.
+__global__ void __launch_bounds__(kThreads) k_pack(const int* rows, int n_rows, int dp,
+                                                   const uint8_t* slot, float* X, float* XA,
+                                                   float* HX, float* HA, float* HW0) {
+  const int r = blockIdx.x;
+  if (r >= n_rows) return;
+  const int j = rows ? rows[r] : r;
+  const size_t base = size_t(j) * dp;
+  const int groups = dp / 4;
+  for (int c0 = 0; c0 < groups; c0 += kThreads) {
+    const int g = c0 + threadIdx.x;
+    const bool on = g < groups;
+    float2 x = make_float2(0.f, 0.f), hx = x, hw = x;
+    if (on) {
+      const SlotCode c = slot_code(slot[size_t(j) * groups + g]);
+      const float4 x4 = ld4(X + base + 4 * g), h4 = ld4(HX + base + 4 * g),
+                   w4 = ld4(HW0 + base + 4 * g);
+      const float xv[4] = {x4.x, x4.y, x4.z, x4.w}, hv[4] = {h4.x, h4.y, h4.z, h4.w},
+                  wv[4] = {w4.x, w4.y, w4.z, w4.w};
+      x = pick_pair(xv, c);
+      hx = pick_pair(hv, c);
+      hw = pick_pair(wv, c);
+    }
+    __syncthreads();
+    if (on) {
+      const size_t o = base + 2 * g;
+      st2(X + o, x);
+      st2(XA + o, x);
+      st2(HX + o, hx);
+      st2(HA + o, hx);
+      st2(HW0 + o, hw);
+      st2(HA + base + dp / 2 + 2 * g, make_float2(hx.x - hw.x, hx.y - hw.y));
     }
   }
 }
@@ -542,15 +769,17 @@ __global__ void __launch_bounds__(kThreads) k_split_h(const float* Hm, int dp, u
 
 // Index words of the 2:4-compressed layout, one thread per row, 64-column
 // block and lane group (dp / 16 words per row; word w covers columns
-// 16 w .. 16 w + 15 of the row), and flags[1] = 1 if some group of 4 keeps
-// more than 2 (the mask then has no compressed form).
+// 16 w .. 16 w + 15 of the row), the slot codes of those 4 groups (dp / 4
+// bytes per row), and flags[1] = 1 if some group of 4 keeps more than 2
+// (the mask then has no compressed form).
 __global__ void __launch_bounds__(kThreads) k_sparse_index(const uint8_t* mask, int n_cols, int d,
-                                                           int dp, uint16_t* idx, int* flags) {
+                                                           int dp, uint16_t* idx, uint8_t* slot,
+                                                           int* flags) {
   const int words = dp / 16;
   const int64_t t = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (t >= int64_t(n_cols) * words) return;
   const int j = int(t / words), w = int(t % words);
-  uint32_t word = 0;
+  uint32_t word = 0, codes = 0;
   bool bad = false;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -558,8 +787,10 @@ __global__ void __launch_bounds__(kThreads) k_sparse_index(const uint8_t* mask, 
     mask4(mask, d, j, 16 * w + 4 * q, keep);
     bad |= int(keep[0]) + int(keep[1]) + int(keep[2]) + int(keep[3]) > 2;
     word |= sparse_pair_code(keep) << (4 * q);
+    codes |= slot_code_bits(keep) << (8 * q);
   }
   idx[size_t(j) * words + w] = uint16_t(word);
+  *reinterpret_cast<uint32_t*>(slot + size_t(j) * (dp / 4) + 4 * w) = codes;
   if (bad) atomicOr(flags + 1, 1);
 }
 
@@ -601,6 +832,7 @@ struct ColState {
   double* f_anchor;
   double* c_norm;     // ||2 H w0||_2
   double* w0hw0;      // w0^T H w0
+  double* f_start;    // f(x0)
 };
 
 struct CheckArgs {
@@ -609,7 +841,9 @@ struct CheckArgs {
   int dp, d;
   float* X;            // current x
   uint16_t* XP;        // its split planes (kPrecBf16x3), else NULL
-  int sparse;          // XP holds the 2:4-compressed planes
+  int packed;          // sparse solve after the initial check: packed vectors,
+                       // XP holds the 2:4-compressed planes
+  const uint8_t* slot; // slot codes (packed)
   float* XA;
   float* HX;
   float* HA;
@@ -641,7 +875,42 @@ __global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
   // are taken with the gradient in the original coordinates (divided by D),
   // gap, f and z^T H z are the same in both.
   double rdx = 0, gpx = 0, fx = 0, qx = 0, rda = 0, gpa = 0, fa = 0, qa = 0, cn = 0, wq = 0;
-  for (int n = threadIdx.x; n < a.d; n += kThreads) {
+  const int groups = a.dp / 4;
+  const uint8_t* sl = a.packed ? a.slot + size_t(j) * groups : nullptr;
+  // Packed: sums over the stored slots; f is accumulated as
+  // (z - x0)^T (H z - H w0 + g0) and f(x0) is added after the reduction.
+  for (int g = threadIdx.x; a.packed && g < groups; g += kThreads) {
+    const SlotCode c = slot_code(sl[g]);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const size_t o = base + 2 * g + t;
+      const bool keep = t ? c.k1 : c.k0;
+      const int n = 4 * g + (t ? c.p1 : c.p0);
+      float x0f = 0.f;
+      double inv = 1.0;
+      if (keep) {
+        x0f = a.W0[size_t(j) * a.d + n];
+        if (a.scale) {
+          x0f = x0f / a.scale[n];
+          inv = 1.0 / double(a.scale[n]);
+        }
+      }
+      const double x0 = x0f, hw = a.HW0[o], g0 = a.HA[base + a.dp / 2 + 2 * g + t];
+      const double x = a.X[o], hx = a.HX[o];
+      const double gx = 2.0 * (hx - hw);
+      rdx += keep ? (gx * inv) * (gx * inv) : 0.0;
+      gpx += x * gx;
+      fx += (x - x0) * ((hx - hw) + g0);
+      qx += x * hx;
+      const double xa = a.XA[o], ha = a.HA[o];
+      const double ga = 2.0 * (ha - hw);
+      rda += keep ? (ga * inv) * (ga * inv) : 0.0;
+      gpa += xa * ga;
+      fa += (xa - x0) * ((ha - hw) + g0);
+      qa += xa * ha;
+    }
+  }
+  for (int n = threadIdx.x; !a.packed && n < a.d; n += kThreads) {
     const size_t o = base + n;
     const double hw = a.HW0[o];
     const double inv = a.scale ? 1.0 / double(a.scale[n]) : 1.0;
@@ -691,6 +960,10 @@ __global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
     } else {
       c_norm = st.c_norm[j];
       w0hw0 = st.w0hw0[j];
+      if (a.packed) {
+        fx += st.f_start[j];
+        fa += st.f_start[j];
+      }
     }
     const double rd_x = sqrt(rdx), gap_x = fabs(gpx), kkt_x = sqrt(rd_x * rd_x + gap_x * gap_x);
     double rd_c = rd_x, gap_c = gap_x, kkt_c = kkt_x, f_c = fx, q_c = qx;
@@ -712,6 +985,7 @@ __global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
     int dec = cand_x ? 4 : 0;
     if (a.initial) {
       if (a.stats.f_initial) a.stats.f_initial[j] = float(fx);
+      st.f_start[j] = fx;
       st.kkt_restart[j] = kkt_x;
       st.kkt_prev[j] = kkt_x;
       st.f_anchor[j] = fx;
@@ -754,26 +1028,33 @@ __global__ void __launch_bounds__(kThreads) k_check(CheckArgs a) {
   const int dec = decision;
   if (dec & 1) {
     const float* src = (dec & 4) ? a.X : a.XA;
-    for (int n = threadIdx.x; n < a.d; n += kThreads)
-      a.W_out[size_t(j) * a.d + n] = a.scale ? src[base + n] * a.scale[n] : src[base + n];
+    for (int n = threadIdx.x; n < a.d; n += kThreads) {
+      float v;
+      if (a.packed) {  // +0 at pruned positions
+        const SlotCode c = slot_code(sl[n >> 2]);
+        const int e = n & 3;
+        v = c.k0 && e == c.p0 ? src[base + 2 * (n >> 2)]
+            : c.k1 && e == c.p1 ? src[base + 2 * (n >> 2) + 1]
+                                : 0.f;
+      } else {
+        v = src[base + n];
+      }
+      a.W_out[size_t(j) * a.d + n] = a.scale ? v * a.scale[n] : v;
+    }
   } else if (dec & 2) {
     float* xd = (dec & 4) ? a.XA : a.X;
     float* hd = (dec & 4) ? a.HA : a.HX;
     const float* xs = (dec & 4) ? a.X : a.XA;
     const float* hs = (dec & 4) ? a.HX : a.HA;
-    for (int n = threadIdx.x; n < a.dp; n += kThreads) {
+    const int len = a.packed ? a.dp / 2 : a.dp;
+    for (int n = threadIdx.x; n < len; n += kThreads) {
       xd[base + n] = xs[base + n];
       hd[base + n] = hs[base + n];
-      if (!(dec & 4) && a.XP && !a.sparse) store_split(a.XP + base * 2, n, xs[base + n]);
+      if (!(dec & 4) && a.XP && !a.packed) store_split(a.XP + base * 2, n, xs[base + n]);
     }
-    if (!(dec & 4) && a.XP && a.sparse) {
-      for (int n = 4 * threadIdx.x; n < a.dp; n += 4 * kThreads) {
-        bool keep[4];
-        mask4(a.mask, a.d, j, n, keep);
-        const float v[4] = {xs[base + n], xs[base + n + 1], xs[base + n + 2], xs[base + n + 3]};
-        store_sparse4(a.XP + base, n, keep, v);
-      }
-    }
+    if (!(dec & 4) && a.XP && a.packed)
+      for (int g = threadIdx.x; g < groups; g += kThreads)
+        store_pair_planes(a.XP + base, g, xs[base + 2 * g], xs[base + 2 * g + 1]);
   }
 }
 
@@ -963,6 +1244,7 @@ struct Layout {
   float *X0, *X1, *XA, *HX, *HA, *HW0, *Hp, *L;
   uint16_t *XP0, *XP1, *HP;  // split planes for kPrecBf16x3
   uint16_t* XIDX;            // index words of the 2:4-compressed x planes
+  uint8_t* SLOT;             // slot codes of the packed vectors, dp / 4 per column
   int *rows0, *rows1, *n_active, *flags;
   ColState st;
 };
@@ -987,6 +1269,7 @@ Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
   l.XP1 = c.take<uint16_t>(2 * vec);
   l.HP = c.take<uint16_t>(2 * size_t(l.dp) * size_t(l.dp));
   l.XIDX = c.take<uint16_t>(size_t(n_cols) * size_t(l.dp / 16));
+  l.SLOT = c.take<uint8_t>(size_t(n_cols) * size_t(l.dp / 4));
   l.rows0 = c.take<int>(n_cols);
   l.rows1 = c.take<int>(n_cols);
   l.st.kbase = c.take<int>(n_cols);
@@ -997,6 +1280,7 @@ Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
   l.st.f_anchor = c.take<double>(n_cols);
   l.st.c_norm = c.take<double>(n_cols);
   l.st.w0hw0 = c.take<double>(n_cols);
+  l.st.f_start = c.take<double>(n_cols);
   l.n_active = c.take<int>(4);
   l.flags = c.take<int>(4);
   l.L = c.take<float>(4);
@@ -1068,7 +1352,15 @@ int choose_splits_one_per_cu(int tiles, int stages, int rows_pad, int dp, size_t
 
 template <int MODE, int PREC>
 optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t s) {
-  if constexpr ((MODE == kFused || MODE == kStore) && PREC != kPrecF32) {
+  if constexpr ((MODE == kFused || MODE == kStore) && PREC == kPrecSparse) {
+    if (p.n_rows <= kSkinnyRows) {
+      hipLaunchKernelGGL((k_product_skinny_sparse<MODE>), dim3(unsigned(p.dp / kSkinnyHRows)),
+                         dim3(64 * kSkinnyWaves), 0, s, p);
+      OPTIMA_LAUNCH_CHECK();
+      return OPTIMA_OK;
+    }
+  }
+  if constexpr ((MODE == kFused || MODE == kStore) && PREC == kPrecBf16x3) {
     if (p.n_rows <= kSkinnyRows && p.dp % (32 * kSkinnyWaves) == 0) {
       hipLaunchKernelGGL((k_product_skinny<MODE, PREC>), dim3(unsigned(p.dp / kSkinnyHRows)),
                          dim3(64 * kSkinnyWaves), 0, s, p);
@@ -1239,7 +1531,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   if (try_sparse) {
     const int64_t words = int64_t(nc) * (dp / 16);
     hipLaunchKernelGGL(k_sparse_index, dim3(unsigned(ceil_div(words, kThreads))), dim3(kThreads),
-                       0, s, mask, nc, di, dp, l.XIDX, l.flags);
+                       0, s, mask, nc, di, dp, l.XIDX, l.SLOT, l.flags);
     OPTIMA_LAUNCH_CHECK();
   }
   int flags[2] = {0, 0};
@@ -1261,6 +1553,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   p.n_rows = nc;
   p.Bp = l.HP;
   p.Aidx = l.XIDX;
+  p.slot = l.SLOT;
   // The setup products use the solve's precision too: H w0 and H x0 then
   // agree bit for bit wherever w0 and x0 do (all-kept columns start at
   // their optimum with a zero gradient).
@@ -1286,7 +1579,8 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   ca.W0 = W0;
   ca.mask = mask;
   ca.scale = o.col_scale;
-  ca.sparse = sparse ? 1 : 0;
+  ca.packed = 0;
+  ca.slot = l.SLOT;
   ca.st = l.st;
   ca.o = o;
   ca.W_out = W_out;
@@ -1325,6 +1619,12 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   int n_act = 0;
   OPTIMA_HIP_TRY(hipMemcpyAsync(&n_act, l.n_active, sizeof(int), hipMemcpyDeviceToHost, s));
   OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  if (sparse && n_act > 0) {
+    hipLaunchKernelGGL(k_pack, dim3(unsigned(n_act)), dim3(kThreads), 0, s, l.rows0, n_act, dp,
+                       l.SLOT, l.X0, l.XA, l.HX, l.HA, l.HW0);
+    OPTIMA_LAUNCH_CHECK();
+    ca.packed = 1;
+  }
 
   // Optional timing of the iteration loop's product launches.
   hipEvent_t ev[2] = {nullptr, nullptr};
@@ -1364,7 +1664,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     const dim3 ug(unsigned(n_act), unsigned(ceil_div(dp, 4 * kThreads)));
     hipLaunchKernelGGL(k_update, ug, dim3(kThreads), 0, s, rows, n_act, dp, di, xbuf[cur],
                        xbuf[cur ^ 1], l.XA, l.HX, l.HA, l.HW0, mask, l.st.kbase, l.L,
-                       split ? xpl[cur ^ 1] : nullptr, sparse ? 1 : 0);
+                       split ? xpl[cur ^ 1] : nullptr, sparse ? 1 : 0, l.SLOT);
     OPTIMA_LAUNCH_CHECK();
     cur ^= 1;
     p.rows = rows;
