@@ -364,8 +364,6 @@ struct SpOperands {
   const char* a[SpTile::kLoadsA];  // A segment of this thread's direct loads at stage 0
   const char* b[SpTile::kLoadsB];  // B segment of this thread's direct loads at stage 0
   const char* ai;                  // its 4 bytes of index words at stage 0
-  const char* pf;                  // the 128-byte line it touches ahead (see sp_prefetch_line)
-  int pf_stride;                   // that line's advance per stage (128 for A, 256 for B)
 };
 
 // Tile rows fetched by this thread's direct loads and the byte offset of the
@@ -390,24 +388,6 @@ __device__ inline int sp_b_seg_bytes(int i) {
 }
 __device__ inline int sp_idx_row() { return (threadIdx.x >> 6) * 32 + (threadIdx.x & 63) / 2; }
 __device__ inline int sp_idx_bytes() { return (threadIdx.x & 1) * 4; }
-
-// L2 prefetch one stage further ahead. A stage's operands are 512 lines of
-// 128 bytes (one per A row, two per B row); every lane touches one of them
-// with a 4-byte direct load into a scratch LDS area nobody reads: lanes
-// 0-31 of wave w take A rows 32 w .. 32 w + 31, lanes 32-63 the two lines of
-// B rows 16 w .. 16 w + 15. The stage loop waits on these one stage later
-// than on the real loads, so two stages of operands are in flight with LDS
-// room for only two.
-__device__ inline int sp_pf_a_row() { return (threadIdx.x >> 6) * 32 + (threadIdx.x & 31); }
-__device__ inline int sp_pf_b_row() { return (threadIdx.x >> 6) * 16 + ((threadIdx.x & 31) >> 1); }
-__device__ inline int sp_pf_b_line() { return (threadIdx.x & 1) * 128; }
-__device__ inline bool sp_pf_is_a() { return (threadIdx.x & 63) < 32; }
-
-__device__ inline void sp_prefetch_line(const SpOperands& src, int s, char* scratch) {
-  __builtin_amdgcn_global_load_lds(
-      (const __attribute__((address_space(1))) void*)(src.pf + size_t(s) * src.pf_stride),
-      (__attribute__((address_space(3))) void*)(scratch), 4, 0, 0);
-}
 
 __device__ inline void sp_issue_stage(const SpOperands& src, int s, char* buf) {
   const int wave = threadIdx.x >> 6;
@@ -481,7 +461,7 @@ __device__ inline void sp_compute_stage(f4 (&acc)[SpTile::MB][SpTile::NB], const
       acc[mi][ni] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(al[mi],
                                                               bh, acc[mi][ni], ix[mi], 0, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x020, SpTile::kLoadsA + SpTile::kLoadsB + 2, 0);
+  __builtin_amdgcn_sched_group_barrier(0x020, SpTile::kLoadsA + SpTile::kLoadsB + 1, 0);
   __builtin_amdgcn_sched_group_barrier(0x100, 3 * MB + 8, 0);
 #pragma unroll
   for (int ni = 0; ni < NB - 2; ++ni) {
@@ -491,41 +471,37 @@ __device__ inline void sp_compute_stage(f4 (&acc)[SpTile::MB][SpTile::NB], const
   __builtin_amdgcn_sched_group_barrier(0x008, 6 * MB, 0);
 }
 
-// n stages (of 64 K values) of the sparse product, starting at the stage the
-// operand addresses point to; lds0 / lds1 are distinct __shared__ arrays of
-// SpTile::kBufBytes.
-// Stage barrier of the sparse loop: this wave's direct loads except the
-// newest one (the prefetch touch) and its LDS reads are complete, then all
-// waves meet. __syncthreads() would also drain the prefetch (its release
-// fence waits for every outstanding load). The empty asm statements keep
-// the compiler from moving memory accesses across the barrier.
+// Stage barrier of the sparse loop: this wave's direct loads and LDS reads
+// are complete, then all waves meet. The empty asm statements keep the
+// compiler from moving memory accesses across the barrier.
 __device__ inline void sp_stage_barrier() {
   asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(1 | 0x70);  // vmcnt(1) lgkmcnt(0)
+  __builtin_amdgcn_s_waitcnt(0 | 0x70);  // vmcnt(0) lgkmcnt(0)
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
 
+// n stages (of 64 K values) of the sparse product, starting at the stage the
+// operand addresses point to; lds0 / lds1 are distinct __shared__ arrays of
+// SpTile::kBufBytes. The loads of stage s + 1 run during the compute of
+// stage s. (An L2 prefetch touch of stage s + 2 was measured to cost more in
+// load requests than it saved in latency.)
 __device__ inline void gemm_sparse_mainloop(f4 (&acc)[SpTile::MB][SpTile::NB],
                                             const SpOperands& src, int n, char* lds0,
-                                            char* lds1, char* scratch) {
+                                            char* lds1) {
 #pragma unroll
   for (int mi = 0; mi < SpTile::MB; ++mi)
 #pragma unroll
     for (int ni = 0; ni < SpTile::NB; ++ni) acc[mi][ni] = f4{0.f, 0.f, 0.f, 0.f};
   if (n <= 0) return;
-  auto cl = [n](int s) { return s < n ? s : n - 1; };
   sp_issue_stage(src, 0, lds0);
-  sp_prefetch_line(src, cl(1), scratch);
   int s = 0;
   for (; s + 1 < n; s += 2) {
     sp_stage_barrier();
     sp_issue_stage(src, s + 1, lds1);
-    sp_prefetch_line(src, cl(s + 2), scratch);
     sp_compute_stage(acc, lds0);
     sp_stage_barrier();
-    sp_issue_stage(src, cl(s + 2), lds0);
-    sp_prefetch_line(src, cl(s + 3), scratch);
+    if (s + 2 < n) sp_issue_stage(src, s + 2, lds0);
     sp_compute_stage(acc, lds1);
   }
   if (s < n) {  // odd count: the last stage is in lds0

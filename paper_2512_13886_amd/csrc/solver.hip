@@ -345,7 +345,6 @@ __global__ void __launch_bounds__(SpTile::kThreads) k_product_sparse(ProductArgs
                                                                      float* part) {
   __shared__ __attribute__((aligned(1024))) char lds0[SpTile::kBufBytes];
   __shared__ __attribute__((aligned(1024))) char lds1[SpTile::kBufBytes];
-  __shared__ __attribute__((aligned(256))) char lds_pf[256];
   const int tiles_m = (p.n_rows + SpTile::BM - 1) / SpTile::BM;
   const int tiles_n = p.dp / SpTile::BN;
   const int n_tiles = tiles_m * tiles_n;
@@ -375,16 +374,8 @@ __global__ void __launch_bounds__(SpTile::kThreads) k_product_sparse(ProductArgs
                size_t(s0) * SpTile::kBRowBytes + sp_b_seg_bytes(i);
   src.ai = reinterpret_cast<const char*>(p.Aidx) + size_t(col_of(sp_idx_row())) * (p.dp / 8) +
            size_t(s0) * 8 + sp_idx_bytes();
-  if (sp_pf_is_a()) {
-    src.pf = ap + size_t(col_of(sp_pf_a_row())) * p.dp * 2 + size_t(s0) * SpTile::kARowBytes;
-    src.pf_stride = SpTile::kARowBytes;
-  } else {
-    src.pf = reinterpret_cast<const char*>(p.Bp) + size_t(n0 + sp_pf_b_row()) * p.dp * 4 +
-             size_t(s0) * SpTile::kBRowBytes + sp_pf_b_line();
-    src.pf_stride = SpTile::kBRowBytes;
-  }
   f4 acc[SpTile::MB][SpTile::NB];
-  gemm_sparse_mainloop(acc, src, s1 - s0, lds0, lds1, lds_pf);
+  gemm_sparse_mainloop(acc, src, s1 - s0, lds0, lds1);
 
   sp_stage_tile(acc, lds0, lds1);
   __syncthreads();
