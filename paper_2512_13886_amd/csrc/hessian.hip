@@ -314,9 +314,46 @@ __device__ inline void compute(f4 (&acc)[C::kMB][C::kNB], const char* buf) {
 
 }  // namespace dt
 
-// X: [n_rows][d] bf16 with n_rows >= stages * 64. Workgroup b handles split
-// sp = b / n_tiles of tile b % n_tiles of the triangle of d / 256 blocks;
-// split sp covers stages [stages sp / splits, stages (sp + 1) / splits).
+// Lower-triangle tile (ti >= tj) of position idx in an order that keeps
+// nearby positions on few feature blocks: the triangle of nt blocks is cut
+// into super-tiles of 4 x 4 blocks, taken row by row (SI >= SJ), and each
+// super-tile's tiles row by row. 32 consecutive positions touch 8 to 12
+// blocks instead of nearly all of them.
+__device__ inline void grouped_tri_tile(int idx, int nt, int* ti, int* tj) {
+  constexpr int G = 4;
+  const int ns = (nt + G - 1) / G;
+  *ti = 0;
+  *tj = 0;
+  for (int SI = 0; SI < ns; ++SI)
+    for (int SJ = 0; SJ <= SI; ++SJ) {
+      const int i0 = G * SI, i1 = min(i0 + G, nt), j0 = G * SJ, j1 = min(j0 + G, nt);
+      const int w = j1 - j0, m = i1 - i0;
+      const int cnt = SI != SJ ? m * w : m * (m + 1) / 2;
+      if (idx < cnt) {
+        if (SI != SJ) {
+          *ti = i0 + idx / w;
+          *tj = j0 + idx % w;
+        } else {
+          int r = 0;
+          while (idx > r) idx -= ++r;
+          *ti = i0 + r;
+          *tj = j0 + idx;
+        }
+        return;
+      }
+      idx -= cnt;
+    }
+}
+
+// X: [n_rows][d] bf16 with n_rows >= stages * 64. The work units are the
+// (split, tile) pairs of the triangle of d / 256 blocks, split-major, tiles
+// in grouped_tri_tile order; split sp covers stages
+// [stages sp / splits, stages (sp + 1) / splits). The dispatcher sends
+// workgroup b to XCD b % 8, so XCD x runs workgroups x, x + 8, ... in that
+// order; it takes the x-th eighth of the units as one contiguous range.
+// Its 32 resident workgroups then share one token range and few feature
+// blocks, which its L2 fetches once for all of them. The grid is 8 times
+// the longest range; workgroups beyond their XCD's range exit at once.
 // Writes (first) or adds the tile's partial sum into part[sp] ([d][d] fp32).
 template <int WAVES>
 __global__ void __launch_bounds__(64 * WAVES) k_syrk_direct(const uint16_t* X, int64_t d,
@@ -326,14 +363,16 @@ __global__ void __launch_bounds__(64 * WAVES) k_syrk_direct(const uint16_t* X, i
   using C = Cfg<WAVES>;
   __shared__ __attribute__((aligned(1024))) char lds0[kBufBytes];
   __shared__ __attribute__((aligned(1024))) char lds1[kBufBytes];
-  // Split-major order: the workgroups resident at one time work on one or
-  // two token ranges, so every block of X they share is fetched into the
-  // L2 / MALL once for all of them.
-  const int n_tiles = int(gridDim.x) / splits;
-  const int sp = blockIdx.x / n_tiles;
-  const int tile = blockIdx.x - sp * n_tiles;
+  const int nt = int(d / kBlock);
+  const int n_tiles = nt * (nt + 1) / 2;
+  const int64_t units = int64_t(n_tiles) * splits;
+  const int x = blockIdx.x & 7, l = blockIdx.x >> 3;
+  const int64_t u0 = units * x / 8, u1 = units * (x + 1) / 8;
+  if (u0 + l >= u1) return;
+  const int64_t u = u0 + l;
+  const int sp = int(u / n_tiles);
   int ti, tj;
-  tri_tile(tile, &ti, &tj);
+  grouped_tri_tile(int(u - int64_t(sp) * n_tiles), nt, &ti, &tj);
   const int s0 = int(int64_t(stages) * sp / splits);
   const int s1 = int(int64_t(stages) * (sp + 1) / splits);
   const int n = s1 - s0;
@@ -410,6 +449,10 @@ struct DirectPlan {
   size_t part_elems;
 };
 
+// Grid of k_syrk_direct for `units` (split, tile) pairs: 8 times the
+// longest per-XCD range.
+unsigned direct_grid(int64_t units) { return unsigned(8 * ceil_div(units, int64_t(8))); }
+
 bool direct_ok(int64_t d, int dtype) {
   return dtype == OPTIMA_DTYPE_BF16 && d % dt::kBlock == 0;
 }
@@ -470,7 +513,7 @@ optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_
     const uint16_t* Xb = static_cast<const uint16_t*>(X);
     int splits = p.splits;
     if (p.full_stages > 0) {
-      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(unsigned(p.tiles * splits)),
+      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(direct_grid(p.tiles * splits)),
                          dim3(64 * kDirectWaves), 0, s, Xb, d, p.full_stages, splits, part, 1);
       OPTIMA_LAUNCH_CHECK();
     } else {
@@ -480,7 +523,7 @@ optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_
       hipLaunchKernelGGL(k_tail_rows, dim3(256), dim3(kThreads), 0, s, Xb, d,
                          int64_t(p.full_stages) * dt::kRows, p.tail_rows, tail);
       OPTIMA_LAUNCH_CHECK();
-      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(unsigned(p.tiles)),
+      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(direct_grid(p.tiles)),
                          dim3(64 * kDirectWaves), 0, s, tail, d, 1, 1, part,
                          p.full_stages > 0 ? 0 : 1);
       OPTIMA_LAUNCH_CHECK();
