@@ -32,7 +32,9 @@
 namespace optima {
 namespace {
 
-enum GemmMode { kPlain = 0, kPlain2 = 1, kStore = 2, kFused = 3 };
+// kPlainAdd: out1 = H x + out2 (the setup product H w0 = H x0 + H p of a
+// sparse solve, p = w0 - x0 the pruned part).
+enum GemmMode { kPlain = 0, kPlain2 = 1, kStore = 2, kFused = 3, kPlainAdd = 4 };
 // kPrecSparse: bf16x3 with the multiplied vectors stored 2:4-compressed (the
 // iteration products of a solve whose mask keeps at most 2 of every 4).
 enum Prec { kPrecF32 = OPTIMA_PREC_FP32, kPrecBf16x3 = OPTIMA_PREC_BF16X3, kPrecSparse = 2 };
@@ -44,8 +46,8 @@ struct ProductArgs {
   int n_rows;
   int dp;
   int d;
-  float* out1;         // kPlain/kPlain2: destination; kStore: Hx
-  float* out2;         // kPlain2: second destination
+  float* out1;         // kPlain/kPlain2/kPlainAdd: destination; kStore: Hx
+  float* out2;         // kPlain2: second destination; kPlainAdd: the addend
   float* HA;           // Hx_ag (kStore, kFused)
   const float* HW0;    // kFused
   const float* Xin;    // kFused: x of the current iteration (same as A)
@@ -231,6 +233,9 @@ __device__ inline void epilogue4(const ProductArgs& p, int j, int n, float4 y4, 
   } else if (MODE == kPlain2) {
     st4(p.out1 + o, y4);
     st4(p.out2 + o, y4);
+  } else if (MODE == kPlainAdd) {
+    const float4 a = ld4(p.out2 + o);
+    st4(p.out1 + o, make_float4(a.x + y4.x, a.y + y4.y, a.z + y4.z, a.w + y4.w));
   } else if (MODE == kStore) {
     float4 ha = ld4(p.HA + o);
     ha.x = (1.f - c.alpha) * ha.x + c.alpha * y4.x;
@@ -762,27 +767,65 @@ __global__ void __launch_bounds__(kThreads) k_split_h(const float* Hm, int dp, u
 // block and lane group (dp / 16 words per row; word w covers columns
 // 16 w .. 16 w + 15 of the row), the slot codes of those 4 groups (dp / 4
 // bytes per row), and flags[1] = 1 if some group of 4 keeps more than 2
-// (the mask then has no compressed form).
+// (the mask then has no compressed form). idx2 gets the index words of the
+// pruned columns below d, and flags[2] = 1 if some group prunes more than 2
+// of them (the pruned part of w0 then has no compressed form).
 __global__ void __launch_bounds__(kThreads) k_sparse_index(const uint8_t* mask, int n_cols, int d,
                                                            int dp, uint16_t* idx, uint8_t* slot,
-                                                           int* flags) {
+                                                           uint16_t* idx2, int* flags) {
   const int words = dp / 16;
   const int64_t t = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   if (t >= int64_t(n_cols) * words) return;
   const int j = int(t / words), w = int(t % words);
-  uint32_t word = 0, codes = 0;
-  bool bad = false;
+  uint32_t word = 0, codes = 0, word2 = 0;
+  bool bad = false, bad2 = false;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    bool keep[4];
-    mask4(mask, d, j, 16 * w + 4 * q, keep);
+    const int n = 16 * w + 4 * q;
+    bool keep[4], pruned[4];
+    mask4(mask, d, j, n, keep);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pruned[e] = !keep[e] && n + e < d;
     bad |= int(keep[0]) + int(keep[1]) + int(keep[2]) + int(keep[3]) > 2;
+    bad2 |= int(pruned[0]) + int(pruned[1]) + int(pruned[2]) + int(pruned[3]) > 2;
     word |= sparse_pair_code(keep) << (4 * q);
     codes |= slot_code_bits(keep) << (8 * q);
+    word2 |= sparse_pair_code(pruned) << (4 * q);
   }
   idx[size_t(j) * words + w] = uint16_t(word);
+  idx2[size_t(j) * words + w] = uint16_t(word2);
   *reinterpret_cast<uint32_t*>(slot + size_t(j) * (dp / 4) + 4 * w) = codes;
   if (bad) atomicOr(flags + 1, 1);
+  if (bad2) atomicOr(flags + 2, 1);
+}
+
+// Compressed planes of the two setup operands of a sparse solve, one thread
+// per group of 4: x0 = sel(mask, w0, 0) at the kept pair (into XP0) and the
+// pruned part p = w0 - x0 at the pruned pair (into XP1). W is the padded
+// copy of w0 (pitch dp).
+__global__ void __launch_bounds__(kThreads) k_setup_planes(const float* W, const uint8_t* mask,
+                                                           int n_cols, int d, int dp,
+                                                           uint16_t* XP0, uint16_t* XP1) {
+  const int groups = dp / 4;
+  const int64_t t = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (t >= int64_t(n_cols) * groups) return;
+  const int j = int(t / groups), g = int(t % groups);
+  const float4 w4 = ld4(W + size_t(j) * dp + 4 * g);
+  const float w[4] = {w4.x, w4.y, w4.z, w4.w};
+  bool keep[4], pruned[4];
+  mask4(mask, d, j, 4 * g, keep);
+  float x0[4], pv[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    pruned[e] = !keep[e] && 4 * g + e < d;
+    x0[e] = keep[e] ? w[e] : 0.f;
+    pv[e] = pruned[e] ? w[e] : 0.f;
+  }
+  const uint32_t c0 = sparse_pair_code(keep), c1 = sparse_pair_code(pruned);
+  const float2 a = pick_pair(x0, SlotCode{int(c0 & 3u), int(c0 >> 2), true, true});
+  const float2 b = pick_pair(pv, SlotCode{int(c1 & 3u), int(c1 >> 2), true, true});
+  store_pair_planes(XP0 + size_t(j) * dp, g, a.x, a.y);
+  store_pair_planes(XP1 + size_t(j) * dp, g, b.x, b.y);
 }
 
 // Zero-padded copy of H (used when d is not a multiple of the tile) with a
@@ -1235,6 +1278,7 @@ struct Layout {
   float *X0, *X1, *XA, *HX, *HA, *HW0, *Hp, *L;
   uint16_t *XP0, *XP1, *HP;  // split planes for kPrecBf16x3
   uint16_t* XIDX;            // index words of the 2:4-compressed x planes
+  uint16_t* XIDX2;           // index words of the pruned part of w0
   uint8_t* SLOT;             // slot codes of the packed vectors, dp / 4 per column
   int *rows0, *rows1, *n_active, *flags;
   ColState st;
@@ -1260,6 +1304,7 @@ Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
   l.XP1 = c.take<uint16_t>(2 * vec);
   l.HP = c.take<uint16_t>(2 * size_t(l.dp) * size_t(l.dp));
   l.XIDX = c.take<uint16_t>(size_t(n_cols) * size_t(l.dp / 16));
+  l.XIDX2 = c.take<uint16_t>(size_t(n_cols) * size_t(l.dp / 16));
   l.SLOT = c.take<uint8_t>(size_t(n_cols) * size_t(l.dp / 4));
   l.rows0 = c.take<int>(n_cols);
   l.rows1 = c.take<int>(n_cols);
@@ -1522,11 +1567,11 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   if (try_sparse) {
     const int64_t words = int64_t(nc) * (dp / 16);
     hipLaunchKernelGGL(k_sparse_index, dim3(unsigned(ceil_div(words, kThreads))), dim3(kThreads),
-                       0, s, mask, nc, di, dp, l.XIDX, l.SLOT, l.flags);
+                       0, s, mask, nc, di, dp, l.XIDX, l.SLOT, l.XIDX2, l.flags);
     OPTIMA_LAUNCH_CHECK();
   }
-  int flags[2] = {0, 0};
-  OPTIMA_HIP_TRY(hipMemcpyAsync(flags, l.flags, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
+  int flags[3] = {0, 0, 0};
+  OPTIMA_HIP_TRY(hipMemcpyAsync(flags, l.flags, 3 * sizeof(int), hipMemcpyDeviceToHost, s));
   OPTIMA_HIP_TRY(hipStreamSynchronize(s));
   if (flags[0]) return OPTIMA_E_NONFINITE;
   const bool sparse = try_sparse && !flags[1];
@@ -1545,18 +1590,41 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   p.Bp = l.HP;
   p.Aidx = l.XIDX;
   p.slot = l.SLOT;
-  // The setup products use the solve's precision too: H w0 and H x0 then
-  // agree bit for bit wherever w0 and x0 do (all-kept columns start at
-  // their optimum with a zero gradient).
-  p.A = l.HX;
-  p.Ap = l.XP1;
-  p.out1 = l.HW0;
-  if (auto e = launch_product<kPlain>(p, l, o.precision, s)) return e;
-  p.A = l.X0;
-  p.Ap = l.XP0;
-  p.out1 = l.HX;
-  p.out2 = l.HA;
-  if (auto e = launch_product<kPlain2>(p, l, o.precision, s)) return e;
+  if (sparse && !flags[2]) {
+    // Both setup operands are 2:4-compressible: H x0 on the kept pairs and
+    // H w0 = H x0 + H p with p = w0 - x0 on the pruned pairs, both on the
+    // sparse MFMA. Where w0 is zero off the mask, H p is exactly zero and
+    // H w0 equals H x0 bit for bit.
+    const int64_t groups = int64_t(nc) * (dp / 4);
+    hipLaunchKernelGGL(k_setup_planes, dim3(unsigned(ceil_div(groups, kThreads))), dim3(kThreads),
+                       0, s, l.HX, mask, nc, di, dp, l.XP0, l.XP1);
+    OPTIMA_LAUNCH_CHECK();
+    p.A = l.X0;
+    p.Ap = l.XP0;
+    p.Aidx = l.XIDX;
+    p.out1 = l.HX;
+    p.out2 = l.HA;
+    if (auto e = launch_product<kPlain2>(p, l, kPrecSparse, s)) return e;
+    p.Ap = l.XP1;
+    p.Aidx = l.XIDX2;
+    p.out1 = l.HW0;
+    p.out2 = l.HX;
+    if (auto e = launch_product<kPlainAdd>(p, l, kPrecSparse, s)) return e;
+    p.Aidx = l.XIDX;
+  } else {
+    // The setup products use the solve's precision too: H w0 and H x0 then
+    // agree bit for bit wherever w0 and x0 do (all-kept columns start at
+    // their optimum with a zero gradient).
+    p.A = l.HX;
+    p.Ap = l.XP1;
+    p.out1 = l.HW0;
+    if (auto e = launch_product<kPlain>(p, l, o.precision, s)) return e;
+    p.A = l.X0;
+    p.Ap = l.XP0;
+    p.out1 = l.HX;
+    p.out2 = l.HA;
+    if (auto e = launch_product<kPlain2>(p, l, o.precision, s)) return e;
+  }
   inf.gemm_calls += 2;
   inf.row_products += 2 * int64_t(nc);
 
