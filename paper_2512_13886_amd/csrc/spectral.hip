@@ -195,11 +195,15 @@ __global__ void k_copy_iters(const PowState* st, int32_t* iters) { *iters = st->
 // ---------------------------------------------------------------------------
 
 constexpr int kMaxBlock = 16;
-constexpr int kSubRows = 32;                 // rows of H per workgroup
-constexpr int kSubThreads = 512;             // 8 waves: 2 row blocks x 4 slices of K
+constexpr int kSubRows = 16;                 // rows of H per workgroup
+constexpr int kSubThreads = 512;             // 8 waves: 8 slices of K
 constexpr int kGram = kMaxBlock * kMaxBlock;
 constexpr int kPart = 3 * kGram;             // G, T, S partials per workgroup
 constexpr int kSquarings = 32;
+// The squarings stop once no entry of the trace-normalised M moves by more
+// than this: M is then the projector onto the top eigenvector, or the next
+// eigenvalue is within this relative distance of the top one.
+constexpr double kSquareTol = 1e-14;
 constexpr double kDropRel = 1e-14;
 constexpr int kPitch = kMaxBlock + 1;
 
@@ -229,44 +233,49 @@ __device__ void chol_drop(double (*A)[kPitch], double (*L)[kPitch], double* diag
 }
 
 // X = L^-1 for a lower-triangular L whose zero diagonal entries mark dropped
-// directions (their rows and columns of X are 0). Thread c < b owns column c.
+// directions (their rows and columns of X are 0). Thread c < 16 forms
+// column c by forward substitution with the column in registers.
 __device__ void inv_lower(double (*L)[kPitch], double (*X)[kPitch], int b) {
-  const int t = threadIdx.x;
-  X[t >> 4][t & 15] = 0.0;
-  __syncthreads();
-  if (t < b) {
-    const int c = t;
-    for (int i = c; i < b; ++i) {
-      if (L[i][i] == 0.0) continue;
+  const int c = threadIdx.x;
+  if (c < kMaxBlock) {
+    double xc[kMaxBlock];
+#pragma unroll
+    for (int i = 0; i < kMaxBlock; ++i) {
       double s = i == c ? 1.0 : 0.0;
-      for (int k = c; k < i; ++k) s -= L[i][k] * X[k][c];
-      X[i][c] = s / L[i][i];
+#pragma unroll
+      for (int k = 0; k < i; ++k) s -= k >= c ? L[i][k] * xc[k] : 0.0;
+      const double piv = L[i][i];
+      xc[i] = (i >= c && i < b && c < b && piv != 0.0) ? s / piv : 0.0;
     }
+#pragma unroll
+    for (int i = 0; i < kMaxBlock; ++i) X[i][c] = xc[i];
   }
   __syncthreads();
 }
 
 // Pass i >= 1 (see the file comment); workgroup blk covers rows
-// [32 blk, 32 blk + 32) of the padded row range [0, dpp).
+// [16 blk, 16 blk + 16) of the padded row range [0, dpp).
 template <bool VEC4>
 __global__ void __launch_bounds__(kSubThreads) k_subspace_pass(const float* H, int64_t d,
                                                                int64_t dpp, const float* Yprev,
                                                                float* Ycur, const double* Rinv,
                                                                double* part, SubState* st) {
   if (st->conv) return;
-  __shared__ float red[kSubThreads / 64][256];
+  constexpr int kSlices = kSubThreads / 64;
+  __shared__ float red[kSlices][256];
   __shared__ double Rs[kGram];
   __shared__ double Zs[kSubRows][kPitch], Ys[kSubRows][kPitch], Qs[kSubRows][kPitch];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int rb = w & 1, ks = w >> 1;
+  const int ks = w;
   const int64_t r0 = int64_t(blockIdx.x) * kSubRows;
   for (int i = tid; i < kGram; i += kSubThreads) Rs[i] = Rinv[i];
 
   // Z = H Y_{i-1}^T for this workgroup's rows. MFMA lane l supplies row
   // (l % 16) of H and vector (l % 16) of Y at contraction indices
   // 16 c + 4 (l / 16) + {0..3}: four MFMAs per 16-wide chunk c of K, each
-  // fed by one 16-byte load per operand.
-  const int64_t row = r0 + rb * 16 + (lane & 15);
+  // fed by one 16-byte load per operand. Wave w takes the chunks c = w
+  // (mod 8).
+  const int64_t row = r0 + (lane & 15);
   const bool row_ok = row < d;
   const float* hrow = H + (row_ok ? row : 0) * d;
   const float* yrow = Yprev + int64_t(lane & 15) * dpp + 4 * (lane >> 4);
@@ -293,42 +302,41 @@ __global__ void __launch_bounds__(kSubThreads) k_subspace_pass(const float* H, i
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, y.w, acc, 0, 0, 0);
   };
   int64_t c = ks;
-  for (; c + 28 < nch; c += 32) {  // eight 16-byte loads per operand in flight
+  for (; c + 7 * kSlices < nch; c += 8 * kSlices) {  // eight 16-byte loads per operand in flight
     float4 a[8], y[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      a[u] = load_a(c + 4 * u);
-      y[u] = *reinterpret_cast<const float4*>(yrow + (c + 4 * u) * 16);
+      a[u] = load_a(c + kSlices * u);
+      y[u] = *reinterpret_cast<const float4*>(yrow + (c + kSlices * u) * 16);
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) mfma4(a[u], y[u]);
   }
-  for (; c + 12 < nch; c += 16) {
-    const float4 a0 = load_a(c), a1 = load_a(c + 4), a2 = load_a(c + 8), a3 = load_a(c + 12);
-    const float4 y0 = *reinterpret_cast<const float4*>(yrow + c * 16);
-    const float4 y1 = *reinterpret_cast<const float4*>(yrow + (c + 4) * 16);
-    const float4 y2 = *reinterpret_cast<const float4*>(yrow + (c + 8) * 16);
-    const float4 y3 = *reinterpret_cast<const float4*>(yrow + (c + 12) * 16);
-    mfma4(a0, y0);
-    mfma4(a1, y1);
-    mfma4(a2, y2);
-    mfma4(a3, y3);
+  for (; c + 3 * kSlices < nch; c += 4 * kSlices) {
+    float4 a[4], y[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      a[u] = load_a(c + kSlices * u);
+      y[u] = *reinterpret_cast<const float4*>(yrow + (c + kSlices * u) * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) mfma4(a[u], y[u]);
   }
-  for (; c < nch; c += 4) mfma4(load_a(c), *reinterpret_cast<const float4*>(yrow + c * 16));
+  for (; c < nch; c += kSlices) mfma4(load_a(c), *reinterpret_cast<const float4*>(yrow + c * 16));
 #pragma unroll
   for (int e = 0; e < 4; ++e) red[w][e * 64 + lane] = acc[e];
   __syncthreads();
-  // Sum the four K slices in a fixed order. MFMA output (lane, e) is row
+  // Sum the K slices in a fixed order. MFMA output (lane, e) is row
   // 4 (lane / 16) + e, vector lane % 16 of the 16 x 16 tile.
-  {
-    const int b2 = tid >> 8, within = tid & 255, ln = within & 63, e = within >> 6;
+  if (tid < 256) {
+    const int ln = tid & 63, e = tid >> 6;
     double z = 0.0;
-    for (int q = 0; q < 4; ++q) z += double(red[b2 + 2 * q][e * 64 + ln]);
-    Zs[b2 * 16 + 4 * (ln >> 4) + e][ln & 15] = z;
+    for (int q = 0; q < kSlices; ++q) z += double(red[q][e * 64 + ln]);
+    Zs[4 * (ln >> 4) + e][ln & 15] = z;
   }
   __syncthreads();
   // Y_i = Z R^-1 (stored in fp32), Q_i = Y_{i-1} R^-1 for these rows.
-  {
+  if (tid < kSubRows * kMaxBlock) {
     const int r = tid >> 4, a = tid & 15;
     double yn = 0.0, q = 0.0;
     for (int k = 0; k < kMaxBlock; ++k) {
@@ -364,9 +372,11 @@ __global__ void __launch_bounds__(kSubThreads) k_subspace_init(const float* V0, 
   __shared__ double Ys[kSubRows][kPitch];
   const int tid = threadIdx.x, r = tid >> 4, a = tid & 15;
   const int64_t row = int64_t(blockIdx.x) * kSubRows + r;
-  const float v = (a < b && row < d) ? V0[int64_t(a) * d + row] : 0.f;
-  Y0[int64_t(a) * dpp + row] = v;
-  Ys[r][a] = double(v);
+  if (r < kSubRows) {
+    const float v = (a < b && row < d) ? V0[int64_t(a) * d + row] : 0.f;
+    Y0[int64_t(a) * dpp + row] = v;
+    Ys[r][a] = double(v);
+  }
   if (blockIdx.x == 0 && tid == 0) {
     st->theta = 0.0;
     st->conv = 0;
@@ -467,8 +477,10 @@ __global__ void __launch_bounds__(256) k_subspace_finish(const double* tot, int 
         __syncthreads();
         double tr2 = 0.0;
         for (int k = 0; k < kMaxBlock; ++k) tr2 += W[k][k];
-        M[i][j] = m2 / tr2;
-        __syncthreads();
+        const double mn = m2 / tr2;
+        const bool moved = !(fabs(mn - M[i][j]) <= kSquareTol);
+        M[i][j] = mn;
+        if (!__syncthreads_or(moved)) break;
       }
       if (t < kMaxBlock) {
         double rs = 0.0;
