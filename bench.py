@@ -49,8 +49,8 @@ SPECTRAL_BLOCK = 16
 
 # HBM traffic of the product kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (profiles/), valid only for the kernel sources they were taken on.
-TRAFFIC = {"sources_sha1": "274e418ed3e858ded062f8b41b54ae1300716853",
-           "bytes_per_launch": 171985 * 1024}
+TRAFFIC = {"sources_sha1": "a3a96c141a277c728d1179606c6ee21e89d3c330",
+           "bytes_per_launch": 171981 * 1024}
 
 
 def log(msg: str):
