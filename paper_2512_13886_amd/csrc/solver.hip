@@ -757,10 +757,18 @@ __global__ void __launch_bounds__(kThreads) k_prep(const float* W0, const uint8_
 }
 
 // Split planes of H (row pitch 4 dp bytes), built once per solve.
-__global__ void __launch_bounds__(kThreads) k_split_h(const float* Hm, int dp, uint16_t* HP) {
+// With `flags`, it also sets flags[0] = 1 if H holds a NaN or Inf (the scan
+// of k_scan_pad_h, for an H that needs no padding).
+__global__ void __launch_bounds__(kThreads) k_split_h(const float* Hm, int dp, uint16_t* HP,
+                                                      int* flags) {
   const int i = blockIdx.x;
-  for (int n = blockIdx.y * kThreads + threadIdx.x; n < dp; n += gridDim.y * kThreads)
-    store_split(HP + size_t(i) * dp * 2, n, Hm[size_t(i) * dp + n]);
+  bool bad = false;
+  for (int n = blockIdx.y * kThreads + threadIdx.x; n < dp; n += gridDim.y * kThreads) {
+    const float v = Hm[size_t(i) * dp + n];
+    bad |= !isfinite(v);
+    store_split(HP + size_t(i) * dp * 2, n, v);
+  }
+  if (flags && bad) atomicOr(flags, 1);
 }
 
 // Index words of the 2:4-compressed layout, one thread per row, 64-column
@@ -1536,7 +1544,11 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   OPTIMA_HIP_TRY(hipMemsetAsync(l.flags, 0, 4 * sizeof(int), s));
   OPTIMA_HIP_TRY(hipMemsetAsync(l.st.done, 0, size_t(nc) * sizeof(int), s));
   const float* Hm = H;
-  {
+  const bool split = o.precision == kPrecBf16x3;
+  // The finiteness scan of H: a pass of its own when H needs padding or no
+  // split planes are built, else part of the split (k_split_h).
+  const bool scan_in_split = split && !l.pad_h;
+  if (!scan_in_split) {
     const int blocks = int(std::min<int64_t>(4096, ceil_div(int64_t(dp) * dp, kThreads)));
     hipLaunchKernelGGL(k_scan_pad_h, dim3(blocks), dim3(kThreads), 0, s, H, di, dp, l.Hp, l.flags);
     OPTIMA_LAUNCH_CHECK();
@@ -1550,7 +1562,6 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   }
   const dim3 vec_grid(unsigned(nc), unsigned(ceil_div(dp, 4 * kThreads)));
   // W0 padded copy goes to HX first; Hw0 = H w0, then Hx = Hx_ag = H x0.
-  const bool split = o.precision == kPrecBf16x3;
   // Split planes: x0 into XP0, W0 into XP1 (free until the first update).
   hipLaunchKernelGGL(k_prep, vec_grid, dim3(kThreads), 0, s, W0, mask, nc, di, dp, l.HX, l.X0,
                      l.XA, split ? l.XP0 : nullptr, split ? l.XP1 : nullptr, o.col_scale,
@@ -1558,7 +1569,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   OPTIMA_LAUNCH_CHECK();
   if (split) {
     hipLaunchKernelGGL(k_split_h, dim3(unsigned(dp), unsigned(ceil_div(dp, 4 * kThreads))),
-                       dim3(kThreads), 0, s, Hm, dp, l.HP);
+                       dim3(kThreads), 0, s, Hm, dp, l.HP, scan_in_split ? l.flags : nullptr);
     OPTIMA_LAUNCH_CHECK();
   }
   // The rAPDHG iteration products skip the pruned entries on the 2:4 sparse

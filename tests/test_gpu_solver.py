@@ -264,11 +264,26 @@ def test_error_paths(L):
     Hd, lmd = to_dev(H), to_dev(np.array([lam]))
     W0d, Md = to_dev(W0), to_dev(M, torch.uint8)
     out = torch.empty_like(W0d)
-    Hn = Hd.clone()
-    Hn[2, 5] = float("inf")
-    with pytest.raises(L.OptimaError) as e:
-        L.optima_qp_solve_batched(Hn, lmd, W0d, Md, out)
-    assert e.value.status == -3
+    # A non-finite H: scanned while the split planes are built (bf16x3) or
+    # in a pass of its own (fp32).
+    for prec in (L.PREC_FP32, L.PREC_BF16X3):
+        for (i, j, v) in ((2, 5, float("inf")), (cfg.d - 1, cfg.d - 1, float("nan"))):
+            Hn = Hd.clone()
+            Hn[i, j] = v
+            with pytest.raises(L.OptimaError) as e:
+                L.optima_qp_solve_batched(Hn, lmd, W0d, Md, out, opts=_opts(L, precision=prec))
+            assert e.value.status == -3
+        # a width that needs padding: the scan runs with the padded copy
+        rng = np.random.default_rng(5)
+        A = rng.standard_normal((300, 100))
+        Hr = to_dev(f32_exact(A.T @ A + np.eye(100)))
+        Hr[99, 0] = float("nan")
+        Wr = to_dev((rng.standard_normal((3, 100)) * 0.02).astype(np.float32))
+        Mr = to_dev(np.ones((3, 100), dtype=np.uint8), torch.uint8)
+        with pytest.raises(L.OptimaError) as e:
+            L.optima_qp_solve_batched(Hr, lmd, Wr, Mr, torch.empty_like(Wr),
+                                      opts=_opts(L, precision=prec))
+        assert e.value.status == -3
     with pytest.raises(L.OptimaError) as e:
         L.optima_qp_solve_batched(Hd, torch.zeros_like(lmd), W0d, Md, out)
     assert e.value.status == -3
@@ -287,9 +302,9 @@ def test_error_paths(L):
 @pytest.mark.parametrize("prec", PRECISIONS)
 @pytest.mark.parametrize("n", [1, 5, 8, 9])
 def test_few_columns_match_closed_form(L, prec, n):
-    # At most 8 active columns take the HBM-streaming product (H read once
-    # per iteration, the same bf16x3 or fp32 products on the vector units);
-    # 9 take the MFMA tiles. Both reach the closed form; the columns of the
+    # At most 8 active columns take the HBM-streaming bf16x3 product (H's
+    # planes read once per iteration; fp32 solves keep the MFMA tiles);
+    # 9 take the tiles. Both reach the closed form; the columns of the
     # small batch agree with the same columns solved in a full batch.
     cfg = workloads.TINY
     H, W0, M, lam = _oracle_layer(cfg)
