@@ -49,8 +49,9 @@ SPECTRAL_BLOCK = 16
 
 # HBM traffic of the product kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (profiles/), valid only for the kernel sources they were taken on.
-TRAFFIC = {"sources_sha1": "a3a96c141a277c728d1179606c6ee21e89d3c330",
-           "bytes_per_launch": 171981 * 1024}
+TRAFFIC = {"sources_sha1": "0434addf604f26fe3856a4f49934432e18706ab3",
+           "bytes_per_launch": 276887 * 1024,       # k_product_sparse<fused|store>
+           "few_bytes_per_launch": 67074 * 1024}    # k_product_skinny_sparse<fused|store>
 
 
 def log(msg: str):
@@ -320,19 +321,32 @@ def main() -> int:
     solve_ms = np.mean([e[2].elapsed_time(e[3]) for e, _ in recs])
     it = np.mean([i["iterations"] for _, i in recs])
     col_it = np.mean([i["row_products"] for _, i in recs])
-    launches = sum(i["timed_launches"] for _, i in recs)
-    rows = sum(i["timed_row_products"] for _, i in recs)
-    prod_ms = sum(i["timed_product_ms"] for _, i in recs)
+    all_launches = sum(i["timed_launches"] for _, i in recs)
+    all_rows = sum(i["timed_row_products"] for _, i in recs)
+    all_ms = sum(i["timed_product_ms"] for _, i in recs)
     sparse_products = all(i["sparse_products"] == 1 for _, i in recs)
+    # The dominant kernel is the tiled product; the launches over at most 8
+    # active columns run another kernel (H streamed once per launch), timed
+    # and reported on their own.
+    few_launches = sum(i["few_launches"] for _, i in recs)
+    few_rows = sum(i["few_row_products"] for _, i in recs)
+    few_ms = sum(i["few_product_ms"] for _, i in recs)
+    launches = all_launches - few_launches
+    rows = all_rows - few_rows
+    prod_ms = all_ms - few_ms
     flops = 2.0 * d * d * rows
     achieved = flops / (prod_ms * 1e-3) / 1e12
     avg_launch_us = prod_ms * 1e3 / launches
+    all_tflops = 2.0 * d * d * all_rows / (all_ms * 1e-3) / 1e12
     per_col_it = iters.cpu().numpy()
     f_ratio_rapdhg = float(f_fin.double().sum() / f_init.double().sum())
     log(f"step {ms_step:.1f} ms: hessian {hess_ms:.2f} ms, damp+spectral {spec_ms:.2f} ms, "
         f"solve {solve_ms:.1f} ms ({it:.0f} iterations, {conv.sum().item()}/{C} converged, "
         f"per-column iterations {per_col_it.min()}..{per_col_it.max()})")
-    log(f"H-product: {launches} launches, avg {avg_launch_us:.1f} us, {achieved:.1f} TFLOP/s")
+    log(f"H-product (tiles): {launches} launches, avg {avg_launch_us:.1f} us, {achieved:.1f} TFLOP/s;"
+        f" few-column: {few_launches} launches, avg "
+        f"{(few_ms * 1e3 / few_launches) if few_launches else 0.0:.1f} us;"
+        f" all: {all_launches} launches, {all_tflops:.1f} TFLOP/s")
 
     # Unconstrained-form leg (Eq. (7)-(11)): conjugate gradients on the same
     # layer and H at the same tolerances, tested every 8 iterations; no step
@@ -529,6 +543,27 @@ def main() -> int:
         }
     roofline.update({"avg_launch_us": avg_launch_us, "launches": launches,
                      "flops_per_launch": flops / launches})
+    if few_launches:
+        # H's split planes (4 d^2 bytes) dominate these launches; per active
+        # column they add the compressed x planes (2 d bytes) and the packed
+        # update (16.25 d bytes), or x in fp32 (4 d) and the update (33 d).
+        per_col = (2.0 + 16.25) * d if sparse_products else (4.0 + 33.0) * d
+        few_bytes = 4.0 * d * d * few_launches + per_col * few_rows
+        few_gbs = few_bytes / (few_ms * 1e-3) / 1e9
+        few_traffic = None
+        if traffic is not None:
+            few_traffic = TRAFFIC.get("few_bytes_per_launch")
+        roofline["few_column_kernel"] = {
+            "kernel": ("k_product_skinny_sparse" if sparse_products else "k_product_skinny") +
+                      "<fused>: the same product when at most 8 columns are active, H's planes "
+                      "streamed once per launch",
+            "bound": "hbm", "achieved": few_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": few_gbs / HBM_PEAK_GBS, "traffic": few_traffic,
+            "avg_launch_us": few_ms * 1e3 / few_launches, "launches": few_launches,
+            "bytes_per_launch": few_bytes / few_launches}
+    roofline["all_iteration_products"] = {
+        "launches": all_launches, "avg_launch_us": all_ms * 1e3 / all_launches,
+        "achieved": all_tflops, "unit": "TFLOP/s"}
 
     out = {
         "metric": METRIC,

@@ -318,6 +318,10 @@ typedef struct {
   double timed_product_ms;    /* their device time, from HIP events recorded on `stream`
                                  around each run of back-to-back product launches */
   int64_t sparse_products;    /* 1 if the iteration products ran 2:4-sparse (opts.sparse) */
+  int64_t few_launches;       /* the timed launches that ran the few-column kernel (at most 8
+                                 active columns with split planes: H streamed once per launch) */
+  int64_t few_row_products;   /* columns multiplied by those launches */
+  double few_product_ms;      /* their device time (included in timed_product_ms) */
 } optima_solve_info;
 
 void optima_solver_opts_default(optima_solver_opts* opts);

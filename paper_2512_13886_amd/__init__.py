@@ -3,7 +3,7 @@
 The compute lives in liboptima.so (hand-written HIP kernels behind a C ABI,
 declared in include/optima.h). This package is its thin Python binding; the
 names match the C entry points. Importing it fails loudly if the library has
-not been built (python -m paper_2512_13886_amd.build).
+not been built (python paper_2512_13886_amd/build.py) or is stale.
 """
 from ._lib import (OptimaError, SolverOpts, DTYPE_F32, DTYPE_BF16, DTYPE_F64, PREC_FP32,
                    PREC_BF16X3, SPECTRAL_MAX_BLOCK, MASK_UNSTRUCTURED, MASK_2TO4, METHOD_RAPDHG,

@@ -38,7 +38,7 @@ class OptimaError(RuntimeError):
 
 if not os.path.exists(_LIB_PATH):
     raise ImportError(
-        f"{_LIB_PATH} is missing: build it with `python -m paper_2512_13886_amd.build`")
+        f"{_LIB_PATH} is missing: build it with `python paper_2512_13886_amd/build.py`")
 _lib = ctypes.CDLL(_LIB_PATH)
 
 _i64, _i32, _sz, _vp, _f32 = ctypes.c_int64, ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_float
@@ -63,7 +63,9 @@ class _Info(ctypes.Structure):
     _fields_ = [("iterations", ctypes.c_int64), ("gemm_calls", ctypes.c_int64),
                 ("row_products", ctypes.c_int64), ("checks", ctypes.c_int64),
                 ("timed_launches", ctypes.c_int64), ("timed_row_products", ctypes.c_int64),
-                ("timed_product_ms", ctypes.c_double), ("sparse_products", ctypes.c_int64)]
+                ("timed_product_ms", ctypes.c_double), ("sparse_products", ctypes.c_int64),
+                ("few_launches", ctypes.c_int64), ("few_row_products", ctypes.c_int64),
+                ("few_product_ms", ctypes.c_double)]
 
 
 def _sig(name, res, args):
@@ -75,6 +77,11 @@ def _sig(name, res, args):
 
 _status_string = _sig("optima_status_string", ctypes.c_char_p, [_i32])
 _abi_version = _sig("optima_abi_version", _i32, [])
+# The structs above mirror include/optima.h at this ABI version.
+ABI_VERSION = 9
+if _abi_version() != ABI_VERSION:
+    raise ImportError(f"{_LIB_PATH} has ABI version {_abi_version()}, the binding expects "
+                      f"{ABI_VERSION}: rebuild the library")
 _hess_ws = _sig("optima_hessian_workspace_bytes", _sz, [_i64, _i64, _i32])
 _hess_acc = _sig("optima_hessian_accumulate", _i32,
                  [_vp, _i32, _i64, _i64, _vp, _i32, _vp, _sz, _vp])

@@ -1,6 +1,7 @@
 """Builds liboptima.so (the gfx950 HIP library) in the package directory.
 
-Usage: python -m paper_2512_13886_amd.build   (or build() from Python).
+Usage: python paper_2512_13886_amd/build.py   (or build() from Python). It runs as a
+plain script: importing the package would load the library it builds.
 Every HIP source under csrc/ is compiled with hipcc for gfx950 only and linked
 into one shared library next to this file.
 """

@@ -1394,10 +1394,18 @@ int choose_splits_one_per_cu(int tiles, int stages, int rows_pad, int dp, size_t
   return best;
 }
 
+// Whether the iteration products (kFused / kStore) of n_rows active columns
+// run the few-column kernels.
+bool few_column_path(int prec, int n_rows, int dp) {
+  if (n_rows > kSkinnyRows) return false;
+  if (prec == kPrecSparse) return true;
+  return prec == kPrecBf16x3 && dp % (32 * kSkinnyWaves) == 0;
+}
+
 template <int MODE, int PREC>
 optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t s) {
   if constexpr ((MODE == kFused || MODE == kStore) && PREC == kPrecSparse) {
-    if (p.n_rows <= kSkinnyRows) {
+    if (few_column_path(PREC, p.n_rows, p.dp)) {
       hipLaunchKernelGGL((k_product_skinny_sparse<MODE>), dim3(unsigned(p.dp / kSkinnyHRows)),
                          dim3(64 * kSkinnyWaves), 0, s, p);
       OPTIMA_LAUNCH_CHECK();
@@ -1405,7 +1413,7 @@ optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t 
     }
   }
   if constexpr ((MODE == kFused || MODE == kStore) && PREC == kPrecBf16x3) {
-    if (p.n_rows <= kSkinnyRows && p.dp % (32 * kSkinnyWaves) == 0) {
+    if (few_column_path(PREC, p.n_rows, p.dp)) {
       hipLaunchKernelGGL((k_product_skinny<MODE, PREC>), dim3(unsigned(p.dp / kSkinnyHRows)),
                          dim3(64 * kSkinnyWaves), 0, s, p);
       OPTIMA_LAUNCH_CHECK();
@@ -1763,6 +1771,8 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     inf.row_products += int64_t(n) * n_act;
     inf.timed_launches += n;
     inf.timed_row_products += int64_t(n) * n_act;
+    const bool few = few_column_path(iprec, n_act, dp);  // this block's launches
+    const int act_block = n_act;
     t = t_next;
 
     ca.rows = rows;
@@ -1786,6 +1796,11 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
       float ms = 0.f;
       OPTIMA_HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));
       inf.timed_product_ms += ms;
+      if (few) {
+        inf.few_launches += n;
+        inf.few_row_products += int64_t(n) * act_block;
+        inf.few_product_ms += ms;
+      }
     }
   }
   inf.iterations = t;

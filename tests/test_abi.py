@@ -116,3 +116,38 @@ def test_forward_queries_and_validation(lib):
     assert f(X, 10, 128, W, 8, 0, None, 1, None, Y, None, 0, None) == -1      # err w/o Y_ref
     assert f(vp((1 << 20) + 8), 10, 128, W, 8, 0, Y, 1, None, None, None, 0, None) == -1  # align
     assert f(X, 10, 128, W, 8, 0, Y, 1, None, None, None, 0, None) == -4      # no workspace
+
+
+def _header_struct(name):
+    """(type, field) pairs of `typedef struct { ... } name;` in the header."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    m = re.search(r"typedef struct\s*\{([^}]*)\}\s*" + name + r"\s*;", text)
+    assert m, name
+    fields = []
+    for decl in m.group(1).split(";"):
+        decl = " ".join(decl.split())
+        if decl:
+            t, f = decl.rsplit(" ", 1)
+            if f.startswith("*"):
+                t, f = t + "*", f[1:]
+            fields.append((t, f))
+    return fields
+
+
+@pytest.mark.parametrize("c_name,py_name", [("optima_solver_opts", "_Opts"),
+                                            ("optima_solve_stats", "_Stats"),
+                                            ("optima_solve_info", "_Info")])
+def test_binding_structs_mirror_the_header(c_name, py_name):
+    # The ctypes structs of the binding list the header's fields in order,
+    # with the same C types (the library's ABI version pins this layout).
+    from paper_2512_13886_amd import _lib
+    ctype = {"int64_t": ctypes.c_int64, "int32_t": ctypes.c_int32, "float": ctypes.c_float,
+             "double": ctypes.c_double}
+    header = _header_struct(c_name)
+    mirror = getattr(_lib, py_name)._fields_
+    assert [f for _, f in header] == [f for f, _ in mirror]
+    for (t, f), (_, pt) in zip(header, mirror):
+        if t.endswith("*"):
+            assert pt is ctypes.c_void_p, f
+        else:
+            assert pt is ctype[t], (f, t)
