@@ -756,6 +756,58 @@ __global__ void __launch_bounds__(kThreads) k_prep(const float* W0, const uint8_
   if (bad) atomicOr(flags, 1);
 }
 
+// k_prep for a solve that may run on the sparse products, one thread per
+// group of 4 columns. k_sparse_index has already set flags[1] and flags[2].
+// When both are clear, the setup products run on the sparse kernel and need
+// only x0 and the compressed planes of x0 (kept pairs, into XP) and of the
+// pruned part p = w0 - x0 (pruned pairs, into WP): nothing else is written.
+// Otherwise everything k_prep writes is written.
+__global__ void __launch_bounds__(kThreads) k_prep_sparse(const float* W0, const uint8_t* mask,
+                                                          int d, int dp, float* W0P, float* X,
+                                                          float* XA, uint16_t* XP, uint16_t* WP,
+                                                          const float* scale, int* flags) {
+  const int j = blockIdx.x;
+  const size_t base = size_t(j) * dp;
+  const bool compressed = flags[1] == 0 && flags[2] == 0;  // uniform
+  bool bad = false;
+  for (int g = blockIdx.y * kThreads + threadIdx.x; 4 * g < dp; g += gridDim.y * kThreads) {
+    const int n = 4 * g;
+    bool keep[4], pruned[4];
+    mask4(mask, d, j, n, keep);
+    float w[4], x[4], pv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      w[e] = 0.f;
+      if (n + e < d) {
+        w[e] = W0[size_t(j) * d + n + e];
+        bad |= !isfinite(w[e]);
+        if (scale) {
+          const float sc = scale[n + e];
+          bad |= !(sc > 0.f) || !isfinite(sc);
+          w[e] = w[e] / sc;
+        }
+      }
+      pruned[e] = !keep[e] && n + e < d;
+      x[e] = keep[e] ? w[e] : 0.f;
+      pv[e] = pruned[e] ? w[e] : 0.f;
+    }
+    st4(X + base + n, make_float4(x[0], x[1], x[2], x[3]));
+    if (compressed) {
+      const uint32_t c0 = sparse_pair_code(keep), c1 = sparse_pair_code(pruned);
+      const float2 a = pick_pair(x, SlotCode{int(c0 & 3u), int(c0 >> 2), true, true});
+      const float2 b = pick_pair(pv, SlotCode{int(c1 & 3u), int(c1 >> 2), true, true});
+      store_pair_planes(XP + base, g, a.x, a.y);
+      store_pair_planes(WP + base, g, b.x, b.y);
+    } else {
+      st4(W0P + base + n, make_float4(w[0], w[1], w[2], w[3]));
+      st4(XA + base + n, make_float4(x[0], x[1], x[2], x[3]));
+      store_split4(XP + base * 2, n, x);
+      store_split4(WP + base * 2, n, w);
+    }
+  }
+  if (bad) atomicOr(flags, 1);
+}
+
 // Split planes of H (row pitch 4 dp bytes), built once per solve.
 // With `flags`, it also sets flags[0] = 1 if H holds a NaN or Inf (the scan
 // of k_scan_pad_h, for an H that needs no padding).
@@ -807,34 +859,6 @@ __global__ void __launch_bounds__(kThreads) k_sparse_index(const uint8_t* mask, 
   if (bad2) atomicOr(flags + 2, 1);
 }
 
-// Compressed planes of the two setup operands of a sparse solve, one thread
-// per group of 4: x0 = sel(mask, w0, 0) at the kept pair (into XP0) and the
-// pruned part p = w0 - x0 at the pruned pair (into XP1). W is the padded
-// copy of w0 (pitch dp).
-__global__ void __launch_bounds__(kThreads) k_setup_planes(const float* W, const uint8_t* mask,
-                                                           int n_cols, int d, int dp,
-                                                           uint16_t* XP0, uint16_t* XP1) {
-  const int groups = dp / 4;
-  const int64_t t = int64_t(blockIdx.x) * kThreads + threadIdx.x;
-  if (t >= int64_t(n_cols) * groups) return;
-  const int j = int(t / groups), g = int(t % groups);
-  const float4 w4 = ld4(W + size_t(j) * dp + 4 * g);
-  const float w[4] = {w4.x, w4.y, w4.z, w4.w};
-  bool keep[4], pruned[4];
-  mask4(mask, d, j, 4 * g, keep);
-  float x0[4], pv[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    pruned[e] = !keep[e] && 4 * g + e < d;
-    x0[e] = keep[e] ? w[e] : 0.f;
-    pv[e] = pruned[e] ? w[e] : 0.f;
-  }
-  const uint32_t c0 = sparse_pair_code(keep), c1 = sparse_pair_code(pruned);
-  const float2 a = pick_pair(x0, SlotCode{int(c0 & 3u), int(c0 >> 2), true, true});
-  const float2 b = pick_pair(pv, SlotCode{int(c1 & 3u), int(c1 >> 2), true, true});
-  store_pair_planes(XP0 + size_t(j) * dp, g, a.x, a.y);
-  store_pair_planes(XP1 + size_t(j) * dp, g, b.x, b.y);
-}
 
 // Zero-padded copy of H (used when d is not a multiple of the tile) with a
 // finiteness scan; with hp == nullptr it only scans.
@@ -1569,24 +1593,31 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     OPTIMA_LAUNCH_CHECK();
   }
   const dim3 vec_grid(unsigned(nc), unsigned(ceil_div(dp, 4 * kThreads)));
-  // W0 padded copy goes to HX first; Hw0 = H w0, then Hx = Hx_ag = H x0.
-  // Split planes: x0 into XP0, W0 into XP1 (free until the first update).
-  hipLaunchKernelGGL(k_prep, vec_grid, dim3(kThreads), 0, s, W0, mask, nc, di, dp, l.HX, l.X0,
-                     l.XA, split ? l.XP0 : nullptr, split ? l.XP1 : nullptr, o.col_scale,
-                     l.flags);
-  OPTIMA_LAUNCH_CHECK();
-  if (split) {
-    hipLaunchKernelGGL(k_split_h, dim3(unsigned(dp), unsigned(ceil_div(dp, 4 * kThreads))),
-                       dim3(kThreads), 0, s, Hm, dp, l.HP, scan_in_split ? l.flags : nullptr);
-    OPTIMA_LAUNCH_CHECK();
-  }
   // The rAPDHG iteration products skip the pruned entries on the 2:4 sparse
-  // MFMA when every group of 4 of every mask row keeps at most 2.
+  // MFMA when every group of 4 of every mask row keeps at most 2. The index
+  // words come first: k_prep_sparse reads the flags they set.
   const bool try_sparse = split && !use_cg && o.sparse;
   if (try_sparse) {
     const int64_t words = int64_t(nc) * (dp / 16);
     hipLaunchKernelGGL(k_sparse_index, dim3(unsigned(ceil_div(words, kThreads))), dim3(kThreads),
                        0, s, mask, nc, di, dp, l.XIDX, l.SLOT, l.XIDX2, l.flags);
+    OPTIMA_LAUNCH_CHECK();
+    // x0, and either the compressed planes of x0 and of p = w0 - x0 or
+    // everything k_prep writes (see k_prep_sparse).
+    const dim3 g_grid(unsigned(nc), unsigned(ceil_div(dp / 4, kThreads)));
+    hipLaunchKernelGGL(k_prep_sparse, g_grid, dim3(kThreads), 0, s, W0, mask, di, dp, l.HX, l.X0,
+                       l.XA, l.XP0, l.XP1, o.col_scale, l.flags);
+  } else {
+    // W0 padded copy goes to HX first; Hw0 = H w0, then Hx = Hx_ag = H x0.
+    // Split planes: x0 into XP0, W0 into XP1 (free until the first update).
+    hipLaunchKernelGGL(k_prep, vec_grid, dim3(kThreads), 0, s, W0, mask, nc, di, dp, l.HX, l.X0,
+                       l.XA, split ? l.XP0 : nullptr, split ? l.XP1 : nullptr, o.col_scale,
+                       l.flags);
+  }
+  OPTIMA_LAUNCH_CHECK();
+  if (split) {
+    hipLaunchKernelGGL(k_split_h, dim3(unsigned(dp), unsigned(ceil_div(dp, 4 * kThreads))),
+                       dim3(kThreads), 0, s, Hm, dp, l.HP, scan_in_split ? l.flags : nullptr);
     OPTIMA_LAUNCH_CHECK();
   }
   int flags[3] = {0, 0, 0};
@@ -1612,12 +1643,9 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   if (sparse && !flags[2]) {
     // Both setup operands are 2:4-compressible: H x0 on the kept pairs and
     // H w0 = H x0 + H p with p = w0 - x0 on the pruned pairs, both on the
-    // sparse MFMA. Where w0 is zero off the mask, H p is exactly zero and
-    // H w0 equals H x0 bit for bit.
-    const int64_t groups = int64_t(nc) * (dp / 4);
-    hipLaunchKernelGGL(k_setup_planes, dim3(unsigned(ceil_div(groups, kThreads))), dim3(kThreads),
-                       0, s, l.HX, mask, nc, di, dp, l.XP0, l.XP1);
-    OPTIMA_LAUNCH_CHECK();
+    // sparse MFMA (k_prep_sparse wrote their compressed planes). Where w0 is
+    // zero off the mask, H p is exactly zero and H w0 equals H x0 bit for
+    // bit.
     p.A = l.X0;
     p.Ap = l.XP0;
     p.Aidx = l.XIDX;
