@@ -153,3 +153,22 @@ def test_sparse_option_validation(L):
         _, _, info = gpu_solve(L, to_dev(H), to_dev(np.array([lam])), W0, M,
                                _opts(L, max_iters=64, fixed_iters=1, **kw))
         assert info["sparse_products"] == 0
+
+
+@pytest.mark.parametrize("n", [1, 5, 8, 9])
+def test_sparse_few_columns_match_closed_form(L, n):
+    # 1 to 8 active columns of a 2:4 solve run the few-column sparse kernel
+    # (H streamed once per iteration, x compressed); 9 take the tiles. Both
+    # reach the closed form, and the columns agree with the same columns of a
+    # full batch.
+    H, W0, M, lam = _tiny_2to4()
+    Hd, lmd = to_dev(H), to_dev(np.array([lam]))
+    opts = _opts(L, max_iters=1000, fixed_iters=1)
+    Wg, st, info = gpu_solve(L, Hd, lmd, W0[:n], M[:n], opts)
+    assert info["sparse_products"] == 1
+    assert info["few_launches"] == (1000 if n <= 8 else 0)
+    Wg = Wg.cpu().numpy()
+    _assert_w_and_f(H, W0[:n], M[:n], Wg, oracle.closed_form(H, W0[:n], M[:n]),
+                    label=f"sparse {n} columns")
+    full, _, _ = gpu_solve(L, Hd, lmd, W0, M, opts)
+    assert rel_fro(Wg, full.cpu().numpy()[:n]) <= 1e-5
