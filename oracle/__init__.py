@@ -3,11 +3,12 @@
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
 this package. The product library never does.
 """
-from .optima_oracle import (hessian, damp, jacobi_scale, power_iteration, subspace_iteration, wanda_mask,
+from .optima_oracle import (hessian, damp, jacobi_scale, power_iteration, subspace_iteration, lanczos,
+                            wanda_mask,
                             objective,
                             closed_form, kkt_solve, cg, rapdhg, check_decision,
                             SolverOptions, SolveResult)
 
-__all__ = ["hessian", "damp", "jacobi_scale", "power_iteration", "subspace_iteration", "wanda_mask", "objective",
+__all__ = ["hessian", "damp", "jacobi_scale", "power_iteration", "subspace_iteration", "lanczos", "wanda_mask", "objective",
            "closed_form",
            "kkt_solve", "cg", "rapdhg", "check_decision", "SolverOptions", "SolveResult"]

@@ -26,6 +26,15 @@ subspace_iteration
                  lambda_2/lambda_1, which matters for Hessians whose top
                  eigenvalues cluster (outlier channels). b = 1 is
                  power_iteration.
+lanczos          The same quantity by the Lanczos method with full
+                 reorthogonalisation (Lanczos 1950; Golub & Van Loan, "Matrix
+                 Computations", the symmetric Lanczos process; Parlett, "The
+                 Symmetric Eigenvalue Problem"): the largest Ritz value of the
+                 Krylov space of the start vector, from the tridiagonal matrix
+                 of the three-term recurrence. It converges like a Chebyshev
+                 polynomial of the step count, so spectra whose top has no gap
+                 (near-isotropic inputs, or H after diagonal scaling) need far
+                 fewer products with H than subspace_iteration.
 wanda_mask       The mask the weight update starts from (Algorithm 1 takes M from
                  a selector; the configurations use Wanda, cited in Section 2,
                  with the 2:4 pattern of Section 4): score w0_ji^2 c_i in fp64
@@ -85,7 +94,11 @@ hessian, damp, objective, closed_form, kkt_solve: pinned by brute force, exact
 rational arithmetic and closed forms in the CPU tests. power_iteration: pinned
 by LAPACK eigenvalues. subspace_iteration: pinned by LAPACK eigenvalues of
 matrices with known spectra, the Ritz upper bound, a hand-worked 2x2 case and
-its reduction to power_iteration at b = 1. wanda_mask: pinned by the rank
+its reduction to power_iteration at b = 1. lanczos: pinned by the
+recurrence coefficients of the discrete Chebyshev (Gram) polynomials (H =
+diag(1..n), all-ones start), the Rayleigh-Ritz value of an explicitly built
+Krylov basis, a hand-worked 2x2 case, breakdown on a two-eigenvalue spectrum,
+the monotone Ritz bound, and LAPACK eigenvalues of the layer Hessians. wanda_mask: pinned by the rank
 definition evaluated by brute force (an entry is kept iff fewer than k
 entries beat it), hand-made ties and the keep counts. rapdhg: its fixed point is pinned by closed_form and its
 iterates by the invariants (pruned entries exactly +0.0, accepted restarts never
@@ -197,6 +210,62 @@ def subspace_iteration(H: np.ndarray, V0: np.ndarray, max_iters: int = 1000,
             return theta, it
         theta_prev = theta
     return theta, max_iters
+
+
+# Relative size of beta_j below which the Krylov space counts as invariant.
+LANCZOS_BREAKDOWN = 1e-6
+
+
+def lanczos(H: np.ndarray, v0: np.ndarray, max_steps: int = 256, tol: float = 1e-6,
+            tridiagonal: bool = False):
+    """Largest eigenvalue of symmetric PSD H by the Lanczos method.
+
+    Step j (1-based) extends the orthonormal basis q_1 = v0/||v0||, ..., q_j of
+    the Krylov space K_j = span{v0, H v0, ..., H^(j-1) v0}:
+      w = H q_j, alpha_j = q_j^T w,
+      w <- w - alpha_j q_j - beta_(j-1) q_(j-1),
+      w <- w - Q_j (Q_j^T w)   (full reorthogonalisation, once more),
+      beta_j = ||w||, q_(j+1) = w / beta_j.
+    T_j = tridiag(beta_(1..j-1); alpha_(1..j); beta_(1..j-1)) equals
+    Q_j^T H Q_j, so theta_j = lambda_max(T_j) is the largest Ritz value of
+    K_j. Ritz values never exceed lambda_max(H) and theta_j never decreases
+    with j. It stops when |theta_j - theta_(j-1)| <= tol * theta_j, when
+    beta_j <= LANCZOS_BREAKDOWN * theta_j (K_j is numerically invariant and
+    theta_j an eigenvalue), or after max_steps steps (at most d).
+    Returns (theta, steps), plus (alpha, beta) when `tridiagonal` is set.
+    """
+    H = np.asarray(H, dtype=np.float64)
+    d = H.shape[0]
+    q = np.asarray(v0, dtype=np.float64)
+    q = q / np.linalg.norm(q)
+    Q = [q]
+    alpha: list[float] = []
+    beta: list[float] = []
+    theta = 0.0
+    theta_prev = None
+    steps = 0
+    for j in range(1, min(max_steps, d) + 1):
+        steps = j
+        w = H @ Q[-1]
+        alpha.append(float(Q[-1] @ w))
+        w = w - alpha[-1] * Q[-1]
+        if j > 1:
+            w = w - beta[-1] * Q[-2]
+        B = np.array(Q)
+        w = w - B.T @ (B @ w)
+        b = float(np.linalg.norm(w))
+        T = np.diag(alpha) + np.diag(beta, 1) + np.diag(beta, -1)
+        theta = float(np.linalg.eigvalsh(T)[-1])
+        if theta_prev is not None and abs(theta - theta_prev) <= tol * abs(theta):
+            break
+        if b <= LANCZOS_BREAKDOWN * abs(theta):
+            break
+        theta_prev = theta
+        beta.append(b)
+        Q.append(w / b)
+    if tridiagonal:
+        return theta, steps, np.array(alpha), np.array(beta[:steps - 1])
+    return theta, steps
 
 
 # ----------------------------------------------------------------------------
