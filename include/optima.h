@@ -174,6 +174,43 @@ optima_status optima_spectral_norm(const float* H, int64_t d, const float* V0,
                                    int32_t* iters, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * The same lambda_max (the step size of Section 3.3's first-order solver) by
+ * the symmetric Lanczos process with full reorthogonalisation. Step j builds
+ * q_j of an orthonormal basis of the Krylov space span{v0, H v0, ...,
+ * H^(j-1) v0} from one product with H:
+ *   w = H q_j, alpha_j = q_j^T w, w <- w - alpha_j q_j - beta_(j-1) q_(j-1),
+ *   w <- w - Q (Q^T w), beta_j = ||w||, q_(j+1) = w / beta_j,
+ * and rho_j = the largest eigenvalue of the j x j tridiagonal matrix
+ * T = tridiag(beta; alpha; beta) = Q^T H Q (the largest Ritz value of the
+ * Krylov space; never above lambda_max(H), non-decreasing in j). Its
+ * convergence goes as a Chebyshev polynomial of the step count, so spectra
+ * whose top has no gap (near-isotropic inputs, or H after diagonal scaling)
+ * need far fewer passes over H than the subspace iteration of
+ * optima_spectral_norm. The basis is fp32, all sums fp64; the eigenvalue of
+ * T comes from Sturm-count bisection in fp64 (relative width 1e-15).
+ *
+ * H: [d][d] fp32, symmetric, 4-byte aligned (16-byte alignment and d % 4 ==
+ * 0 enable vector loads). v0: [d] fp32 device start vector, not modified.
+ * It stops once |rho_j - rho_(j-1)| <= tol * rho_j, once beta_j <= 1e-6 *
+ * rho_j (the Krylov space is invariant: rho_j is an eigenvalue), or after
+ * min(max_steps, d) steps, 1 <= max_steps <= OPTIMA_LANCZOS_MAX_STEPS.
+ * Without a gap at the top of the spectrum the Ritz value rises by small
+ * amounts long before it converges: there tol = 1e-7 stops within about
+ * 1e-6 of lambda_max where 1e-6 can stop 3e-4 short.
+ * lambda_max (device, one float) receives the last rho (0 for a zero v0, NaN
+ * if H or v0 holds NaN/Inf); steps (device int32, may be NULL) the step
+ * count. Blocking: the call synchronises `stream` every 8 steps to test
+ * convergence. ws: optima_spectral_lanczos_workspace_bytes(d, max_steps)
+ * bytes (about max_steps * d * 4 for the basis).
+ * ------------------------------------------------------------------------- */
+#define OPTIMA_LANCZOS_MAX_STEPS 256
+size_t optima_spectral_lanczos_workspace_bytes(int64_t d, int max_steps);
+optima_status optima_spectral_lanczos(const float* H, int64_t d, const float* v0,
+                                      int max_steps, float tol, void* ws,
+                                      size_t ws_bytes, float* lambda_max,
+                                      int32_t* steps, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Wanda mask selection -- the mask M that the weight update starts from
  * (Algorithm 1 takes it from a selector; the configurations use the Wanda
  * saliency cited in Section 2, with the 2:4 pattern of Section 4).

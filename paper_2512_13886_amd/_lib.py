@@ -78,7 +78,7 @@ def _sig(name, res, args):
 _status_string = _sig("optima_status_string", ctypes.c_char_p, [_i32])
 _abi_version = _sig("optima_abi_version", _i32, [])
 # The structs above mirror include/optima.h at this ABI version.
-ABI_VERSION = 9
+ABI_VERSION = 10
 if _abi_version() != ABI_VERSION:
     raise ImportError(f"{_LIB_PATH} has ABI version {_abi_version()}, the binding expects "
                       f"{ABI_VERSION}: rebuild the library")
@@ -90,6 +90,9 @@ _jacobi = _sig("optima_hessian_jacobi", _i32, [_vp, _i64, _vp, _vp])
 _spec_ws = _sig("optima_spectral_norm_workspace_bytes", _sz, [_i64, _i32])
 _spec = _sig("optima_spectral_norm", _i32,
              [_vp, _i64, _vp, _i32, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
+_lz_ws = _sig("optima_spectral_lanczos_workspace_bytes", _sz, [_i64, _i32])
+_lz = _sig("optima_spectral_lanczos", _i32,
+           [_vp, _i64, _vp, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
 _mask = _sig("optima_wanda_mask", _i32,
              [_vp, _i64, _i64, _vp, _i32, _i64, _i32, ctypes.c_double, _vp, _vp])
 _fwd_ws = _sig("optima_linear_forward_workspace_bytes", _sz, [_i64, _i64, _i64])
@@ -249,6 +252,31 @@ def optima_spectral_norm(H: torch.Tensor, V0: torch.Tensor, lambda_max: torch.Te
     ws, nbytes = _workspace(optima_spectral_norm_workspace_bytes(d, block), ws, H.device)
     _check(_spec(_ptr(H), d, _ptr(V0), int(block), int(max_iters), float(tol), _ptr(ws), nbytes,
                  _ptr(lambda_max), _ptr(iters), _stream(stream)))
+
+
+LANCZOS_MAX_STEPS = 256
+
+
+def optima_spectral_lanczos_workspace_bytes(d: int, max_steps: int = LANCZOS_MAX_STEPS) -> int:
+    return int(_lz_ws(d, max_steps))
+
+
+def optima_spectral_lanczos(H: torch.Tensor, v0: torch.Tensor, lambda_max: torch.Tensor,
+                            max_steps: int = LANCZOS_MAX_STEPS, tol: float = 1e-7,
+                            ws: torch.Tensor | None = None, steps: torch.Tensor | None = None,
+                            stream=None) -> None:
+    """lambda_max(H) by the Lanczos process started from v0 [d]."""
+    _need_cuda("H", H, torch.float32)
+    _need_cuda("v0", v0, torch.float32)
+    _need_cuda("lambda_max", lambda_max, torch.float32)
+    if steps is not None:
+        _need_cuda("steps", steps, torch.int32)
+    d = H.shape[0]
+    if v0.dim() != 1 or v0.shape[0] != d:
+        raise ValueError("v0 must be [d]")
+    ws, nbytes = _workspace(optima_spectral_lanczos_workspace_bytes(d, max_steps), ws, H.device)
+    _check(_lz(_ptr(H), d, _ptr(v0), int(max_steps), float(tol), _ptr(ws), nbytes,
+               _ptr(lambda_max), _ptr(steps), _stream(stream)))
 
 
 ACT_NONE = 0

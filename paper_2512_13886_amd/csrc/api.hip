@@ -12,6 +12,10 @@ size_t spectral_norm_workspace_bytes(int64_t d, int block);
 optima_status spectral_norm(const float* H, int64_t d, const float* V0, int block, int max_iters,
                             float tol, void* ws, float* lambda_max, int32_t* iters,
                             hipStream_t s);
+size_t spectral_lanczos_workspace_bytes(int64_t d, int max_steps);
+optima_status spectral_lanczos(const float* H, int64_t d, const float* v0, int max_steps,
+                               float tol, void* ws, float* lambda_max, int32_t* steps,
+                               hipStream_t s);
 optima_status wanda_mask(const float* W0, int64_t n_cols, int64_t d, const void* col_sq,
                          int col_dtype, int64_t col_stride, int pattern, double sparsity,
                          uint8_t* mask, hipStream_t s);
@@ -51,7 +55,7 @@ const char* optima_status_string(optima_status status) {
   }
 }
 
-int optima_abi_version(void) { return 9; }
+int optima_abi_version(void) { return 10; }
 
 size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
   if (n_tok < 0 || d < 1 || d > kMaxDim) return 0;
@@ -107,6 +111,23 @@ optima_status optima_spectral_norm(const float* H, int64_t d, const float* V0, i
   if (!ws || ws_bytes < optima::spectral_norm_workspace_bytes(d, block))
     return OPTIMA_E_WORKSPACE;
   return optima::spectral_norm(H, d, V0, block, max_iters, tol, ws, lambda_max, iters, stream);
+}
+
+size_t optima_spectral_lanczos_workspace_bytes(int64_t d, int max_steps) {
+  if (d < 1 || d > kMaxDim || max_steps < 1 || max_steps > OPTIMA_LANCZOS_MAX_STEPS) return 0;
+  return optima::spectral_lanczos_workspace_bytes(d, max_steps);
+}
+
+optima_status optima_spectral_lanczos(const float* H, int64_t d, const float* v0, int max_steps,
+                                      float tol, void* ws, size_t ws_bytes, float* lambda_max,
+                                      int32_t* steps, hipStream_t stream) {
+  if (!H || !v0 || !lambda_max || d < 1 || d > kMaxDim || !(tol >= 0.f)) return OPTIMA_E_INVAL;
+  if (max_steps < 1 || max_steps > OPTIMA_LANCZOS_MAX_STEPS) return OPTIMA_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(v0) & 3) || (reinterpret_cast<uintptr_t>(H) & 3))
+    return OPTIMA_E_INVAL;
+  if (!ws || ws_bytes < optima::spectral_lanczos_workspace_bytes(d, max_steps))
+    return OPTIMA_E_WORKSPACE;
+  return optima::spectral_lanczos(H, d, v0, max_steps, tol, ws, lambda_max, steps, stream);
 }
 
 optima_status optima_wanda_mask(const float* W0, int64_t n_cols, int64_t d, const void* col_sq,

@@ -37,6 +37,33 @@ struct PowState {
 constexpr int kRowsPerWave = 2;
 constexpr int kRowsPerBlock = (kThreads / 64) * kRowsPerWave;
 
+// h . v over d entries by one wave (16-byte loads when VEC4: d % 4 == 0 and
+// both rows 16-byte aligned); every lane returns the sum.
+template <bool VEC4>
+__device__ inline float row_dot(const float* h, const float* v, int64_t d, int lane) {
+  float acc0 = 0.f, acc1 = 0.f;
+  if (VEC4) {
+    const int64_t n4 = d >> 2;
+    const float4* h4 = reinterpret_cast<const float4*>(h);
+    const float4* v4 = reinterpret_cast<const float4*>(v);
+    int64_t k = lane;
+    for (; k + 64 < n4; k += 128) {
+      const float4 a = h4[k], b = v4[k], c = h4[k + 64], e = v4[k + 64];
+      acc0 += a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+      acc1 += c.x * e.x + c.y * e.y + c.z * e.z + c.w * e.w;
+    }
+    for (; k < n4; k += 64) {
+      const float4 a = h4[k], b = v4[k];
+      acc0 += a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+    }
+  } else {
+    for (int64_t k = lane; k < d; k += 64) acc0 += h[k] * v[k];
+  }
+  float acc = acc0 + acc1;
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+  return acc;
+}
+
 // Power iteration i (1-based): y_i = H v_{i-1} / ||v_{i-1}|| with one wave per
 // row. Every workgroup first sums the partials (||y||^2, v.y) that all
 // workgroups of iteration i - 1 left in part[(i-1) & 1], in the same fixed
@@ -93,27 +120,7 @@ __global__ void __launch_bounds__(kThreads) k_power_iter(const float* H, int64_t
     const int64_t row = int64_t(blockIdx.x) * kRowsPerBlock + lr;
     double n2 = 0.0, dt = 0.0;
     if (row < d) {
-      const float* h = H + row * d;
-      float acc0 = 0.f, acc1 = 0.f;
-      if (VEC4) {
-        const int64_t n4 = d >> 2;
-        const float4* h4 = reinterpret_cast<const float4*>(h);
-        const float4* v4 = reinterpret_cast<const float4*>(vin);
-        int64_t k = lane;
-        for (; k + 64 < n4; k += 128) {
-          const float4 a = h4[k], b = v4[k], c = h4[k + 64], e = v4[k + 64];
-          acc0 += a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
-          acc1 += c.x * e.x + c.y * e.y + c.z * e.z + c.w * e.w;
-        }
-        for (; k < n4; k += 64) {
-          const float4 a = h4[k], b = v4[k];
-          acc0 += a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
-        }
-      } else {
-        for (int64_t k = lane; k < d; k += 64) acc0 += h[k] * vin[k];
-      }
-      float acc = acc0 + acc1;
-      for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+      const float acc = row_dot<VEC4>(H + row * d, vin, d, lane);
       const float yr = float(double(acc) * inv);
       if (lane == 0) {
         y[row] = yr;
@@ -514,6 +521,313 @@ __global__ void __launch_bounds__(256) k_subspace_finish(const double* tot, int 
 
 __global__ void k_copy_sub_iters(const SubState* st, int32_t* iters) { *iters = st->iters; }
 
+// ---------------------------------------------------------------------------
+// Lanczos
+// ---------------------------------------------------------------------------
+//
+// Step j (0-based) of the symmetric Lanczos process with full
+// reorthogonalisation, six launches:
+//   k_lz_matvec  q_j = w / ||w|| (w: the previous step's residual, or v0),
+//                y = H q_j (one wave per row, HBM-bound), and per workgroup
+//                the partial sums of q_i . y, i <= j;
+//   k_lz_coef    c_i = q_i . y (fixed-order sums of those partials);
+//   k_lz_orth    w = y - sum_i c_i q_i, and partial sums of q_i . w;
+//   k_lz_coef    c'_i = q_i . w;
+//   k_lz_orth    w <- w - sum_i c'_i q_i, and partial sums of ||w||^2;
+//   k_lz_finish  alpha_j = c_j + c'_j, beta_j = ||w||, and the largest
+//                eigenvalue of T = tridiag(beta; alpha; beta) by Sturm-count
+//                multisection in fp64; the stopping test.
+// In exact arithmetic c_i vanishes for i < j - 1, c_(j-1) = beta_(j-1) and
+// c_j = alpha_j: the two passes are the three-term recurrence followed by one
+// more Gram-Schmidt pass over the whole basis, in classical form. The basis
+// is kept in fp32 (pitch dp), every sum in fp64. A set `conv` makes every
+// later launch return at once.
+
+constexpr int kLzMax = OPTIMA_LANCZOS_MAX_STEPS;
+constexpr int kLzRows = 64;                 // rows per workgroup of k_lz_orth
+constexpr int kLzFinThreads = 512;          // multisection points per round
+constexpr double kLzBreakdown = 1e-6;       // beta_j <= this * theta_j: K_j invariant
+constexpr double kLzWidth = 1e-12;          // relative width that ends the multisection
+constexpr int kLzRounds = 8;
+constexpr double kLzGeoSpan = 44.0;         // first round: offsets W 2^-44 .. W
+
+struct LzState {
+  double alpha[kLzMax];
+  double beta[kLzMax];
+  double c[2][kLzMax];  // coefficients of the two Gram-Schmidt passes
+  double inv;           // 1 / ||w|| of the vector that becomes q_j
+  double theta;         // largest Ritz value after the last finished step
+  double theta_lo;      // a value not above it (the final bracket's lower end)
+  int conv;
+  int steps;
+};
+
+// w = v0, inv = 1 / ||v0||. A zero start vector ends at once with 0; a
+// non-finite one with NaN.
+__global__ void __launch_bounds__(1024) k_lz_init(const float* v0, int64_t d, float* w,
+                                                  LzState* st, float* lambda_out) {
+  __shared__ double red[16];
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < d; i += 1024) {
+    const float x = v0[i];
+    w[i] = x;
+    s += double(x) * double(x);
+  }
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int k = 0; k < 16; ++k) t += red[k];
+    const bool ok = t > 0.0 && isfinite(t);
+    st->inv = ok ? 1.0 / sqrt(t) : 0.0;
+    st->theta = 0.0;
+    st->theta_lo = -INFINITY;
+    st->conv = ok ? 0 : 1;
+    st->steps = 0;
+    *lambda_out = isfinite(t) ? 0.f : __builtin_nanf("");
+  }
+}
+
+template <bool VEC4>
+__global__ void __launch_bounds__(kThreads) k_lz_matvec(const float* H, int64_t d, int64_t dp,
+                                                        const float* w, float* Q, int j, float* y,
+                                                        double* part, int nblk, LzState* st) {
+  if (st->conv) return;
+  __shared__ float ys[kRowsPerBlock], qs[kRowsPerBlock];
+  const double inv = st->inv;
+  float* qj = Q + int64_t(j) * dp;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int q = 0; q < kRowsPerWave; ++q) {
+    const int lr = wv * kRowsPerWave + q;
+    const int64_t row = int64_t(blockIdx.x) * kRowsPerBlock + lr;
+    float yr = 0.f, qr = 0.f;
+    if (row < d) {
+      yr = float(double(row_dot<VEC4>(H + row * d, w, d, lane)) * inv);
+      qr = float(double(w[row]) * inv);
+      if (lane == 0) {
+        y[row] = yr;
+        qj[row] = qr;
+      }
+    }
+    if (lane == 0) {
+      ys[lr] = yr;
+      qs[lr] = qr;
+    }
+  }
+  __syncthreads();
+  const int64_t r0 = int64_t(blockIdx.x) * kRowsPerBlock;
+  for (int i = threadIdx.x; i <= j; i += kThreads) {
+    double sum = 0.0;
+    for (int r = 0; r < kRowsPerBlock && r0 + r < d; ++r) {
+      const float qv = i == j ? qs[r] : Q[int64_t(i) * dp + r0 + r];
+      sum += double(qv) * double(ys[r]);
+    }
+    part[int64_t(i) * nblk + blockIdx.x] = sum;
+  }
+}
+
+// c[pass][i] = sum over blocks of part[i][*] in a fixed order, one wave per i.
+__global__ void __launch_bounds__(kThreads) k_lz_coef(const double* part, int nblk, int j,
+                                                      int pass, LzState* st) {
+  if (st->conv) return;
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (i > j) return;
+  const double* p = part + int64_t(i) * nblk;
+  double s0 = 0.0, s1 = 0.0;
+  int b = lane;
+  for (; b + 64 < nblk; b += 128) {
+    s0 += p[b];
+    s1 += p[b + 64];
+  }
+  if (b < nblk) s0 += p[b];
+  double s = s0 + s1;
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  if (lane == 0) st->c[pass][i] = s;
+}
+
+// One Gram-Schmidt pass over kLzRows rows: w = src - sum_{i<=j} c[pass]_i q_i
+// (wave v takes the terms i = v mod 4, summed in LDS in a fixed order). Pass
+// 0 then leaves the partial sums of q_i . w in part[i][block]; pass 1 the
+// partial ||w||^2 in norm_part[block].
+__global__ void __launch_bounds__(kThreads) k_lz_orth(const float* Q, int64_t d, int64_t dp,
+                                                      int j, int pass, const float* src,
+                                                      float* w, double* part, int nblk,
+                                                      double* norm_part, LzState* st) {
+  if (st->conv) return;
+  constexpr int kW = kThreads / 64;
+  __shared__ double sum[kW][kLzRows];
+  __shared__ float ws[kLzRows];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t r0 = int64_t(blockIdx.x) * kLzRows, r = r0 + lane;
+  const bool in = r < d;
+  const double* c = st->c[pass];
+  double acc = 0.0;
+  if (in)
+    for (int i = wv; i <= j; i += kW) acc += c[i] * double(Q[int64_t(i) * dp + r]);
+  sum[wv][lane] = acc;
+  __syncthreads();
+  if (wv == 0) {
+    float wr = 0.f;
+    if (in) {
+      const double t = ((sum[0][lane] + sum[1][lane]) + sum[2][lane]) + sum[3][lane];
+      wr = float(double(src[r]) - t);
+      w[r] = wr;
+    }
+    ws[lane] = wr;
+  }
+  __syncthreads();
+  if (pass == 0) {
+    for (int i = wv; i <= j; i += kW) {
+      double s = in ? double(Q[int64_t(i) * dp + r]) * double(ws[lane]) : 0.0;
+      for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+      if (lane == 0) part[int64_t(i) * nblk + blockIdx.x] = s;
+    }
+  } else if (wv == 0) {
+    double s = double(ws[lane]) * double(ws[lane]);
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    if (lane == 0) norm_part[blockIdx.x] = s;
+  }
+}
+
+// Number of eigenvalues of the n x n tridiagonal matrix below x, from the
+// signs of the LDL^T pivots of T - x I (Sturm count). ab[k] holds (a_k,
+// b_(k-1)^2), b_(-1)^2 = 0. Pivots smaller than pivmin in magnitude become
+// -pivmin. Each pivot's reciprocal is the hardware estimate refined by one
+// Newton step (error a few ulps); the count tolerates relative errors of
+// that size in the pivots, since they amount to a tiny perturbation of T.
+__device__ inline int lz_count_below(const double2* ab, int n, double x, double pivmin) {
+  double p = 1.0;  // the pivot before the first one: b_(-1)^2 / p adds nothing
+  int cnt = 0;
+  for (int k = 0; k < n; ++k) {
+    const double2 e = ab[k];
+    double r = __builtin_amdgcn_rcp(p);
+    r = fma(r, fma(-p, r, 1.0), r);
+    p = fma(-e.y, r, e.x - x);
+    if (fabs(p) < pivmin) p = -pivmin;
+    cnt += p < 0.0;
+  }
+  return cnt;
+}
+
+// Multisection point t of round `round` in [lo, hi]: the first round spaces
+// the offsets from lo geometrically (W 2^-44 .. W, W = hi - lo), since the
+// top Ritz value moves little from one step to the next; later rounds
+// uniformly.
+__device__ inline double lz_point(double lo, double hi, int round, int t) {
+  if (round == 0)
+    return t == kLzFinThreads - 1
+               ? hi
+               : lo + (hi - lo) * exp2(-kLzGeoSpan * (1.0 - double(t + 1) / kLzFinThreads));
+  return lo + (hi - lo) / double(kLzFinThreads + 1) * double(t + 1);
+}
+
+// alpha_j, beta_j, theta_j = lambda_max(T_(j+1)) and the stopping decision:
+// stop when |theta_j - theta_(j-1)| <= tol theta_j, when beta_j <=
+// kLzBreakdown theta_j, or after n_max steps. One workgroup; the largest
+// eigenvalue of T to a relative width of kLzWidth.
+__global__ void __launch_bounds__(kLzFinThreads) k_lz_finish(const double* norm_part, int nblk,
+                                                             int j, int n_max, float tol,
+                                                             LzState* st, float* lambda_out) {
+  if (st->conv) return;
+  constexpr int kW = kLzFinThreads / 64;
+  __shared__ double2 ab[kLzMax];
+  __shared__ double rs[kW], ramax[kW], rgmax[kW], rbmax[kW];
+  __shared__ int rbad[kW];
+  __shared__ double lo_s, hi_s;
+  __shared__ int first_all;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6, n = j + 1;
+  const double alpha = st->c[0][j] + st->c[1][j];
+  // ||w||^2, and per row of T its diagonal and Gershgorin bound.
+  double s = 0.0;
+  for (int k = t; k < nblk; k += kLzFinThreads) s += norm_part[k];
+  double am = -INFINITY, gm = -INFINITY, bm = 0.0;
+  int bad = 0;
+  if (t < n) {
+    const double a = t == j ? alpha : st->alpha[t];
+    const double bl = t > 0 ? st->beta[t - 1] : 0.0, br = t < j ? st->beta[t] : 0.0;
+    ab[t] = make_double2(a, bl * bl);
+    am = a;
+    gm = a + fabs(bl) + fabs(br);
+    bm = br * br;
+    bad = !(isfinite(a) && isfinite(bl));
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    s += __shfl_xor(s, o, 64);
+    am = fmax(am, __shfl_xor(am, o, 64));
+    gm = fmax(gm, __shfl_xor(gm, o, 64));
+    bm = fmax(bm, __shfl_xor(bm, o, 64));
+    bad |= __shfl_xor(bad, o, 64);
+  }
+  if (lane == 0) {
+    rs[wv] = s;
+    ramax[wv] = am;
+    rgmax[wv] = gm;
+    rbmax[wv] = bm;
+    rbad[wv] = bad;
+  }
+  __syncthreads();
+  double beta2 = 0.0, amax = -INFINITY, gmax = -INFINITY, bmax = 0.0;
+  for (int k = 0; k < kW; ++k) {
+    beta2 += rs[k];
+    amax = fmax(amax, ramax[k]);
+    gmax = fmax(gmax, rgmax[k]);
+    bmax = fmax(bmax, rbmax[k]);
+    bad |= rbad[k];
+  }
+  const bool finite = !bad && isfinite(beta2);
+  double theta;
+  if (!finite) {
+    theta = __builtin_nan("");
+  } else {
+    // lambda_max(T) lies in [max(a_k, theta_lo of the previous step),
+    // Gershgorin bound]: a diagonal entry is a Rayleigh quotient, and T_j
+    // contains T_(j-1) as a leading block (Cauchy interlacing).
+    const double pivmin = 1e-290 * fmax(1.0, bmax);
+    if (t == 0) {
+      lo_s = fmax(amax, st->theta_lo);
+      hi_s = gmax + fmax(fabs(gmax) * 1e-14, 1e-300);
+    }
+    __syncthreads();
+    for (int round = 0; round < kLzRounds; ++round) {
+      const double lo = lo_s, hi = hi_s;
+      if (hi - lo <= kLzWidth * fmax(fabs(lo), fabs(hi))) break;
+      const double x = lz_point(lo, hi, round, t);
+      if (t == 0) first_all = kLzFinThreads;
+      __syncthreads();
+      // count(x_t) is non-decreasing in t; the top eigenvalue lies between the
+      // last point with fewer than n eigenvalues below it and the first with n.
+      if (lz_count_below(ab, n, x, pivmin) == n) atomicMin(&first_all, t);
+      __syncthreads();
+      if (t == 0) {
+        const int f = first_all;
+        lo_s = f == 0 ? lo : lz_point(lo, hi, round, f - 1);
+        hi_s = f == kLzFinThreads ? hi : lz_point(lo, hi, round, f);
+      }
+      __syncthreads();
+    }
+    theta = 0.5 * (lo_s + hi_s);
+  }
+  if (t == 0) {
+    const double beta = sqrt(beta2);
+    const bool done = !finite || n >= n_max ||
+                      (j >= 1 && fabs(theta - st->theta) <= double(tol) * fabs(theta)) ||
+                      beta <= kLzBreakdown * fabs(theta);
+    st->alpha[j] = alpha;
+    st->beta[j] = beta;
+    st->theta = theta;
+    st->theta_lo = finite ? lo_s : -INFINITY;
+    st->steps = n;
+    st->inv = done ? 0.0 : 1.0 / beta;
+    *lambda_out = float(theta);
+    if (done) st->conv = 1;
+  }
+}
+
+__global__ void k_copy_lz_steps(const LzState* st, int32_t* steps) { *steps = st->steps; }
+
 }  // namespace
 
 size_t spectral_norm_workspace_bytes(int64_t d, int block) {
@@ -629,6 +943,33 @@ optima_status subspace_iteration(const float* H, int64_t d, const float* V0, int
   return OPTIMA_OK;
 }
 
+// Workspace of the Lanczos process for at most m steps: the basis (m rows of
+// pitch dp), y, w, the partial sums of both passes and of the norm, state.
+struct LzLayout {
+  float *Q, *y, *w;
+  double *part1, *part2, *norm_part;
+  LzState* st;
+  int64_t dp;
+  int nblk1, nblk2;
+};
+
+LzLayout lz_layout(void* ws, int64_t d, int m, size_t* bytes) {
+  Carver c(ws);
+  LzLayout l{};
+  l.dp = round_up(d, 64);
+  l.nblk1 = int(ceil_div(d, kRowsPerBlock));
+  l.nblk2 = int(ceil_div(d, kLzRows));
+  l.Q = c.take<float>(size_t(m) * size_t(l.dp));
+  l.y = c.take<float>(size_t(l.dp));
+  l.w = c.take<float>(size_t(l.dp));
+  l.part1 = c.take<double>(size_t(m) * size_t(l.nblk1));
+  l.part2 = c.take<double>(size_t(m) * size_t(l.nblk2));
+  l.norm_part = c.take<double>(size_t(l.nblk2));
+  l.st = c.take<LzState>(1);
+  if (bytes) *bytes = c.bytes();
+  return l;
+}
+
 }  // namespace
 
 optima_status spectral_norm(const float* H, int64_t d, const float* V0, int block, int max_iters,
@@ -636,6 +977,58 @@ optima_status spectral_norm(const float* H, int64_t d, const float* V0, int bloc
                             hipStream_t s) {
   if (block == 1) return power_iteration(H, d, V0, max_iters, tol, ws, lambda_max, iters, s);
   return subspace_iteration(H, d, V0, block, max_iters, tol, ws, lambda_max, iters, s);
+}
+
+size_t spectral_lanczos_workspace_bytes(int64_t d, int max_steps) {
+  size_t bytes = 0;
+  lz_layout(nullptr, d, int(std::min<int64_t>(max_steps, d)), &bytes);
+  return bytes;
+}
+
+optima_status spectral_lanczos(const float* H, int64_t d, const float* v0, int max_steps,
+                               float tol, void* ws, float* lambda_max, int32_t* steps,
+                               hipStream_t s) {
+  const int m = int(std::min<int64_t>(max_steps, d));
+  const LzLayout l = lz_layout(ws, d, m, nullptr);
+  hipLaunchKernelGGL(k_lz_init, dim3(1), dim3(1024), 0, s, v0, d, l.w, l.st, lambda_max);
+  OPTIMA_LAUNCH_CHECK();
+  const bool vec4 = (d % 4) == 0 && aligned16(H);
+  constexpr int kPoll = 8;
+  for (int j = 0; j < m; ++j) {
+    if (vec4)
+      hipLaunchKernelGGL(k_lz_matvec<true>, dim3(unsigned(l.nblk1)), dim3(kThreads), 0, s, H, d,
+                         l.dp, l.w, l.Q, j, l.y, l.part1, l.nblk1, l.st);
+    else
+      hipLaunchKernelGGL(k_lz_matvec<false>, dim3(unsigned(l.nblk1)), dim3(kThreads), 0, s, H, d,
+                         l.dp, l.w, l.Q, j, l.y, l.part1, l.nblk1, l.st);
+    OPTIMA_LAUNCH_CHECK();
+    const dim3 cg(unsigned(ceil_div(j + 1, kThreads / 64)));
+    hipLaunchKernelGGL(k_lz_coef, cg, dim3(kThreads), 0, s, l.part1, l.nblk1, j, 0, l.st);
+    OPTIMA_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_lz_orth, dim3(unsigned(l.nblk2)), dim3(kThreads), 0, s, l.Q, d, l.dp, j,
+                       0, l.y, l.w, l.part2, l.nblk2, l.norm_part, l.st);
+    OPTIMA_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_lz_coef, cg, dim3(kThreads), 0, s, l.part2, l.nblk2, j, 1, l.st);
+    OPTIMA_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_lz_orth, dim3(unsigned(l.nblk2)), dim3(kThreads), 0, s, l.Q, d, l.dp, j,
+                       1, l.w, l.w, l.part2, l.nblk2, l.norm_part, l.st);
+    OPTIMA_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_lz_finish, dim3(1), dim3(kLzFinThreads), 0, s, l.norm_part, l.nblk2, j,
+                       m, tol, l.st, lambda_max);
+    OPTIMA_LAUNCH_CHECK();
+    if ((j + 1) % kPoll == 0 && j + 1 < m) {
+      int conv = 0;
+      OPTIMA_HIP_TRY(hipMemcpyAsync(&conv, &l.st->conv, sizeof(int), hipMemcpyDeviceToHost, s));
+      OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+      if (conv) break;
+    }
+  }
+  if (steps) {
+    hipLaunchKernelGGL(k_copy_lz_steps, dim3(1), dim3(1), 0, s, l.st, steps);
+    OPTIMA_LAUNCH_CHECK();
+  }
+  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  return OPTIMA_OK;
 }
 
 }  // namespace optima

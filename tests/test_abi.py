@@ -70,6 +70,12 @@ def test_workspace_queries():
     assert L.optima_spectral_norm_workspace_bytes(4096, 16) >= 2 * 16 * 4096 * 4
     assert L.optima_spectral_norm_workspace_bytes(4096, 17) == 0
     assert L.optima_spectral_norm_workspace_bytes(4096, 0) == 0
+    # The Lanczos basis: one fp32 row of d per step, at most d steps.
+    assert L.optima_spectral_lanczos_workspace_bytes(4096, 64) >= 64 * 4096 * 4
+    assert L.optima_spectral_lanczos_workspace_bytes(10, 256) < \
+        L.optima_spectral_lanczos_workspace_bytes(10, 1) + 10 * 64 * 4 + 4096
+    assert L.optima_spectral_lanczos_workspace_bytes(4096, L.LANCZOS_MAX_STEPS + 1) == 0
+    assert L.optima_spectral_lanczos_workspace_bytes(4096, 0) == 0
     assert L.SPECTRAL_MAX_BLOCK == 16
 
 
