@@ -107,8 +107,11 @@ def block_leg(L, torch, dev, precision) -> dict:
     stream the Hessian, the Wanda masks of its matrices (from the undamped
     Hessian's diagonal, on the device), damping, the step size and the paper-
     mode solves. Tokens and weights are moved to the device before timing;
-    the reported time is the device time of all of that work."""
+    the reported time is the device time of all of that work. The step size
+    comes from the block iteration, or from Lanczos where the block iteration
+    has not converged within a few passes (spectral_step_size)."""
     import workloads
+    from paper_2512_13886_amd.pipeline import spectral_step_size
     total_ms = 0.0
     layers = {}
     streams = {}
@@ -122,7 +125,6 @@ def block_leg(L, torch, dev, precision) -> dict:
         H = torch.empty((d, d), dtype=torch.float32, device=dev)
         lam = torch.empty(1, dtype=torch.float32, device=dev)
         lmax = torch.empty(1, dtype=torch.float32, device=dev)
-        sp_it = torch.zeros(1, dtype=torch.int32, device=dev)
         V0 = torch.from_numpy(workloads.power_start_block(d, SPECTRAL_BLOCK)).to(dev)
         masks = [torch.empty((lc.n_cols, d), dtype=torch.uint8, device=dev) for lc in mats]
         outs = [torch.empty_like(w) for w in W0s]
@@ -144,7 +146,7 @@ def block_leg(L, torch, dev, precision) -> dict:
             L.optima_wanda_mask(W0d, H, M, L.MASK_UNSTRUCTURED, lc.sparsity, col_sq_stride=d + 1)
         ev[1].record()
         L.optima_hessian_damp(H, scfg.rel_damp, lam)
-        L.optima_spectral_norm(H, V0, lmax, max_iters=1000, tol=1e-6, iters=sp_it)
+        spec = spectral_step_size(H, V0, lmax)
         ev[2].record()
         infos = []
         for i, (lc, W0d, M, out, st) in enumerate(zip(mats, W0s, masks, outs, stats)):
@@ -155,7 +157,7 @@ def block_leg(L, torch, dev, precision) -> dict:
         total_ms += s_ms
         streams[sname] = {"d": d, "hessian_and_masks_ms": ev[0].elapsed_time(ev[1]),
                           "damp_spectral_ms": ev[1].elapsed_time(ev[2]),
-                          "spectral_passes": int(sp_it.item()), "ms": s_ms}
+                          "spectral": spec, "ms": s_ms}
         prev = ev[2]
         for i, (lc, st, inf) in enumerate(zip(mats, stats, infos)):
             layers[lc.name[len("block_"):]] = {
@@ -164,8 +166,8 @@ def block_leg(L, torch, dev, precision) -> dict:
                 "f_final_over_f_initial":
                     (st["f_final"].double().sum() / st["f_initial"].double().sum()).item()}
             prev = ev[3 + i]
-        log(f"block stream {sname}: {s_ms:.1f} ms ({streams[sname]['spectral_passes']} "
-            f"spectral passes)")
+        log(f"block stream {sname}: {s_ms:.1f} ms (step size: {spec['method']}, "
+            f"{spec['block_passes']} block passes, {spec['lanczos_steps']} Lanczos steps)")
         del Xd, H, hws, W0s, outs, masks, stats
         torch.cuda.empty_cache()
     cols = sum(v["columns"] for v in layers.values())
@@ -245,6 +247,7 @@ def main() -> int:
 
     import torch
     import paper_2512_13886_amd as L
+    from paper_2512_13886_amd.pipeline import spectral_step_size
     import workloads
 
     dev = torch.device("cuda:0")
@@ -386,7 +389,6 @@ def main() -> int:
     Hs.copy_(H)
     Ds = torch.empty(d, dtype=torch.float32, device=dev)
     lmax_s = torch.empty(1, dtype=torch.float32, device=dev)
-    sp_it = torch.zeros(1, dtype=torch.int32, device=dev)
     stats_d = {"iters": iters, "converged": conv, "f_initial": f_init, "f_final": f_fin}
 
     def timed_solve(Hm, lm, o):
@@ -403,7 +405,7 @@ def main() -> int:
     e[0].record()
     L.optima_hessian_jacobi(Hs, Ds)
     e[1].record()
-    L.optima_spectral_norm(Hs, V0d, lmax_s, max_iters=1000, tol=1e-6, ws=sws, iters=sp_it)
+    spec_s = spectral_step_size(Hs, V0d, lmax_s)
     e[2].record()
     torch.cuda.synchronize()
 
@@ -415,7 +417,7 @@ def main() -> int:
 
     tight = dict(eps_rel=1e-4, eps_abs=0.0, max_iters=20000)
     pre = {"scale_ms": e[0].elapsed_time(e[1]), "spectral_ms": e[1].elapsed_time(e[2]),
-           "spectral_passes": int(sp_it.item()),
+           "spectral": spec_s,
            "paper_tolerance": {
                "rapdhg_scaled": timed_solve(Hs, lmax_s, o_(col_scale=Ds)),
                "cg_scaled": timed_solve(Hs, None, o_(method=L.METHOD_CG, check_every=8,
@@ -428,7 +430,8 @@ def main() -> int:
                                                      col_scale=Ds, **tight))}}
     tt = pre["tight_tolerance_eps_rel_1e-4"]
     log(f"jacobi-preconditioned: scale {pre['scale_ms']:.2f} ms, spectral {pre['spectral_ms']:.2f} ms "
-        f"({pre['spectral_passes']} passes); tight: rapdhg {tt['rapdhg']['iterations']} -> "
+        f"({spec_s['method']}: {spec_s['block_passes']} block passes, "
+        f"{spec_s['lanczos_steps']} Lanczos steps); tight: rapdhg {tt['rapdhg']['iterations']} -> "
         f"{tt['rapdhg_scaled']['iterations']} it ({tt['rapdhg']['ms']:.1f} -> "
         f"{tt['rapdhg_scaled']['ms']:.1f} ms), cg {tt['cg']['iterations']} -> "
         f"{tt['cg_scaled']['iterations']} it ({tt['cg']['ms']:.1f} -> {tt['cg_scaled']['ms']:.1f} ms)")

@@ -4,8 +4,8 @@ For every layer, in order, on the device through the C ABI:
   1. H = X^T X over the calibration tokens X (the layer's inputs, already the
      outputs of the pruned layers before it);
   2. the Wanda mask from the undamped diagonal of H;
-  3. damping, the step size and the batched column QPs (paper tolerances
-     unless `opts` says otherwise);
+  3. damping, the step size (spectral_step_size below) and the batched
+     column QPs (paper tolerances unless `opts` says otherwise);
   4. the skip rule of Appendix D, read as: more than half of the columns
      unconverged, or sum f_final > sum f_initial. A skipped layer keeps the
      mask-only (Wanda) weights;
@@ -42,6 +42,35 @@ class LayerReport:
     def error_ratio(self) -> float:
         """MSE(Y_kept, Y_dense) / MSE(Y_wanda, Y_dense) (Section 4)."""
         return self.err_kept / self.err_wanda if self.err_wanda > 0 else float("nan")
+
+
+# Passes of the block iteration before the step size falls back to Lanczos.
+BLOCK_PASSES = 8
+
+
+def spectral_step_size(H: torch.Tensor, V0: torch.Tensor, lambda_max: torch.Tensor,
+                       block_passes: int = BLOCK_PASSES, tol_block: float = 1e-6,
+                       tol_lanczos: float = 1e-7) -> dict:
+    """lambda_max(H) for the solver's step size, into lambda_max (device).
+
+    Outlier channels put a cluster of eigenvalues far above the rest; the
+    block subspace iteration from the start block V0 [b, d] captures it and
+    converges in a handful of passes. Without such a gap (near-isotropic
+    inputs, or H after diagonal scaling) it crawls, and the Lanczos process
+    from V0[0] gets there in far fewer passes over H. So: at most
+    `block_passes` block passes, then Lanczos if they did not converge.
+    Returns {"method", "block_passes", "lanczos_steps"}.
+    """
+    it = torch.zeros(1, dtype=torch.int32, device=H.device)
+    L.optima_spectral_norm(H, V0, lambda_max, max_iters=block_passes, tol=tol_block, iters=it)
+    passes = int(it.item())
+    rep = {"method": "subspace", "block_passes": passes, "lanczos_steps": 0}
+    if passes >= block_passes:
+        st = torch.zeros(1, dtype=torch.int32, device=H.device)
+        v0 = V0[0] if V0.dim() == 2 else V0
+        L.optima_spectral_lanczos(H, v0.contiguous(), lambda_max, tol=tol_lanczos, steps=st)
+        rep.update(method="lanczos", lanczos_steps=int(st.item()))
+    return rep
 
 
 def skip_layer(converged: torch.Tensor, f_initial: torch.Tensor, f_final: torch.Tensor) -> bool:
@@ -82,7 +111,7 @@ def prune_chain(X0: torch.Tensor, weights: list, start: Callable[[int], torch.Te
         lam = torch.empty(1, dtype=torch.float32, device=dev)
         L.optima_hessian_damp(H, rel_damp, lam)
         lmax = torch.empty(1, dtype=torch.float32, device=dev)
-        L.optima_spectral_norm(H, start(d_in), lmax)
+        spectral_step_size(H, start(d_in), lmax)
         if timed:
             ev[1].record()
         W = torch.empty_like(W0)

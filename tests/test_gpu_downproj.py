@@ -59,6 +59,18 @@ def test_downproj_hessian_and_spectral_full_size(L):
     th, it_o = oracle.subspace_iteration(Hd, V0, 1000, 1e-6)
     log(f"  lambda_max gpu {float(lm.item()):.8e} ({it} it) oracle {th:.8e} ({it_o} it)")
     assert float(lm.item()) == pytest.approx(th, rel=2e-5)
+    # Lanczos on the same matrix: the oracle's Lanczos value within 1e-5, and
+    # no lower than the block iteration's Ritz value (the spectrum has no gap
+    # at the top, so the block iteration stops short of lambda_max).
+    v0 = workloads.power_start(CFG.d)
+    lz = torch.empty(1, dtype=torch.float32, device=dev())
+    st = torch.zeros(1, dtype=torch.int32, device=dev())
+    L.optima_spectral_lanczos(H, to_dev(v0), lz, tol=1e-7, steps=st)
+    thz, st_o = oracle.lanczos(Hd, v0, 256, 1e-7)
+    log(f"  lanczos gpu {float(lz.item()):.8e} ({int(st.item())} steps) "
+        f"oracle {thz:.8e} ({st_o} steps)")
+    assert float(lz.item()) == pytest.approx(thz, rel=1e-5)
+    assert float(lz.item()) >= float(lm.item()) * (1 - 2e-6)
 
 
 @pytest.fixture(scope="module")
