@@ -1,0 +1,91 @@
+"""The benchmark's q_proj step at full size, checked on sampled outputs.
+
+The step is the one bench.py times:
+* H from all 262144 bf16 tokens (Student-t, 8 outlier channels);
+* damping;
+* the block-16 step size;
+* the paper-mode rAPDHG solve of 4096 columns under the 2:4 Wanda mask, with the 2:4-sparse
+  bf16x3 products.
+
+The oracle cannot redo the whole layer in seconds. It takes the device's damped H (fp32 values,
+copied back) and recomputes:
+* the step size;
+* the paper-mode solve of sampled columns, from the same H and lambda_max.
+
+The sampled columns are the ones that stop at each check, including every column of the
+few-column phase. Both sides must stop at the same check on nearly every sampled column and,
+where they do, agree to the W and objective bars.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from gpu_util import dev, to_dev, to_dev_x, gpu_solve, rel_fro, log
+
+pytestmark = pytest.mark.gpu
+
+CFG = workloads.Q_PROJ
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2512_13886_amd as lib_mod  # fails loudly when the library is missing
+    return lib_mod
+
+
+def test_qproj_full_step_sampled(L):
+    log("q_proj step: generating 262144 x 4096 bf16 tokens")
+    X = workloads.x_all(CFG)
+    W0 = workloads.w0(CFG)
+    M = workloads.layer_mask(CFG, W0, workloads.col_sq_norms(CFG, X))
+    Xd = to_dev_x(X)
+    del X
+    H = torch.empty((CFG.d, CFG.d), dtype=torch.float32, device=dev())
+    L.optima_hessian_accumulate(Xd, H)
+    del Xd
+    lam = torch.empty(1, dtype=torch.float32, device=dev())
+    L.optima_hessian_damp(H, CFG.rel_damp, lam)
+    V0 = workloads.power_start_block(CFG.d, 16)
+    lm = torch.empty(1, dtype=torch.float32, device=dev())
+    it = torch.zeros(1, dtype=torch.int32, device=dev())
+    L.optima_spectral_norm(H, to_dev(V0), lm, max_iters=1000, tol=1e-6, iters=it)
+    Wg, st, info = gpu_solve(L, H, lm, W0, M, L.SolverOpts.default())
+    assert info["sparse_products"] == 1
+    Hd = H.cpu().numpy().astype(np.float64)
+    lam_g = float(lm.item())
+
+    th, it_o = oracle.subspace_iteration(Hd, V0, 1000, 1e-6)
+    log(f"  lambda_max gpu {lam_g:.8e} ({int(it.item())} passes) oracle {th:.8e} ({it_o})")
+    assert lam_g == pytest.approx(th, rel=2e-6)
+
+    # Every column converges, pruned entries are +0.0 and no column ends above
+    # its start objective.
+    Wg = Wg.cpu().numpy()
+    assert st["converged"].all()
+    assert np.all(Wg[M == 0].view(np.uint32) == 0)
+    assert np.all(st["f_final"] <= st["f_initial"] * (1 + 1e-6))
+
+    # Sampled columns: up to 8 from each stopping check, all of the longest.
+    rng = np.random.default_rng(7)
+    cols = []
+    for k in np.unique(st["iters"]):
+        idx = np.flatnonzero(st["iters"] == k)
+        take = idx if k == st["iters"].max() else rng.choice(idx, min(8, idx.size), replace=False)
+        cols.extend(int(c) for c in take)
+    cols = np.array(sorted(set(cols)))
+    log(f"  checks {dict(zip(*np.unique(st['iters'], return_counts=True)))}; "
+        f"{cols.size} sampled columns")
+    r = oracle.rapdhg(Hd, W0[cols], M[cols], lam_g, oracle.SolverOptions())
+    same = r.iters == st["iters"][cols]
+    log(f"  same stopping check on {same.sum()}/{cols.size}")
+    assert same.mean() >= 0.9
+    assert r.converged.all()
+    w_rel = rel_fro(Wg[cols][same], r.W[same])
+    fg = oracle.objective(Hd, W0[cols], Wg[cols])[same]
+    fo = oracle.objective(Hd, W0[cols], r.W)[same]
+    f_rel = float(np.max(np.abs(fg - fo) / np.abs(fo)))
+    log(f"  W rel_fro {w_rel:.3e}, max f rel {f_rel:.3e}")
+    assert w_rel <= 1e-4
+    assert f_rel <= 1e-5
