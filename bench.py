@@ -90,8 +90,16 @@ def cpu_baseline(cfg, X, W0, mask, sample_cols: int, sample_chunks: int) -> dict
     t_solve = time.perf_counter() - t0
     job_s = (t_hess * cfg.n_chunks / sample_chunks + t_pow
              + t_solve * cfg.n_cols / sample_cols)
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in fh
+                              if ln.startswith("model name")), "")
+    except OSError:  # pragma: no cover
+        pass
     return {
         "value": cfg.n_cols / job_s, "unit": "columns/s", "cores": int(threads),
+        "affinity_cores": len(os.sched_getaffinity(0)), "cpu_model": cpu_model,
         "kind": "oracle",
         "sample": (f"fp64 NumPy oracle: Hessian over {sample_chunks} of {cfg.n_chunks} "
                    f"2048-token sequences (time scaled x{cfg.n_chunks // sample_chunks}), "

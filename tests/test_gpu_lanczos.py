@@ -156,3 +156,28 @@ def test_lanczos_without_a_gap_needs_fewer_passes(L):
     assert lam_l == pytest.approx(top, rel=1e-5)
     assert st_l < it_s
     assert 10 * abs(lam_l - top) < abs(lam_s - top)
+
+
+def test_lanczos_maximum_steps_and_more_steps_than_rows(L):
+    # 256 steps (the largest basis and coefficient arrays, the last
+    # coefficient block of 64 waves): H = diag(1..2 evenly over 8192 values),
+    # stored dense, whose top Ritz value is still rising at step 256.
+    d = 8192
+    Hin = np.diag(np.linspace(1.0, 2.0, d)).astype(np.float32)
+    rng = np.random.default_rng(12)
+    v0 = rng.standard_normal(d).astype(np.float32)
+    lam_g, st_g = gpu_lanczos(L, to_dev(Hin), v0, max_steps=L.LANCZOS_MAX_STEPS, tol=0.0)
+    lam_o, st_o = oracle.lanczos(Hin.astype(np.float64), v0, L.LANCZOS_MAX_STEPS, 0.0)
+    log(f"  256 steps: gpu {lam_g:.9e} ({st_g}) oracle {lam_o:.9e} ({st_o})")
+    assert st_g == st_o == L.LANCZOS_MAX_STEPS
+    assert lam_g == pytest.approx(lam_o, rel=2e-6)
+    assert 2.0 * (1 - 1e-5) < lam_g <= 2.0 * (1 + 1e-7)
+    # max_steps above d: the run ends by d steps (the Krylov space is then the
+    # whole space, or invariant earlier) at lambda_max.
+    d = 40
+    Hs = f32_exact((lambda A: A @ A.T + np.eye(d))(rng.standard_normal((d, d))))
+    lam_g, st_g = gpu_lanczos(L, to_dev(Hs), rng.standard_normal(d).astype(np.float32),
+                              max_steps=L.LANCZOS_MAX_STEPS, tol=0.0)
+    log(f"  d=40: gpu {lam_g:.9e} ({st_g} steps)")
+    assert st_g <= d
+    assert lam_g == pytest.approx(np.linalg.eigvalsh(Hs)[-1], rel=2e-6)
