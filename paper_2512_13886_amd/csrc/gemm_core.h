@@ -128,6 +128,9 @@ using Tile128 = TileCfg<128, 128, 2, 2, 2>;
 // The 128 x 128 tile with 8 waves: two K groups of 4 waves of 64 x 64 over
 // 256-byte stages (two waves per SIMD with one workgroup per CU).
 using Tile128K2 = TileCfg<128, 128, 2, 2, 2, 2, 256>;
+// The 256 x 128 tile with 8 waves of 64 x 64 (4 x 2) and two 128-byte stage
+// buffers: a quarter fewer operand bytes per flop than the 128 x 128 tile.
+using Tile256 = TileCfg<256, 128, 4, 2, 2>;
 
 // Rows of the tile that this thread's direct loads fetch: A round i covers
 // A tile row load_row<Cfg>(i), B round i covers B tile row load_row<Cfg>(i);

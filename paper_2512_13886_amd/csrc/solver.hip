@@ -341,6 +341,85 @@ __global__ void __launch_bounds__(ProductTile::kThreads) k_product(ProductArgs p
   }
 }
 
+// The dense products on 256 x 128 tiles of 8 waves, one workgroup per CU,
+// for long contractions (d >= kWideMinDim): a quarter fewer operand bytes per
+// flop than the 128 x 128 tile, whose loads from L2 bound it there. The 128
+// KiB accumulator tile is staged for the epilogue through the two 64 KiB
+// buffers in the layout of the sparse tile (same 4 x 2 waves of 64 x 64).
+// Split ranges, partial sums and the epilogue work as in k_product, with
+// partial rows padded to the 256-row tile.
+using WideTile = Tile256;
+constexpr int kWideStageBytes = 65536;
+constexpr int kWideMinDim = 8192;
+constexpr int kWideMinRows = 256;
+
+template <int MODE, int PREC>
+__global__ void __launch_bounds__(WideTile::kThreads) k_product_wide(ProductArgs p, int splits,
+                                                                     float* part) {
+  using Cfg = WideTile;
+  static_assert(Cfg::MB == SpTile::MB && Cfg::NB == SpTile::NB && Cfg::WGN == SpTile::WGN &&
+                    Cfg::kThreads == SpTile::kThreads && Cfg::BM == SpTile::BM &&
+                    Cfg::BN == SpTile::BN,
+                "accumulator layout of the sparse tile");
+  static_assert(Cfg::kBufBytes <= kWideStageBytes, "stage buffers");
+  __shared__ __attribute__((aligned(1024))) char lds0[kWideStageBytes];
+  __shared__ __attribute__((aligned(1024))) char lds1[kWideStageBytes];
+  const int tiles_m = (p.n_rows + Cfg::BM - 1) / Cfg::BM;
+  const int tiles_n = p.dp / Cfg::BN;
+  const int n_tiles = tiles_m * tiles_n;
+  const int lin = blockIdx.x % n_tiles;
+  const int sp = blockIdx.x / n_tiles;
+  int tm, tn;
+  tile_of_block(lin, n_tiles, tiles_m, tiles_n, &tm, &tn);
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  const int stages = p.dp * 4 / Cfg::SRB;
+  const int s0 = int(int64_t(stages) * sp / splits);
+  const int s1 = int(int64_t(stages) * (sp + 1) / splits);
+
+  Operands<Cfg> src;
+  const size_t k_off = size_t(s0) * Cfg::SRB;
+  const char* a_base = PREC == kPrecBf16x3 ? reinterpret_cast<const char*>(p.Ap)
+                                           : reinterpret_cast<const char*>(p.A);
+  const char* b_base = PREC == kPrecBf16x3 ? reinterpret_cast<const char*>(p.Bp)
+                                           : reinterpret_cast<const char*>(p.B);
+#pragma unroll
+  for (int i = 0; i < Cfg::kLoadsA; ++i) {
+    int r = m0 + load_row<Cfg>(i);
+    r = r < p.n_rows ? r : p.n_rows - 1;
+    const int j = p.rows ? p.rows[r] : r;
+    src.a[i] = a_base + size_t(j) * p.dp * 4 + k_off + load_seg_bytes<Cfg>(i);
+  }
+#pragma unroll
+  for (int i = 0; i < Cfg::kLoadsB; ++i)
+    src.b[i] = b_base + size_t(n0 + load_row<Cfg>(i)) * p.dp * 4 + k_off + load_seg_bytes<Cfg>(i);
+  f4 acc[Cfg::MB][Cfg::NB];
+  if (PREC == kPrecBf16x3)
+    gemm_tile_mainloop<Cfg, Bf16x3Tag>(acc, src, s1 - s0, lds0, lds1, nullptr);
+  else
+    gemm_tile_mainloop<Cfg, float>(acc, src, s1 - s0, lds0, lds1, nullptr);
+
+  sp_stage_tile(acc, lds0, lds1);
+  __syncthreads();
+  const float L = (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f;
+  float* P = part + size_t(sp) * size_t(tiles_m) * Cfg::BM * size_t(p.dp);
+  constexpr int kChunks = Cfg::BM * Cfg::BN / 4;
+#pragma unroll 4
+  for (int q = 0; q < kChunks / Cfg::kThreads; ++q) {
+    const int c = threadIdx.x + Cfg::kThreads * q;  // 16-byte chunk of the tile
+    const int r = c >> 5, ch = c & 31;
+    const int rg = m0 + r;
+    if (rg >= p.n_rows) continue;
+    const float4 y = sp_staged_chunk(lds0, lds1, r, ch);
+    const int n = n0 + 4 * ch;
+    if (splits > 1) {
+      st4(P + size_t(rg) * p.dp + n, y);
+      continue;
+    }
+    const int j = p.rows ? p.rows[rg] : rg;
+    epilogue4<MODE, PREC>(p, j, n, y, row_coef<MODE>(p, j, L));
+  }
+}
+
 // The iteration products with x 2:4-compressed (kPrecSparse): 256 x 128
 // tiles of 8 waves on the sparse MFMA, one workgroup per CU (132 KiB of
 // LDS). Split ranges, partial sums and the epilogue work as in k_product,
@@ -1441,6 +1520,25 @@ optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t 
       hipLaunchKernelGGL((k_product_skinny<MODE, PREC>), dim3(unsigned(p.dp / kSkinnyHRows)),
                          dim3(64 * kSkinnyWaves), 0, s, p);
       OPTIMA_LAUNCH_CHECK();
+      return OPTIMA_OK;
+    }
+  }
+  if constexpr (PREC == kPrecBf16x3) {
+    if (p.dp >= kWideMinDim && p.n_rows >= kWideMinRows) {
+      const int tiles_m = int(ceil_div(p.n_rows, WideTile::BM));
+      const int tiles_n = p.dp / WideTile::BN;
+      const int rows_pad = tiles_m * WideTile::BM;
+      const int S = choose_splits_one_per_cu(tiles_m * tiles_n, p.dp * 4 / WideTile::SRB,
+                                             rows_pad, p.dp, l.part_elems);
+      hipLaunchKernelGGL((k_product_wide<MODE, PREC>), dim3(tiles_m * tiles_n * S),
+                         dim3(WideTile::kThreads), 0, s, p, S, l.part);
+      OPTIMA_LAUNCH_CHECK();
+      if (S > 1) {
+        const dim3 g(unsigned(p.n_rows), unsigned(ceil_div(p.dp, 4 * kThreads)));
+        hipLaunchKernelGGL((k_split_epilogue<MODE, PREC>), g, dim3(kThreads), 0, s, p, S,
+                           rows_pad, static_cast<const float*>(l.part));
+        OPTIMA_LAUNCH_CHECK();
+      }
       return OPTIMA_OK;
     }
   }
