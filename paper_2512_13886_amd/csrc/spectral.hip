@@ -22,6 +22,11 @@
 // the next pass. Directions whose Cholesky pivot falls below 1e-14 of their
 // diagonal are numerically dependent and are dropped (their rows and columns
 // of the factor's inverse are zero).
+//
+// Lanczos (optima_spectral_lanczos): the largest Ritz value of the Krylov
+// space of one start vector, from the tridiagonal matrix of the symmetric
+// Lanczos recurrence with full reorthogonalisation; one HBM-bound GEMV over H
+// per step plus small latency-bound kernels (described with them below).
 #include "common.h"
 
 namespace optima {
