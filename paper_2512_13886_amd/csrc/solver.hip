@@ -26,6 +26,8 @@
 //   f(x) = f(x0) + (x - x0)^T (H x + H x0 - 2 H w0)
 // (x - x0 vanishes off the kept set), with g0 = H x0 - H w0 packed into the
 // second half of Hx_ag's row.
+#include <atomic>
+
 #include "common.h"
 #include "gemm_core.h"
 
@@ -1435,17 +1437,19 @@ Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
   return l;
 }
 
+// CU count of the current device, queried once per device. Calls from
+// several host threads may race to fill an entry; they store the same value.
 int device_cu_count() {
-  static int cache[64] = {0};
+  static std::atomic<int> cache[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (!cache[dev]) {
-    int n = 0;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
       n = 256;
-    cache[dev] = n;
+    cache[dev].store(n, std::memory_order_relaxed);
   }
-  return cache[dev];
+  return n;
 }
 
 // Number of K ranges for a product over `tiles` output tiles: splitting pays
