@@ -1,6 +1,7 @@
-"""The benchmark's q_proj step at full size, checked on sampled outputs.
+"""Whole layer steps at full size, checked on sampled outputs.
 
-The step is the one bench.py times:
+q_proj is the step bench.py times; GPT-2 fc runs the same sequence on the dense (non-2:4) product
+path under a 50 % unstructured mask. The q_proj step is:
 * H from all 262144 bf16 tokens (Student-t, 8 outlier channels);
 * damping;
 * the block-16 step size;
@@ -12,8 +13,8 @@ copied back) and recomputes:
 * the step size;
 * the paper-mode solve of sampled columns, from the same H and lambda_max.
 
-The sampled columns are the ones that stop at each check, including every column of the
-few-column phase. Both sides must stop at the same check on nearly every sampled column and,
+The sampled columns come from every stopping check: up to 8 from each, up to 32 from the last
+(on q_proj that is every column of the few-column phase). Both sides must stop at the same check on nearly every sampled column and,
 where they do, agree to the W and objective bars.
 """
 import numpy as np
@@ -26,8 +27,6 @@ from gpu_util import dev, to_dev, to_dev_x, gpu_solve, rel_fro, log
 
 pytestmark = pytest.mark.gpu
 
-CFG = workloads.Q_PROJ
-
 
 @pytest.fixture(scope="module")
 def L():
@@ -35,8 +34,9 @@ def L():
     return lib_mod
 
 
-def test_qproj_full_step_sampled(L):
-    log("q_proj step: generating 262144 x 4096 bf16 tokens")
+@pytest.mark.parametrize("CFG", [workloads.Q_PROJ, workloads.GPT2_FC], ids=lambda c: c.name)
+def test_full_step_sampled(L, CFG):
+    log(f"{CFG.name} step: generating {CFG.n_tok} x {CFG.d} tokens")
     X = workloads.x_all(CFG)
     W0 = workloads.w0(CFG)
     M = workloads.layer_mask(CFG, W0, workloads.col_sq_norms(CFG, X))
@@ -52,7 +52,7 @@ def test_qproj_full_step_sampled(L):
     it = torch.zeros(1, dtype=torch.int32, device=dev())
     L.optima_spectral_norm(H, to_dev(V0), lm, max_iters=1000, tol=1e-6, iters=it)
     Wg, st, info = gpu_solve(L, H, lm, W0, M, L.SolverOpts.default())
-    assert info["sparse_products"] == 1
+    assert info["sparse_products"] == (1 if CFG.mask_kind == "2:4" else 0)
     Hd = H.cpu().numpy().astype(np.float64)
     lam_g = float(lm.item())
 
@@ -67,13 +67,13 @@ def test_qproj_full_step_sampled(L):
     assert np.all(Wg[M == 0].view(np.uint32) == 0)
     assert np.all(st["f_final"] <= st["f_initial"] * (1 + 1e-6))
 
-    # Sampled columns: up to 8 from each stopping check, all of the longest.
+    # Sampled columns: up to 8 from each stopping check, up to 32 of the longest.
     rng = np.random.default_rng(7)
     cols = []
     for k in np.unique(st["iters"]):
         idx = np.flatnonzero(st["iters"] == k)
-        take = idx if k == st["iters"].max() else rng.choice(idx, min(8, idx.size), replace=False)
-        cols.extend(int(c) for c in take)
+        n = 32 if k == st["iters"].max() else 8
+        cols.extend(int(c) for c in rng.choice(idx, min(n, idx.size), replace=False))
     cols = np.array(sorted(set(cols)))
     log(f"  checks {dict(zip(*np.unique(st['iters'], return_counts=True)))}; "
         f"{cols.size} sampled columns")
