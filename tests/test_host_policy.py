@@ -4,8 +4,17 @@ import numpy as np
 import pytest
 import torch
 
-import paper_2512_13886_amd as L
-from paper_2512_13886_amd import pipeline
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2512_13886_amd as lib_mod  # fails loudly when the library is missing
+    return lib_mod
+
+
+@pytest.fixture(scope="module")
+def pipeline(L):
+    from paper_2512_13886_amd import pipeline as mod
+    return mod
 
 
 class _FakeSpectral:
@@ -27,7 +36,7 @@ class _FakeSpectral:
 
 
 @pytest.mark.parametrize("passes,method", [(4, "subspace"), (7, "subspace"), (8, "lanczos")])
-def test_step_size_falls_back_to_lanczos(monkeypatch, passes, method):
+def test_step_size_falls_back_to_lanczos(monkeypatch, pipeline, passes, method):
     fake = _FakeSpectral(passes)
     monkeypatch.setattr(pipeline.L, "optima_spectral_norm", fake.norm)
     monkeypatch.setattr(pipeline.L, "optima_spectral_lanczos", fake.lanczos)
@@ -47,7 +56,7 @@ def test_step_size_falls_back_to_lanczos(monkeypatch, passes, method):
     assert rep["block_passes"] == min(passes, pipeline.BLOCK_PASSES)
 
 
-def test_skip_rule():
+def test_skip_rule(pipeline):
     ones = torch.ones(10, dtype=torch.uint8)
     f0 = torch.ones(10)
     assert not pipeline.skip_layer(ones, f0, f0 * 0.5)
@@ -63,7 +72,7 @@ def test_skip_rule():
                                    torch.zeros(0))
 
 
-def test_binding_rejects_host_tensors_before_any_call():
+def test_binding_rejects_host_tensors_before_any_call(L):
     H = torch.zeros(8, 8)
     lam = torch.zeros(1)
     with pytest.raises(ValueError, match="device tensor"):
