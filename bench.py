@@ -248,7 +248,7 @@ def main() -> int:
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        log("bench.py measures one MI355X only: this build runs the hot path on a single GPU "
+        log("bench.py measures one MI355X only: the library runs the hot path on a single GPU "
             "(columns would shard across GPUs with no per-iteration communication). "
             "Run it with --gpus 1.")
         return 2
