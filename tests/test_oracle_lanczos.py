@@ -116,3 +116,17 @@ def test_lanczos_beats_subspace_iteration_without_a_gap():
     assert th == pytest.approx(3.0, rel=1e-6)
     sub, passes = oracle.subspace_iteration(H, workloads.power_start_block(400, 16), steps, 1e-10)
     assert passes == steps and abs(sub - 3.0) > 10 * abs(th - 3.0)
+
+
+def test_lanczos_change_test_tolerance_without_a_gap():
+    # Evenly spread spectrum: the Ritz value keeps rising by small amounts
+    # long before it converges, so the change test at tol 1e-6 stops about
+    # 1e-5 short of lambda_max, and tol 1e-7 (the step-size default) within
+    # 1e-6 of it.
+    d = 2048
+    H = np.diag(np.linspace(1.0, 3.0, d))
+    v0 = np.random.default_rng(5).standard_normal(d)
+    th6, _ = oracle.lanczos(H, v0, 256, 1e-6)
+    th7, _ = oracle.lanczos(H, v0, 256, 1e-7)
+    assert (3.0 - th6) / 3.0 > 5e-6
+    assert 0.0 <= (3.0 - th7) / 3.0 < 1e-6
