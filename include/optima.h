@@ -296,7 +296,7 @@ optima_status optima_linear_forward(const void* X, int64_t n_tok, int64_t d_in,
  * depend on the others in the batch (Algorithm 1 batching).
  *
  * H: [d][d] fp32, symmetric, 16-byte aligned. lambda_max: device float (from
- * optima_spectral_norm or the caller). W_out: [n_cols][d] fp32, must not
+ * optima_spectral_norm, optima_spectral_lanczos or the caller). W_out: [n_cols][d] fp32, must not
  * overlap W0. stats (host struct of device arrays, may be NULL; each array may
  * be NULL): per column iterations run, accepted restarts, convergence flag,
  * objective at the start point sel(mask, w0, 0), objective and KKT of W_out
