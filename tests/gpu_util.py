@@ -72,3 +72,53 @@ def f32_exact(H64: np.ndarray) -> np.ndarray:
 
 def log(msg: str):
     print(msg, flush=True)
+
+
+def paper_mode_parity(Hd: np.ndarray, W0: np.ndarray, M: np.ndarray, Wg: np.ndarray, st: dict,
+                      lam: float, per_check: int = 8, last: int = 32, seed: int = 7,
+                      label: str = "") -> None:
+    """A paper-mode solve on the device against the oracle's on sampled columns.
+
+    Samples up to `per_check` columns of every stopping check and up to `last`
+    of the last one, solves them with the oracle from the same H (fp64 values
+    of the device's fp32 matrix) and lambda_max, and requires the same stopping
+    check on at least 90 % of them and, where it agrees, W within 1e-4
+    (relative Frobenius) and every objective within 1e-5.
+    """
+    import oracle
+    rng = np.random.default_rng(seed)
+    cols = []
+    for k in np.unique(st["iters"]):
+        idx = np.flatnonzero(st["iters"] == k)
+        n = last if k == st["iters"].max() else per_check
+        cols.extend(int(c) for c in rng.choice(idx, min(n, idx.size), replace=False))
+    cols = np.array(sorted(set(cols)))
+    r = oracle.rapdhg(Hd, W0[cols], M[cols], lam, oracle.SolverOptions())
+    same = r.iters == st["iters"][cols]
+    w_rel = rel_fro(Wg[cols][same], r.W[same])
+    fg = oracle.objective(Hd, W0[cols], Wg[cols])[same]
+    fo = oracle.objective(Hd, W0[cols], r.W)[same]
+    f_rel = float(np.max(np.abs(fg - fo) / np.abs(fo)))
+    log(f"  {label}: checks {dict(zip(*np.unique(st['iters'], return_counts=True)))}; same check "
+        f"on {same.sum()}/{cols.size} sampled; W rel_fro {w_rel:.3e}, max f rel {f_rel:.3e}")
+    assert same.mean() >= 0.9
+    assert r.converged.all()
+    assert w_rel <= 1e-4
+    assert f_rel <= 1e-5
+
+
+def check_step_size(Hd: np.ndarray, V0: np.ndarray, rep: dict, lam: float, block_passes: int,
+                    label: str = "") -> None:
+    """lambda_max from the step-size policy against the oracle's run of the
+    method the policy took (the block iteration where it converged within its
+    passes, else Lanczos from the block's first vector)."""
+    import oracle
+    if rep["method"] == "subspace":
+        th, n_o = oracle.subspace_iteration(Hd, V0, block_passes, 1e-6)
+        n_g, rel = rep["block_passes"], 2e-6
+    else:
+        th, n_o = oracle.lanczos(Hd, V0[0], 256, 1e-7)
+        n_g, rel = rep["lanczos_steps"], 1e-5
+    log(f"  {label} lambda_max gpu {lam:.8e} ({rep['method']}, {n_g}) oracle {th:.8e} ({n_o})")
+    assert abs(lam - th) <= rel * abs(th)
+    assert abs(n_g - n_o) <= 2

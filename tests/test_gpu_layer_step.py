@@ -22,9 +22,9 @@ import numpy as np
 import pytest
 import torch
 
-import oracle
 import workloads
-from gpu_util import dev, to_dev, to_dev_x, gpu_solve, rel_fro, log
+from gpu_util import (dev, to_dev, to_dev_x, gpu_solve, paper_mode_parity, check_step_size,
+                      log)
 
 pytestmark = pytest.mark.gpu
 
@@ -59,17 +59,7 @@ def test_full_step_sampled(L, CFG):
     del H
     lam_g = float(lm.item())
 
-    # The step size against the oracle's run of the method the policy took:
-    # the block iteration where it converged within its passes, else Lanczos.
-    if rep["method"] == "subspace":
-        th, n_o = oracle.subspace_iteration(Hd, V0, BLOCK_PASSES, 1e-6)
-        n_g = rep["block_passes"]
-    else:
-        th, n_o = oracle.lanczos(Hd, V0[0], 256, 1e-7)
-        n_g = rep["lanczos_steps"]
-    log(f"  lambda_max gpu {lam_g:.8e} ({rep['method']}, {n_g}) oracle {th:.8e} ({n_o})")
-    assert lam_g == pytest.approx(th, rel=1e-5 if rep["method"] == "lanczos" else 2e-6)
-    assert abs(n_g - n_o) <= 2
+    check_step_size(Hd, V0, rep, lam_g, BLOCK_PASSES, label=CFG.name)
 
     # Every column converges, pruned entries are +0.0 and no column ends above
     # its start objective.
@@ -78,25 +68,4 @@ def test_full_step_sampled(L, CFG):
     assert np.all(Wg[M == 0].view(np.uint32) == 0)
     assert np.all(st["f_final"] <= st["f_initial"] * (1 + 1e-6))
 
-    # Sampled columns: up to 8 from each stopping check, up to 32 of the longest.
-    rng = np.random.default_rng(7)
-    cols = []
-    for k in np.unique(st["iters"]):
-        idx = np.flatnonzero(st["iters"] == k)
-        n = 32 if k == st["iters"].max() else 8
-        cols.extend(int(c) for c in rng.choice(idx, min(n, idx.size), replace=False))
-    cols = np.array(sorted(set(cols)))
-    log(f"  checks {dict(zip(*np.unique(st['iters'], return_counts=True)))}; "
-        f"{cols.size} sampled columns")
-    r = oracle.rapdhg(Hd, W0[cols], M[cols], lam_g, oracle.SolverOptions())
-    same = r.iters == st["iters"][cols]
-    log(f"  same stopping check on {same.sum()}/{cols.size}")
-    assert same.mean() >= 0.9
-    assert r.converged.all()
-    w_rel = rel_fro(Wg[cols][same], r.W[same])
-    fg = oracle.objective(Hd, W0[cols], Wg[cols])[same]
-    fo = oracle.objective(Hd, W0[cols], r.W)[same]
-    f_rel = float(np.max(np.abs(fg - fo) / np.abs(fo)))
-    log(f"  W rel_fro {w_rel:.3e}, max f rel {f_rel:.3e}")
-    assert w_rel <= 1e-4
-    assert f_rel <= 1e-5
+    paper_mode_parity(Hd, W0, M, Wg, st, lam_g, label=CFG.name)
