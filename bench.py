@@ -90,6 +90,32 @@ def cpu_baseline(cfg, X, W0, mask, sample_cols: int, sample_chunks: int) -> dict
     t_solve = time.perf_counter() - t0
     job_s = (t_hess * cfg.n_chunks / sample_chunks + t_pow
              + t_solve * cfg.n_cols / sample_cols)
+    # The same work on one thread (BLAS limited to one), on a smaller sample:
+    # one sequence for the Hessian and 16 columns for the solve.
+    one = None
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            oracle.hessian([workloads.x_to_f64(X[:cfg.chunk])])
+            t1_hess = time.perf_counter() - t0
+            t0 = time.perf_counter()
+            oracle.subspace_iteration(H, workloads.power_start_block(cfg.d, SPECTRAL_BLOCK),
+                                      1000, 1e-6)
+            t1_pow = time.perf_counter() - t0
+            cols1 = cols[np.linspace(0, cols.size - 1, 16).astype(int)]
+            t0 = time.perf_counter()
+            oracle.rapdhg(H, W0[cols1], mask[cols1], lam, oracle.SolverOptions())
+            t1_solve = time.perf_counter() - t0
+        one = {"value": cfg.n_cols / (t1_hess * cfg.n_chunks + t1_pow
+                                      + t1_solve * cfg.n_cols / cols1.size),
+               "cores": 1,
+               "sample": (f"one thread: Hessian over 1 sequence (time scaled x{cfg.n_chunks}), "
+                          f"the same subspace iteration, rAPDHG on {cols1.size} of the sampled "
+                          f"columns (time scaled x{cfg.n_cols // cols1.size}); measured "
+                          f"{t1_hess + t1_pow + t1_solve:.1f} s")}
+    except ImportError:  # pragma: no cover
+        pass
     cpu_model = ""
     try:
         with open("/proc/cpuinfo") as fh:
@@ -107,6 +133,7 @@ def cpu_baseline(cfg, X, W0, mask, sample_cols: int, sample_chunks: int) -> dict
                    f"{cfg.n_cols} columns (time scaled x{cfg.n_cols // sample_cols}; "
                    f"max {int(r.iters.max())} iterations); measured "
                    f"{t_hess + t_pow + t_solve:.1f} s of CPU work"),
+        "one_thread": one,
     }
 
 
