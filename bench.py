@@ -253,7 +253,7 @@ def chain_leg(L, torch, dev, precision) -> dict:
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-cols", type=int, default=256)
@@ -357,6 +357,7 @@ def main() -> int:
     hess_ms = np.mean([e[0].elapsed_time(e[1]) for e, _ in recs])
     spec_ms = np.mean([e[1].elapsed_time(e[2]) for e, _ in recs])
     solve_ms = np.mean([e[2].elapsed_time(e[3]) for e, _ in recs])
+    solve_ms_median = float(np.median([e[2].elapsed_time(e[3]) for e, _ in recs]))
     it = np.mean([i["iterations"] for _, i in recs])
     col_it = np.mean([i["row_products"] for _, i in recs])
     all_launches = sum(i["timed_launches"] for _, i in recs)
@@ -628,6 +629,8 @@ def main() -> int:
         "column_iters_per_s": col_it / (solve_ms * 1e-3),
         "iterations": it,
         "phase_ms": {"hessian": hess_ms, "damp_spectral": spec_ms, "solve": solve_ms},
+        "solve_only": {"solve_ms_median": solve_ms_median, "runs": args.steps,
+                       "columns_per_s": C / (solve_ms_median * 1e-3)},
         "hessian_tflops": 2.0 * N * d * d / 2 / (hess_ms * 1e-3) / 1e12,
         "fixed_batch": fixed_batch,
         "mask_select": mask_select,
