@@ -49,9 +49,9 @@ SPECTRAL_BLOCK = 16
 
 # HBM traffic of the product kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (profiles/), valid only for the kernel sources they were taken on.
-TRAFFIC = {"sources_sha1": "cc4aa8ae3cf9e2d9554ef7d6096da2c9d2250999",
-           "bytes_per_launch": 276918 * 1024,       # k_product_sparse<fused|store>
-           "few_bytes_per_launch": 67073 * 1024}    # k_product_skinny_sparse<fused|store>
+TRAFFIC = {"sources_sha1": "83031e9020184cd01698e8f93ad9f1123919a061",
+           "bytes_per_launch": 276962 * 1024,       # k_product_sparse<fused|store>
+           "few_bytes_per_launch": 67072 * 1024}    # k_product_skinny_sparse<fused|store>
 
 
 def log(msg: str):

@@ -12,6 +12,7 @@
 // d_in). Epilogue per 4 consecutive outputs: the squared difference to a
 // reference Z (fp64 partial sums), the activation and the store.
 #include "common.h"
+#include "readback.h"
 #include "gemm_core.h"
 
 namespace optima {
@@ -150,8 +151,7 @@ optima_status linear_forward(const void* X, int64_t n_tok, int64_t d_in, const f
                      d_in, l.Wb, l.flags);
   OPTIMA_LAUNCH_CHECK();
   int flag = 0;
-  OPTIMA_HIP_TRY(hipMemcpyAsync(&flag, l.flags, sizeof(int), hipMemcpyDeviceToHost, s));
-  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  OPTIMA_HIP_TRY(read_back(&flag, l.flags, sizeof(int), s));
   if (flag) return OPTIMA_E_NONFINITE;
   if (n_tok == 0) {
     if (err_out) OPTIMA_HIP_TRY(hipMemsetAsync(err_out, 0, sizeof(double), s));

@@ -29,6 +29,7 @@
 #include <atomic>
 
 #include "common.h"
+#include "readback.h"
 #include "gemm_core.h"
 
 namespace optima {
@@ -1646,8 +1647,7 @@ optima_status cg_loop(const Layout& l, ProductArgs p, int dp, int di, const uint
                        l.n_active);
     OPTIMA_LAUNCH_CHECK();
     std::swap(rows, rows_next);
-    OPTIMA_HIP_TRY(hipMemcpyAsync(&n_act, l.n_active, sizeof(int), hipMemcpyDeviceToHost, s));
-    OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+    OPTIMA_HIP_TRY(read_back(&n_act, l.n_active, sizeof(int), s));
     if (timed) {
       float ms = 0.f;
       OPTIMA_HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));
@@ -1723,8 +1723,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     OPTIMA_LAUNCH_CHECK();
   }
   int flags[3] = {0, 0, 0};
-  OPTIMA_HIP_TRY(hipMemcpyAsync(flags, l.flags, 3 * sizeof(int), hipMemcpyDeviceToHost, s));
-  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  OPTIMA_HIP_TRY(read_back(flags, l.flags, 3 * sizeof(int), s));
   if (flags[0]) return OPTIMA_E_NONFINITE;
   const bool sparse = try_sparse && !flags[1];
   const int iprec = sparse ? int(kPrecSparse) : o.precision;
@@ -1825,8 +1824,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
                      l.rows0, l.n_active);
   OPTIMA_LAUNCH_CHECK();
   int n_act = 0;
-  OPTIMA_HIP_TRY(hipMemcpyAsync(&n_act, l.n_active, sizeof(int), hipMemcpyDeviceToHost, s));
-  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  OPTIMA_HIP_TRY(read_back(&n_act, l.n_active, sizeof(int), s));
   if (sparse && n_act > 0) {
     hipLaunchKernelGGL(k_pack, dim3(unsigned(n_act)), dim3(kThreads), 0, s, l.rows0, n_act, dp,
                        l.SLOT, l.X0, l.XA, l.HX, l.HA, l.HW0);
@@ -1920,8 +1918,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
                        l.n_active);
     OPTIMA_LAUNCH_CHECK();
     std::swap(rows, rows_next);
-    OPTIMA_HIP_TRY(hipMemcpyAsync(&n_act, l.n_active, sizeof(int), hipMemcpyDeviceToHost, s));
-    OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+    OPTIMA_HIP_TRY(read_back(&n_act, l.n_active, sizeof(int), s));
     if (info) {
       float ms = 0.f;
       OPTIMA_HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));

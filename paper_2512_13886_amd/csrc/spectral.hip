@@ -28,6 +28,7 @@
 // Lanczos recurrence with full reorthogonalisation; one HBM-bound GEMV over H
 // per step plus small latency-bound kernels (described with them below).
 #include "common.h"
+#include "readback.h"
 
 namespace optima {
 namespace {
@@ -879,8 +880,7 @@ optima_status power_iteration(const float* H, int64_t d, const float* v0, int ma
     OPTIMA_LAUNCH_CHECK();
     if (it % kPoll == 0 && it < max_iters) {
       int conv = 0;
-      OPTIMA_HIP_TRY(hipMemcpyAsync(&conv, &st->conv, sizeof(int), hipMemcpyDeviceToHost, s));
-      OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+      OPTIMA_HIP_TRY(read_back(&conv, &st->conv, sizeof(int), s));
       if (conv) break;
     }
   }
@@ -893,7 +893,7 @@ optima_status power_iteration(const float* H, int64_t d, const float* v0, int ma
     hipLaunchKernelGGL(k_copy_iters, dim3(1), dim3(1), 0, s, st, iters);
     OPTIMA_LAUNCH_CHECK();
   }
-  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  OPTIMA_HIP_TRY(wait_stream(s));
   return OPTIMA_OK;
 }
 
@@ -935,8 +935,7 @@ optima_status subspace_iteration(const float* H, int64_t d, const float* V0, int
     OPTIMA_LAUNCH_CHECK();
     if (it % kPoll == 0 && it < max_iters) {
       int conv = 0;
-      OPTIMA_HIP_TRY(hipMemcpyAsync(&conv, &st->conv, sizeof(int), hipMemcpyDeviceToHost, s));
-      OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+      OPTIMA_HIP_TRY(read_back(&conv, &st->conv, sizeof(int), s));
       if (conv) break;
     }
   }
@@ -944,7 +943,7 @@ optima_status subspace_iteration(const float* H, int64_t d, const float* V0, int
     hipLaunchKernelGGL(k_copy_sub_iters, dim3(1), dim3(1), 0, s, st, iters);
     OPTIMA_LAUNCH_CHECK();
   }
-  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  OPTIMA_HIP_TRY(wait_stream(s));
   return OPTIMA_OK;
 }
 
@@ -1023,8 +1022,7 @@ optima_status spectral_lanczos(const float* H, int64_t d, const float* v0, int m
     OPTIMA_LAUNCH_CHECK();
     if ((j + 1) % kPoll == 0 && j + 1 < m) {
       int conv = 0;
-      OPTIMA_HIP_TRY(hipMemcpyAsync(&conv, &l.st->conv, sizeof(int), hipMemcpyDeviceToHost, s));
-      OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+      OPTIMA_HIP_TRY(read_back(&conv, &l.st->conv, sizeof(int), s));
       if (conv) break;
     }
   }
@@ -1032,7 +1030,7 @@ optima_status spectral_lanczos(const float* H, int64_t d, const float* v0, int m
     hipLaunchKernelGGL(k_copy_lz_steps, dim3(1), dim3(1), 0, s, l.st, steps);
     OPTIMA_LAUNCH_CHECK();
   }
-  OPTIMA_HIP_TRY(hipStreamSynchronize(s));
+  OPTIMA_HIP_TRY(wait_stream(s));
   return OPTIMA_OK;
 }
 
