@@ -7,8 +7,9 @@ from .optima_oracle import (hessian, damp, jacobi_scale, power_iteration, subspa
                             wanda_mask,
                             objective,
                             closed_form, kkt_solve, cg, rapdhg, check_decision,
+                            anchor_terms, termination,
                             SolverOptions, SolveResult)
 
 __all__ = ["hessian", "damp", "jacobi_scale", "power_iteration", "subspace_iteration", "lanczos", "wanda_mask", "objective",
            "closed_form",
-           "kkt_solve", "cg", "rapdhg", "check_decision", "SolverOptions", "SolveResult"]
+           "kkt_solve", "cg", "rapdhg", "check_decision", "anchor_terms", "termination", "SolverOptions", "SolveResult"]

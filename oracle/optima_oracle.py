@@ -86,7 +86,8 @@ rapdhg           Section 3.3 / 3.4: the batched restarted accelerated
                  progress (KKT <= 0.8 KKT_restart and KKT > KKT_previous check),
                  or when the inner loop is long (k >= 0.36 t); it is accepted
                  only if it does not raise the objective above the last
-                 restart point's.
+                 restart point's. At max_iters every active column stops at
+                 its candidate; no restart is applied or counted there.
 
 Parity status
 -------------
@@ -405,6 +406,34 @@ def _score(H, W0, keep, Z, D=None):
     return {"rd": rd, "gap": gap, "kkt": np.hypot(rd, gap), "f": f, "zHz": zHz}
 
 
+def anchor_terms(H, W0, D=None):
+    """Per-row quantities of the termination test that depend on the anchors
+    only: H w0 (rows), c_norm = ||2 H w0||_2 (the gradient of Eq. (6) at
+    w = 0, in the original coordinates when a scaling D is given) and
+    w0^T H w0 (the constant of the QP form of Eq. (6))."""
+    Hw0 = W0 @ H
+    c_norm = np.linalg.norm(2.0 * (Hw0 if D is None else Hw0 / D[None, :]), axis=1)
+    w0Hw0 = np.sum(W0 * Hw0, axis=1)
+    return Hw0, c_norm, w0Hw0
+
+
+def termination(s: dict, c_norm, w0Hw0, opts: SolverOptions):
+    """Appendix D test of scored rows s (from _score): returns (converged, P, D).
+
+    P = f(z) is the primal objective. D = w0^T H w0 - z^T H z is the dual
+    objective of the QP form 1/2 z^T Q z + c^T z + w0^T H w0 (Q = 2H,
+    c = -2 H w0) with bounds only: -1/2 z^T Q z plus the constant, the bound
+    terms vanishing because every bound is 0. P - D = z^T g, so the gap
+    |z^T g| is |P - D|. A row passes when r_d <= eps_abs + eps_rel c_norm and
+    gap <= eps_abs + eps_rel (|P| + |D|).
+    """
+    P = s["f"]
+    D = w0Hw0 - s["zHz"]
+    conv = ((s["rd"] <= opts.eps_abs + opts.eps_rel * c_norm)
+            & (s["gap"] <= opts.eps_abs + opts.eps_rel * (np.abs(P) + np.abs(D))))
+    return conv, P, D
+
+
 def check_decision(s_x: dict, s_a: dict, kkt_restart, kkt_prev, f_anchor, k, t,
                    c_norm, w0Hw0, opts: SolverOptions):
     """Candidate choice, termination test and restart test at one check.
@@ -413,10 +442,7 @@ def check_decision(s_x: dict, s_a: dict, kkt_restart, kkt_prev, f_anchor, k, t,
     """
     use_x = s_x["kkt"] < s_a["kkt"]  # ties go to the average
     s_c = {key: np.where(use_x, s_x[key], s_a[key]) for key in s_x}
-    P = s_c["f"]
-    D = -s_c["zHz"] + w0Hw0
-    converged = ((s_c["rd"] <= opts.eps_abs + opts.eps_rel * c_norm)
-                 & (s_c["gap"] <= opts.eps_abs + opts.eps_rel * (np.abs(P) + np.abs(D))))
+    converged, _, _ = termination(s_c, c_norm, w0Hw0, opts)
     kc = s_c["kkt"]
     cond = ((kc <= opts.beta_sufficient * kkt_restart)
             | ((kc <= opts.beta_necessary * kkt_restart) & (kc > kkt_prev))
@@ -448,9 +474,7 @@ def cg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, opts: SolverOptions | No
     n, d = W0.shape
 
     x = np.where(keep, W0, 0.0)
-    Hw0 = W0 @ H
-    c_norm = np.linalg.norm(2.0 * (Hw0 if D is None else Hw0 / D[None, :]), axis=1)
-    w0Hw0 = np.sum(W0 * Hw0, axis=1)
+    Hw0, c_norm, w0Hw0 = anchor_terms(H, W0, D)
     r = np.where(keep, Hw0 - x @ H, 0.0)
     p = r.copy()
     rr = np.sum(r * r, axis=1)
@@ -462,10 +486,7 @@ def cg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, opts: SolverOptions | No
 
     def test(Z):
         s = _score(H, W0, keep, Z, D)
-        primal, dual = s["f"], -s["zHz"] + w0Hw0
-        conv = ((s["rd"] <= opts.eps_abs + opts.eps_rel * c_norm)
-                & (s["gap"] <= opts.eps_abs + opts.eps_rel * (np.abs(primal) + np.abs(dual))))
-        return s, conv
+        return s, termination(s, c_norm, w0Hw0, opts)[0]
 
     def finish(rows, s, t, conv):
         out["W"][rows] = (x if D is None else x * D[None, :])[rows]
@@ -535,9 +556,7 @@ def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
 
     x = sel(W0)
     xa = x.copy()
-    Hw0 = W0 @ H
-    c_norm = np.linalg.norm(2.0 * (Hw0 if D is None else Hw0 / D[None, :]), axis=1)
-    w0Hw0 = np.sum(W0 * Hw0, axis=1)
+    _, c_norm, w0Hw0 = anchor_terms(H, W0, D)
 
     k = np.zeros(n, dtype=np.int64)
     done = np.zeros(n, dtype=bool)
@@ -561,10 +580,9 @@ def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
         out["kkt_final"][rows] = s["kkt"][rows]
         done[rows] = True
 
-    # Termination test at the start point (all-kept or all-pruned columns).
-    P0, D0 = s0["f"], -s0["zHz"] + w0Hw0
-    conv0 = ((s0["rd"] <= opts.eps_abs + opts.eps_rel * c_norm)
-             & (s0["gap"] <= opts.eps_abs + opts.eps_rel * (np.abs(P0) + np.abs(D0))))
+    # Termination test at the start point (all-kept or all-pruned columns, or
+    # a start that already meets the tolerances).
+    conv0, _, _ = termination(s0, c_norm, w0Hw0, opts)
     if opts.max_iters <= 0:
         finish(np.ones(n, dtype=bool), x, s0, 0, conv0)
     elif not opts.fixed_iters:
@@ -596,6 +614,11 @@ def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
             stop = act & conv
             finish(stop, cand, s_c, t, conv)
             act = act & ~stop
+        if t == opts.max_iters:
+            # The iteration budget ends here: every active column stops at its
+            # candidate, and a restart that would never run is not counted.
+            finish(act, cand, s_c, t, conv)
+            break
         acc = act & restart
         x[acc] = cand[acc]
         xa[acc] = cand[acc]
@@ -606,8 +629,6 @@ def rapdhg(H: np.ndarray, W0: np.ndarray, mask: np.ndarray, lambda_max: float,
         for j in np.flatnonzero(acc):
             anchors[j].append(float(s_c["f"][j]))
         kkt_prev[act] = s_c["kkt"][act]
-        if t == opts.max_iters:
-            finish(act, cand, s_c, t, conv)
 
     return SolveResult(W=out["W"], iters=out["iters"], restarts=out["restarts"],
                        converged=out["converged"], f_initial=f_initial,

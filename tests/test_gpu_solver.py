@@ -96,6 +96,44 @@ def test_trajectory_before_first_check(L, T, prec):
     assert np.all(st["iters"] == T)
 
 
+@pytest.mark.parametrize("prec", PRECISIONS)
+@pytest.mark.parametrize("T", [8, 16, 24])
+def test_restarts_and_final_kkt_match_oracle(L, T, prec):
+    # Fixed mode with a check every 8 iterations: every check before T takes
+    # restart decisions (PDLP-style decay tests and the monotone safeguard)
+    # from the scores r_d, gap and KKT, and the final check reports the KKT of
+    # the candidate. Per column the device's restart count must equal the
+    # oracle's, and its final KKT must agree within a bound derived from the
+    # arithmetic: with g = 2 H (x - w0),
+    #   |dKKT| <= |d r_d| + |d gap| <= (1 + ||x||) ||dg|| + ||dx|| ||g||,
+    #   ||dg|| <= 2 ||H||_2 ||dx|| + 2 eps (|| |H| |x| || + || |H| |w0| ||),
+    # where dx is the measured difference of the two outputs (the trajectories
+    # round differently) and eps the relative error of one H-product (fp32:
+    # d 2^-24; bf16x3: 3 2^-16 plus that), doubled for the maintained sums.
+    cfg = workloads.TINY
+    H, W0, M, lam = _oracle_layer(cfg)
+    o = oracle.rapdhg(H, W0, M, lam,
+                      oracle.SolverOptions(max_iters=T, fixed_iters=True, check_every=8))
+    Wg, st, _ = gpu_solve(L, to_dev(H), to_dev(np.array([lam])), W0, M,
+                          _opts(L, max_iters=T, fixed_iters=1, check_every=8, precision=prec))
+    Wg = Wg.cpu().numpy().astype(np.float64)
+    d = cfg.d
+    eps = d * 2.0 ** -24 + (3 * 2.0 ** -16 if prec == 1 else 0.0)
+    absH = np.abs(H)
+    hnorm = float(np.linalg.eigvalsh(H)[-1])
+    dx = np.linalg.norm(Wg - o.W, axis=1)
+    prod = np.linalg.norm(np.abs(o.W) @ absH, axis=1) + np.linalg.norm(np.abs(W0) @ absH, axis=1)
+    dg = 2.0 * hnorm * dx + 4.0 * eps * prod
+    g = 2.0 * (o.W - W0) @ H
+    tol = (1.0 + np.linalg.norm(o.W, axis=1)) * dg + dx * np.linalg.norm(g, axis=1)
+    err = np.abs(st["kkt_final"].astype(np.float64) - o.kkt_final)
+    log(f"  T={T}: restarts {np.bincount(o.restarts)}; kkt_final max rel err "
+        f"{np.max(err / o.kkt_final):.2e}, max err / bound {np.max(err / tol):.2e}")
+    np.testing.assert_array_equal(st["restarts"], o.restarts)
+    assert np.all(err <= tol + 2.0 ** -23 * o.kkt_final)
+    assert np.all(st["iters"] == T)
+
+
 def test_paper_mode_tiny(L):
     cfg = workloads.TINY
     H, W0, M, lam = _oracle_layer(cfg)
