@@ -142,11 +142,19 @@ def _need_cuda(name, t, dtype=None):
         raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
 
 
-def _workspace(nbytes: int, ws, device):
+def _workspace(nbytes: int, ws, device, stream=None):
+    """The caller's workspace, or a new one allocated on the stream the call
+    runs on. torch's caching allocator ties a block to the stream it was
+    allocated on, so the block freed when the call returns is handed only to
+    later work on that stream, which runs after the library's kernels."""
     if ws is not None:
         _need_cuda("ws", ws)
         return ws, ws.numel() * ws.element_size()
-    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device), int(nbytes)
+    n = max(int(nbytes), 1)
+    if stream is None:
+        return torch.empty(n, dtype=torch.uint8, device=device), int(nbytes)
+    with torch.cuda.stream(stream):
+        return torch.empty(n, dtype=torch.uint8, device=device), int(nbytes)
 
 
 @dataclass
@@ -201,7 +209,8 @@ def optima_hessian_accumulate(X: torch.Tensor, H: torch.Tensor, accumulate: bool
     if dtype is None:
         raise ValueError("X must be float32 or bfloat16")
     n_tok, d = X.shape
-    ws, nbytes = _workspace(optima_hessian_workspace_bytes(n_tok, d, dtype), ws, X.device)
+    ws, nbytes = _workspace(optima_hessian_workspace_bytes(n_tok, d, dtype), ws, X.device,
+                           stream)
     _check(_hess_acc(_ptr(X), dtype, n_tok, d, _ptr(H), int(bool(accumulate)), _ptr(ws),
                      nbytes, _stream(stream)))
 
@@ -249,7 +258,8 @@ def optima_spectral_norm(H: torch.Tensor, V0: torch.Tensor, lambda_max: torch.Te
         raise ValueError("V0 must be [d] or [block, d]")
     if V0.shape[-1] != d:
         raise ValueError("V0 vectors must have length d")
-    ws, nbytes = _workspace(optima_spectral_norm_workspace_bytes(d, block), ws, H.device)
+    ws, nbytes = _workspace(optima_spectral_norm_workspace_bytes(d, block), ws, H.device,
+                           stream)
     _check(_spec(_ptr(H), d, _ptr(V0), int(block), int(max_iters), float(tol), _ptr(ws), nbytes,
                  _ptr(lambda_max), _ptr(iters), _stream(stream)))
 
@@ -274,7 +284,8 @@ def optima_spectral_lanczos(H: torch.Tensor, v0: torch.Tensor, lambda_max: torch
     d = H.shape[0]
     if v0.dim() != 1 or v0.shape[0] != d:
         raise ValueError("v0 must be [d]")
-    ws, nbytes = _workspace(optima_spectral_lanczos_workspace_bytes(d, max_steps), ws, H.device)
+    ws, nbytes = _workspace(optima_spectral_lanczos_workspace_bytes(d, max_steps), ws, H.device,
+                           stream)
     _check(_lz(_ptr(H), d, _ptr(v0), int(max_steps), float(tol), _ptr(ws), nbytes,
                _ptr(lambda_max), _ptr(steps), _stream(stream)))
 
@@ -316,7 +327,7 @@ def optima_linear_forward(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor | No
     if err_out is not None:
         _need_cuda("err_out", err_out, torch.float64)
     ws, nbytes = _workspace(optima_linear_forward_workspace_bytes(n_tok, d_in, d_out), ws,
-                            W.device)
+                            W.device, stream)
     empty = n_tok == 0  # an empty tensor may report a null address
     _check(_fwd(None if empty else _ptr(X), n_tok, d_in, _ptr(W), d_out, int(act),
                 None if empty else _ptr(Y), y_dtype, None if empty else _ptr(Y_ref),
@@ -378,7 +389,7 @@ def optima_qp_solve_batched(H: torch.Tensor, lambda_max: torch.Tensor | None, W0
         _need_cuda("opts.col_scale", opts.col_scale, torch.float32)
         if opts.col_scale.numel() != d:
             raise ValueError("opts.col_scale must have d entries")
-    ws, nbytes = _workspace(optima_qp_workspace_bytes(d, n_cols), ws, W0.device)
+    ws, nbytes = _workspace(optima_qp_workspace_bytes(d, n_cols), ws, W0.device, stream)
     st = _Stats()
     kinds = {"iters": torch.int32, "restarts": torch.int32, "converged": torch.uint8,
              "f_initial": torch.float32, "f_final": torch.float32, "kkt_final": torch.float32}
