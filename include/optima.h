@@ -174,6 +174,30 @@ optima_status optima_spectral_norm(const float* H, int64_t d, const float* V0,
                                    int32_t* iters, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * optima_spectral_norm for callers that cannot allocate memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, iterations, results and blocking behaviour as
+ * optima_spectral_norm, without `ws`: the work buffer is a fixed array of
+ * OPTIMA_SPECTRAL_NOALLOC_SCRATCH_BYTES inside the library, one copy per
+ * device, held from the library's load until the process ends. It covers
+ * every block size for d <= OPTIMA_SPECTRAL_NOALLOC_MAX_DIM; a larger d
+ * returns OPTIMA_E_WORKSPACE before any launch. The call allocates nothing
+ * (no device memory, no pinned host memory): its convergence polls copy into
+ * host stack memory and synchronise `stream`. The first call on a device
+ * looks up the array's device address once (hipGetSymbolAddress).
+ * Every call on a device shares that device's array and leaves its contents
+ * there: calls that overlap on one device (two streams, or two host threads)
+ * race on it and must be serialised by the caller. Calls on different
+ * devices are independent.
+ * ------------------------------------------------------------------------- */
+#define OPTIMA_SPECTRAL_NOALLOC_MAX_DIM 16384
+#define OPTIMA_SPECTRAL_NOALLOC_SCRATCH_BYTES (8454144)
+optima_status optima_spectral_norm_noalloc(const float* H, int64_t d, const float* V0,
+                                           int block, int max_iters, float tol,
+                                           float* lambda_max, int32_t* iters,
+                                           hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * The same lambda_max (the step size of Section 3.3's first-order solver) by
  * the symmetric Lanczos process with full reorthogonalisation. Step j builds
  * q_j of an orthonormal basis of the Krylov space span{v0, H v0, ...,

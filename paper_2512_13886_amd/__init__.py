@@ -13,6 +13,7 @@ from ._lib import (OptimaError, SolverOpts, DTYPE_F32, DTYPE_BF16, DTYPE_F64, PR
                    optima_hessian_damp, optima_hessian_jacobi,
                    optima_spectral_norm_workspace_bytes,
                    optima_spectral_norm, LANCZOS_MAX_STEPS,
+                   SPECTRAL_NOALLOC_MAX_DIM, optima_spectral_norm_noalloc,
                    optima_spectral_lanczos_workspace_bytes, optima_spectral_lanczos,
                    optima_wanda_mask, optima_qp_workspace_bytes,
                    optima_qp_solve_batched, ACT_NONE, ACT_SILU,
@@ -25,6 +26,7 @@ __all__ = [
     "optima_status_string", "optima_abi_version", "optima_hessian_workspace_bytes",
     "optima_hessian_accumulate", "optima_hessian_damp", "optima_hessian_jacobi",
     "optima_spectral_norm_workspace_bytes", "optima_spectral_norm", "LANCZOS_MAX_STEPS",
+    "SPECTRAL_NOALLOC_MAX_DIM", "optima_spectral_norm_noalloc",
     "optima_spectral_lanczos_workspace_bytes", "optima_spectral_lanczos", "optima_wanda_mask",
     "optima_qp_workspace_bytes", "optima_qp_solve_batched", "ACT_NONE", "ACT_SILU",
     "optima_linear_forward_workspace_bytes", "optima_linear_forward",

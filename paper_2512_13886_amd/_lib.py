@@ -90,6 +90,8 @@ _jacobi = _sig("optima_hessian_jacobi", _i32, [_vp, _i64, _vp, _vp])
 _spec_ws = _sig("optima_spectral_norm_workspace_bytes", _sz, [_i64, _i32])
 _spec = _sig("optima_spectral_norm", _i32,
              [_vp, _i64, _vp, _i32, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
+_spec_na = _sig("optima_spectral_norm_noalloc", _i32,
+                [_vp, _i64, _vp, _i32, _i32, _f32, _vp, _vp, _vp])
 _lz_ws = _sig("optima_spectral_lanczos_workspace_bytes", _sz, [_i64, _i32])
 _lz = _sig("optima_spectral_lanczos", _i32,
            [_vp, _i64, _vp, _i32, _f32, _vp, _sz, _vp, _vp, _vp])
@@ -262,6 +264,28 @@ def optima_spectral_norm(H: torch.Tensor, V0: torch.Tensor, lambda_max: torch.Te
                            stream)
     _check(_spec(_ptr(H), d, _ptr(V0), int(block), int(max_iters), float(tol), _ptr(ws), nbytes,
                  _ptr(lambda_max), _ptr(iters), _stream(stream)))
+
+
+SPECTRAL_NOALLOC_MAX_DIM = 16384
+
+
+def optima_spectral_norm_noalloc(H: torch.Tensor, V0: torch.Tensor, lambda_max: torch.Tensor,
+                                 max_iters: int = 1000, tol: float = 1e-6,
+                                 iters: torch.Tensor | None = None, stream=None) -> None:
+    """optima_spectral_norm with the library's fixed per-device work array
+    instead of a workspace: nothing is allocated (d <= SPECTRAL_NOALLOC_MAX_DIM;
+    calls that overlap on one device race on that array)."""
+    _need_cuda("H", H, torch.float32)
+    _need_cuda("V0", V0, torch.float32)
+    _need_cuda("lambda_max", lambda_max, torch.float32)
+    if iters is not None:
+        _need_cuda("iters", iters, torch.int32)
+    d = H.shape[0]
+    if V0.dim() not in (1, 2) or V0.shape[-1] != d:
+        raise ValueError("V0 must be [d] or [block, d]")
+    block = 1 if V0.dim() == 1 else V0.shape[0]
+    _check(_spec_na(_ptr(H), d, _ptr(V0), int(block), int(max_iters), float(tol),
+                    _ptr(lambda_max), _ptr(iters), _stream(stream)))
 
 
 LANCZOS_MAX_STEPS = 256

@@ -12,6 +12,9 @@ size_t spectral_norm_workspace_bytes(int64_t d, int block);
 optima_status spectral_norm(const float* H, int64_t d, const float* V0, int block, int max_iters,
                             float tol, void* ws, float* lambda_max, int32_t* iters,
                             hipStream_t s);
+optima_status spectral_norm_noalloc(const float* H, int64_t d, const float* V0, int block,
+                                    int max_iters, float tol, float* lambda_max, int32_t* iters,
+                                    hipStream_t s);
 size_t spectral_lanczos_workspace_bytes(int64_t d, int max_steps);
 optima_status spectral_lanczos(const float* H, int64_t d, const float* v0, int max_steps,
                                float tol, void* ws, float* lambda_max, int32_t* steps,
@@ -111,6 +114,19 @@ optima_status optima_spectral_norm(const float* H, int64_t d, const float* V0, i
   if (!ws || ws_bytes < optima::spectral_norm_workspace_bytes(d, block))
     return OPTIMA_E_WORKSPACE;
   return optima::spectral_norm(H, d, V0, block, max_iters, tol, ws, lambda_max, iters, stream);
+}
+
+optima_status optima_spectral_norm_noalloc(const float* H, int64_t d, const float* V0, int block,
+                                           int max_iters, float tol, float* lambda_max,
+                                           int32_t* iters, hipStream_t stream) {
+  if (!H || !V0 || !lambda_max || d < 1 || d > kMaxDim || max_iters < 1 || !(tol >= 0.f))
+    return OPTIMA_E_INVAL;
+  if (block < 1 || block > OPTIMA_SPECTRAL_MAX_BLOCK) return OPTIMA_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(V0) & 3) || (reinterpret_cast<uintptr_t>(H) & 3))
+    return OPTIMA_E_INVAL;
+  if (d > OPTIMA_SPECTRAL_NOALLOC_MAX_DIM) return OPTIMA_E_WORKSPACE;
+  return optima::spectral_norm_noalloc(H, d, V0, block, max_iters, tol, lambda_max, iters,
+                                       stream);
 }
 
 size_t optima_spectral_lanczos_workspace_bytes(int64_t d, int max_steps) {

@@ -144,4 +144,15 @@ inline hipError_t read_back(void* dst, const void* src, size_t bytes, hipStream_
   return hipSuccess;
 }
 
+// The same two waits without the pinned mailbox, for calls that may not
+// allocate: the copy lands in the caller's host memory and the stream is
+// synchronised (a longer wake-up, no allocation).
+inline hipError_t read_back_plain(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  hipError_t e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return e;
+  return hipStreamSynchronize(s);
+}
+
+inline hipError_t wait_stream_plain(hipStream_t s) { return hipStreamSynchronize(s); }
+
 }  // namespace optima

@@ -28,6 +28,8 @@
 // Lanczos recurrence with full reorthogonalisation; one HBM-bound GEMV over H
 // per step plus small latency-bound kernels (described with them below).
 #include "common.h"
+#include <mutex>
+
 #include "readback.h"
 
 namespace optima {
@@ -858,7 +860,8 @@ size_t spectral_norm_workspace_bytes(int64_t d, int block) {
 namespace {
 
 optima_status power_iteration(const float* H, int64_t d, const float* v0, int max_iters, float tol,
-                              void* ws, float* lambda_max, int32_t* iters, hipStream_t s) {
+                              void* ws, float* lambda_max, int32_t* iters, bool plain_waits,
+                              hipStream_t s) {
   Carver c(ws);
   float* buf[2] = {c.take<float>(size_t(d)), c.take<float>(size_t(d))};
   const int nblk = int(ceil_div(d, kRowsPerBlock));
@@ -880,7 +883,8 @@ optima_status power_iteration(const float* H, int64_t d, const float* v0, int ma
     OPTIMA_LAUNCH_CHECK();
     if (it % kPoll == 0 && it < max_iters) {
       int conv = 0;
-      OPTIMA_HIP_TRY(read_back(&conv, &st->conv, sizeof(int), s));
+      OPTIMA_HIP_TRY(plain_waits ? read_back_plain(&conv, &st->conv, sizeof(int), s)
+                                 : read_back(&conv, &st->conv, sizeof(int), s));
       if (conv) break;
     }
   }
@@ -893,13 +897,13 @@ optima_status power_iteration(const float* H, int64_t d, const float* v0, int ma
     hipLaunchKernelGGL(k_copy_iters, dim3(1), dim3(1), 0, s, st, iters);
     OPTIMA_LAUNCH_CHECK();
   }
-  OPTIMA_HIP_TRY(wait_stream(s));
+  OPTIMA_HIP_TRY(plain_waits ? wait_stream_plain(s) : wait_stream(s));
   return OPTIMA_OK;
 }
 
 optima_status subspace_iteration(const float* H, int64_t d, const float* V0, int b,
                                  int max_iters, float tol, void* ws, float* lambda_max,
-                                 int32_t* iters, hipStream_t s) {
+                                 int32_t* iters, bool plain_waits, hipStream_t s) {
   const int64_t dpp = round_up(d, kSubRows);
   const int nblk = int(dpp / kSubRows);
   Carver c(ws);
@@ -935,7 +939,8 @@ optima_status subspace_iteration(const float* H, int64_t d, const float* V0, int
     OPTIMA_LAUNCH_CHECK();
     if (it % kPoll == 0 && it < max_iters) {
       int conv = 0;
-      OPTIMA_HIP_TRY(read_back(&conv, &st->conv, sizeof(int), s));
+      OPTIMA_HIP_TRY(plain_waits ? read_back_plain(&conv, &st->conv, sizeof(int), s)
+                                 : read_back(&conv, &st->conv, sizeof(int), s));
       if (conv) break;
     }
   }
@@ -943,7 +948,7 @@ optima_status subspace_iteration(const float* H, int64_t d, const float* V0, int
     hipLaunchKernelGGL(k_copy_sub_iters, dim3(1), dim3(1), 0, s, st, iters);
     OPTIMA_LAUNCH_CHECK();
   }
-  OPTIMA_HIP_TRY(wait_stream(s));
+  OPTIMA_HIP_TRY(plain_waits ? wait_stream_plain(s) : wait_stream(s));
   return OPTIMA_OK;
 }
 
@@ -979,8 +984,70 @@ LzLayout lz_layout(void* ws, int64_t d, int m, size_t* bytes) {
 optima_status spectral_norm(const float* H, int64_t d, const float* V0, int block, int max_iters,
                             float tol, void* ws, float* lambda_max, int32_t* iters,
                             hipStream_t s) {
-  if (block == 1) return power_iteration(H, d, V0, max_iters, tol, ws, lambda_max, iters, s);
-  return subspace_iteration(H, d, V0, block, max_iters, tol, ws, lambda_max, iters, s);
+  if (block == 1)
+    return power_iteration(H, d, V0, max_iters, tol, ws, lambda_max, iters, false, s);
+  return subspace_iteration(H, d, V0, block, max_iters, tol, ws, lambda_max, iters, false, s);
+}
+
+// ---------------------------------------------------------------------------
+// The spectral norm without allocation: the work buffer is `scratch`, a
+// fixed array of the library's code object (one copy per device, kept until
+// the process ends), and the host waits land in host stack memory.
+// ---------------------------------------------------------------------------
+namespace {
+
+// Covers spectral_norm_workspace_bytes(d, block) for every d <=
+// OPTIMA_SPECTRAL_NOALLOC_MAX_DIM and block <= kMaxBlock: two blocks of 16
+// fp32 vectors (2 MiB at d = 16384), the fp64 partial Gram sums of 16-row
+// slabs (6 MiB) and a few KiB of sums and state.
+constexpr size_t kScratchBytes = OPTIMA_SPECTRAL_NOALLOC_SCRATCH_BYTES;
+static_assert(kScratchBytes == (size_t(8) << 20) + (size_t(64) << 10), "scratch size");
+constexpr int kScratchDevices = 64;
+
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+// Device address of `scratch` per device. In host code the array's name is
+// only a host-side stand-in for the symbol; its device address comes from
+// hipGetSymbolAddress, looked up once per device with that device current.
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices];
+
+hipError_t scratch_for(hipStream_t s, void** out) {
+  int dev = 0;
+  hipError_t e = hipStreamGetDevice(s, &dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = 0;
+    if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+optima_status spectral_norm_noalloc(const float* H, int64_t d, const float* V0, int block,
+                                    int max_iters, float tol, float* lambda_max, int32_t* iters,
+                                    hipStream_t s) {
+  if (d > OPTIMA_SPECTRAL_NOALLOC_MAX_DIM ||
+      spectral_norm_workspace_bytes(d, block) > kScratchBytes)
+    return OPTIMA_E_WORKSPACE;
+  void* ws = nullptr;
+  OPTIMA_HIP_TRY(scratch_for(s, &ws));
+  // The iterations initialise every piece of the buffer they read, so the
+  // contents left by an earlier call need no clearing.
+  if (block == 1)
+    return power_iteration(H, d, V0, max_iters, tol, ws, lambda_max, iters, true, s);
+  return subspace_iteration(H, d, V0, block, max_iters, tol, ws, lambda_max, iters, true, s);
 }
 
 size_t spectral_lanczos_workspace_bytes(int64_t d, int max_steps) {
