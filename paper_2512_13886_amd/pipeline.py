@@ -37,6 +37,9 @@ class LayerReport:
     err_kept: float       # sum of squared output errors of the kept weights vs dense
     err_wanda: float      # the same for the mask-only weights
     ms: dict = field(default_factory=dict)
+    # per-column statistics of the solve (host arrays): iters, converged,
+    # f_initial, f_final
+    columns: dict = field(default_factory=dict)
 
     @property
     def error_ratio(self) -> float:
@@ -145,9 +148,10 @@ def prune_chain(X0: torch.Tensor, weights: list, start: Callable[[int], torch.Te
             ev[4].record()
         del Y_dense, fws
         e = errs.cpu().tolist()
+        cols = {k: v.cpu().numpy() for k, v in stats.items()}
         rep = LayerReport(d_in=d_in, d_out=d_out, iterations=int(info["iterations"]),
-                          converged=int(stats["converged"].cpu().sum().item()), skipped=skipped,
-                          err_kept=e[0], err_wanda=e[1])
+                          converged=int(cols["converged"].sum()), skipped=skipped,
+                          err_kept=e[0], err_wanda=e[1], columns=cols)
         if timed:
             torch.cuda.synchronize()
             rep.ms = {"hessian_mask_step": ev[0].elapsed_time(ev[1]),

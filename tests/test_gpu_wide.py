@@ -68,7 +68,9 @@ def test_wide_tight_reaches_closed_form_and_fp32(L, problem):
     Wb, _, _ = gpu_solve(L, Hd, lm, W0, M, L.SolverOpts.default(precision=L.PREC_BF16X3, **opts))
     Wf, _, _ = gpu_solve(L, Hd, lm, W0, M, L.SolverOpts.default(precision=L.PREC_FP32, **opts))
     Wb, Wf = Wb.cpu().numpy(), Wf.cpu().numpy()
-    cols = np.array([0, 123, 299])
+    # 32 columns spread over both row tiles, the ragged second one included.
+    cols = np.unique(np.linspace(0, N_COLS - 1, 32).astype(int))
+    assert cols.size == 32 and np.sum(cols >= 256) >= 4
     ref = oracle.closed_form(H, W0[cols], M[cols])
     fb = oracle.objective(H, W0[cols], Wb[cols])
     fr = oracle.objective(H, W0[cols], ref)
