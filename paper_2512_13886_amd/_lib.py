@@ -13,7 +13,10 @@ from dataclasses import dataclass, fields
 
 import torch
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liboptima.so")
+# OPTIMA_LIBRARY names another build of the same library (the host-sanitized
+# build that the ABI tests run against); by default the in-tree library.
+_LIB_PATH = os.environ.get("OPTIMA_LIBRARY") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "liboptima.so")
 
 OPTIMA_OK = 0
 OPTIMA_E_INVAL = -1
