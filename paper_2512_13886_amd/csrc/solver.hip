@@ -184,31 +184,50 @@ __device__ inline void store_pair_planes(uint16_t* row, int g, float a, float b)
   *reinterpret_cast<uint32_t*>(blk + 32) = la | (lb << 16);
 }
 
+// What the packed update of the group at column n (a multiple of 4) of
+// column j reads besides the product: its slot code and the packed state.
+// Kernels that know j before their product is done load it early.
+struct PackedIn {
+  uint32_t code;
+  float2 ha, hw, xi, xa;
+};
+template <int MODE>
+__device__ inline PackedIn load_packed(const ProductArgs& p, int j, int n) {
+  PackedIn in{};
+  const int g = n >> 2;
+  const size_t o = size_t(j) * p.dp + 2 * g;
+  in.code = p.slot[size_t(j) * (p.dp >> 2) + g];
+  in.ha = ld2(p.HA + o);
+  if (MODE == kFused) {
+    in.hw = ld2(p.HW0 + o);
+    in.xi = ld2(p.Xin + o);
+    in.xa = ld2(p.XA + o);
+  }
+  return in;
+}
+
 // Consumes y = (H x)[j][n..n+3] for column j (n a multiple of 4); the
 // iteration products of a sparse solve update the packed vectors.
 template <int MODE>
-__device__ inline void epilogue_packed(const ProductArgs& p, int j, int n, float4 y4,
-                                       const RowCoef& c) {
+__device__ inline void finish_packed(const ProductArgs& p, int j, int n, float4 y4,
+                                     const RowCoef& c, const PackedIn& in) {
   const int g = n >> 2;
   const size_t o = size_t(j) * p.dp + 2 * g;
-  const SlotCode sc = slot_code(p.slot[size_t(j) * (p.dp >> 2) + g]);
+  const SlotCode sc = slot_code(in.code);
   const float yv[4] = {y4.x, y4.y, y4.z, y4.w};
   const float2 y2 = pick_pair(yv, sc);
   const float y[2] = {y2.x, y2.y};
   const bool keep[2] = {sc.k0, sc.k1};
+  const float hav[2] = {in.ha.x, in.ha.y};
   if (MODE == kStore) {
-    const float2 ha2 = ld2(p.HA + o);
-    const float hav[2] = {ha2.x, ha2.y};
     float ha[2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) ha[e] = (1.f - c.alpha) * hav[e] + c.alpha * y[e];
     st2(p.HA + o, make_float2(ha[0], ha[1]));
     st2(p.out1 + o, y2);
   } else {
-    const float2 ha2 = ld2(p.HA + o), hw2 = ld2(p.HW0 + o), xi2 = ld2(p.Xin + o),
-                 xa2 = ld2(p.XA + o);
-    const float hav[2] = {ha2.x, ha2.y}, hwv[2] = {hw2.x, hw2.y};
-    const float xiv[2] = {xi2.x, xi2.y}, xav[2] = {xa2.x, xa2.y};
+    const float hwv[2] = {in.hw.x, in.hw.y};
+    const float xiv[2] = {in.xi.x, in.xi.y}, xav[2] = {in.xa.x, in.xa.y};
     float ha[2], xn[2], xa[2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
@@ -221,6 +240,66 @@ __device__ inline void epilogue_packed(const ProductArgs& p, int j, int n, float
     st2(p.HA + o, make_float2(ha[0], ha[1]));
     st2(p.Xout + o, make_float2(xn[0], xn[1]));
     store_pair_planes(p.XoutP + size_t(j) * p.dp, g, xn[0], xn[1]);
+  }
+}
+
+template <int MODE>
+__device__ inline void epilogue_packed(const ProductArgs& p, int j, int n, float4 y4,
+                                       const RowCoef& c) {
+  finish_packed<MODE>(p, j, n, y4, c, load_packed<MODE>(p, j, n));
+}
+
+// What the dense update of columns n..n+3 (n a multiple of 4) of column j
+// reads besides the product (kStore, kFused).
+struct Dense4In {
+  float4 ha, hw, xi, xa;
+  bool keep[4];
+};
+template <int MODE>
+__device__ inline Dense4In load_dense4(const ProductArgs& p, int j, int n) {
+  Dense4In in{};
+  const size_t o = size_t(j) * p.dp + n;
+  in.ha = ld4(p.HA + o);
+  if (MODE == kFused) {
+    in.hw = ld4(p.HW0 + o);
+    in.xi = ld4(p.Xin + o);
+    in.xa = ld4(p.XA + o);
+    mask4(p.mask, p.d, j, n, in.keep);
+  }
+  return in;
+}
+
+// The dense update of columns n..n+3 of column j from y = (H x)[j][n..n+3].
+template <int MODE, int PREC>
+__device__ inline void finish_dense4(const ProductArgs& p, int j, int n, float4 y4,
+                                     const RowCoef& c, const Dense4In& in) {
+  const size_t o = size_t(j) * p.dp + n;
+  if (MODE == kStore) {
+    float4 ha = in.ha;
+    ha.x = (1.f - c.alpha) * ha.x + c.alpha * y4.x;
+    ha.y = (1.f - c.alpha) * ha.y + c.alpha * y4.y;
+    ha.z = (1.f - c.alpha) * ha.z + c.alpha * y4.z;
+    ha.w = (1.f - c.alpha) * ha.w + c.alpha * y4.w;
+    st4(p.HA + o, ha);
+    st4(p.out1 + o, y4);
+  } else {  // kFused: finish this iteration's products, run the next update
+    const float y[4] = {y4.x, y4.y, y4.z, y4.w};
+    const float hav[4] = {in.ha.x, in.ha.y, in.ha.z, in.ha.w};
+    const float hwv[4] = {in.hw.x, in.hw.y, in.hw.z, in.hw.w};
+    const float xiv[4] = {in.xi.x, in.xi.y, in.xi.z, in.xi.w};
+    const float xav[4] = {in.xa.x, in.xa.y, in.xa.z, in.xa.w};
+    float ha[4], xn[4], xa[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      ha[e] = (1.f - c.alpha) * hav[e] + c.alpha * y[e];
+      const float g = 2.f * ((1.f - c.alpha1) * ha[e] + c.alpha1 * y[e] - hwv[e]);
+      xn[e] = in.keep[e] ? xiv[e] - c.eta1 * g : 0.f;
+      xa[e] = (1.f - c.alpha1) * xav[e] + c.alpha1 * xn[e];
+    }
+    st4(p.XA + o, make_float4(xa[0], xa[1], xa[2], xa[3]));
+    st4(p.HA + o, make_float4(ha[0], ha[1], ha[2], ha[3]));
+    st4(p.Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
+    if (PREC == kPrecBf16x3) store_split4(p.XoutP + size_t(j) * p.dp * 2, n, xn);
   }
 }
 
@@ -239,36 +318,8 @@ __device__ inline void epilogue4(const ProductArgs& p, int j, int n, float4 y4, 
   } else if (MODE == kPlainAdd) {
     const float4 a = ld4(p.out2 + o);
     st4(p.out1 + o, make_float4(a.x + y4.x, a.y + y4.y, a.z + y4.z, a.w + y4.w));
-  } else if (MODE == kStore) {
-    float4 ha = ld4(p.HA + o);
-    ha.x = (1.f - c.alpha) * ha.x + c.alpha * y4.x;
-    ha.y = (1.f - c.alpha) * ha.y + c.alpha * y4.y;
-    ha.z = (1.f - c.alpha) * ha.z + c.alpha * y4.z;
-    ha.w = (1.f - c.alpha) * ha.w + c.alpha * y4.w;
-    st4(p.HA + o, ha);
-    st4(p.out1 + o, y4);
-  } else {  // kFused: finish this iteration's products, run the next update
-    const float4 ha4 = ld4(p.HA + o), hw4 = ld4(p.HW0 + o), xi4 = ld4(p.Xin + o),
-                 xa4 = ld4(p.XA + o);
-    const float y[4] = {y4.x, y4.y, y4.z, y4.w};
-    const float hav[4] = {ha4.x, ha4.y, ha4.z, ha4.w};
-    const float hwv[4] = {hw4.x, hw4.y, hw4.z, hw4.w};
-    const float xiv[4] = {xi4.x, xi4.y, xi4.z, xi4.w};
-    const float xav[4] = {xa4.x, xa4.y, xa4.z, xa4.w};
-    bool keep[4];
-    mask4(p.mask, p.d, j, n, keep);
-    float ha[4], xn[4], xa[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      ha[e] = (1.f - c.alpha) * hav[e] + c.alpha * y[e];
-      const float g = 2.f * ((1.f - c.alpha1) * ha[e] + c.alpha1 * y[e] - hwv[e]);
-      xn[e] = keep[e] ? xiv[e] - c.eta1 * g : 0.f;
-      xa[e] = (1.f - c.alpha1) * xav[e] + c.alpha1 * xn[e];
-    }
-    st4(p.XA + o, make_float4(xa[0], xa[1], xa[2], xa[3]));
-    st4(p.HA + o, make_float4(ha[0], ha[1], ha[2], ha[3]));
-    st4(p.Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
-    if (PREC == kPrecBf16x3) store_split4(p.XoutP + size_t(j) * p.dp * 2, n, xn);
+  } else {
+    finish_dense4<MODE, PREC>(p, j, n, y4, c, load_dense4<MODE>(p, j, n));
   }
 }
 
@@ -535,6 +586,15 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny(ProductArg
   const bool has_x = r < nr;
   const float* xrow = p.A + size_t(p.rows ? p.rows[has_x ? r : 0] : (has_x ? r : 0)) * p.dp;
   const char* hrow = reinterpret_cast<const char*>(p.Bp) + size_t(n0 + r) * p.dp * 4 + 16 * g;
+  // The update's inputs do not depend on the product: their loads go out
+  // first and land while H streams in.
+  const int t = threadIdx.x;
+  const bool upd = t < 4 * nr;
+  const int jv = upd ? (p.rows ? p.rows[t >> 2] : (t >> 2)) : 0;
+  const int nv = n0 + 4 * (t & 3);
+  Dense4In din{};
+  if (upd) din = load_dense4<MODE>(p, jv, nv);
+  const RowCoef cv = upd ? row_coef<MODE>(p, jv, *p.Lp) : RowCoef{};
   const int steps = p.dp / 32, per = steps / kSkinnyWaves;  // dp % 256 == 0
   const int s0 = wave * per, s1 = s0 + per;
   f4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -575,9 +635,7 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny(ProductArg
 #pragma unroll
   for (int e = 0; e < 4; ++e) red[wave][4 * g + e][r] = acc[e];
   __syncthreads();
-  const float L = (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f;
-  const int t = threadIdx.x;
-  if (t < 4 * nr) {
+  if (upd) {
     const int v = t >> 2, q = t & 3;
     float y[4];
 #pragma unroll
@@ -587,9 +645,7 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny(ProductArg
       for (int w = 1; w < kSkinnyWaves; ++w) a += red[w][v][4 * q + e];
       y[e] = a;
     }
-    const int j = p.rows ? p.rows[v] : v;
-    epilogue4<MODE, PREC>(p, j, n0 + 4 * q, make_float4(y[0], y[1], y[2], y[3]),
-                          row_coef<MODE>(p, j, L));
+    finish_dense4<MODE, PREC>(p, jv, nv, make_float4(y[0], y[1], y[2], y[3]), cv, din);
   }
 }
 
@@ -617,6 +673,15 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny_sparse(Pro
   const char* arow = reinterpret_cast<const char*>(p.Ap) + size_t(jx) * p.dp * 2 + 16 * g;
   const char* irow = reinterpret_cast<const char*>(p.Aidx) + size_t(jx) * (p.dp / 8) + 2 * g;
   const char* hrow = reinterpret_cast<const char*>(p.Bp) + size_t(n0 + r) * p.dp * 4 + 16 * g;
+  // The update's inputs do not depend on the product: their loads go out
+  // first and land while H streams in.
+  const int t = threadIdx.x;
+  const bool upd = t < 4 * nr;
+  const int jv = upd ? (p.rows ? p.rows[t >> 2] : (t >> 2)) : 0;
+  const int nv = n0 + 4 * (t & 3);
+  PackedIn pin{};
+  if (upd) pin = load_packed<MODE>(p, jv, nv);
+  const RowCoef cv = upd ? row_coef<MODE>(p, jv, *p.Lp) : RowCoef{};
   const int steps = p.dp / 64;
   const int s0 = steps * wave / kSkinnyWaves, s1 = steps * (wave + 1) / kSkinnyWaves;
   f4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -660,9 +725,7 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny_sparse(Pro
 #pragma unroll
   for (int e = 0; e < 4; ++e) red[wave][4 * g + e][r] = acc[e];
   __syncthreads();
-  const float L = *p.Lp;
-  const int t = threadIdx.x;
-  if (t < 4 * nr) {
+  if (upd) {
     const int v = t >> 2, q = t & 3;
     float y[4];
 #pragma unroll
@@ -672,9 +735,7 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny_sparse(Pro
       for (int w = 1; w < kSkinnyWaves; ++w) a += red[w][v][4 * q + e];
       y[e] = a;
     }
-    const int j = p.rows ? p.rows[v] : v;
-    epilogue_packed<MODE>(p, j, n0 + 4 * q, make_float4(y[0], y[1], y[2], y[3]),
-                          row_coef<MODE>(p, j, L));
+    finish_packed<MODE>(p, jv, nv, make_float4(y[0], y[1], y[2], y[3]), cv, pin);
   }
 }
 
