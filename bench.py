@@ -204,19 +204,34 @@ def product_roofline(d: int, infos: list, prec_name: str, traffic=None,
             out["mfma_issued_frac"] = 3.0 * achieved / out["mfma_issued_peak"]
             out["fp32_equivalent_frac"] = achieved / FP32_MFMA_PEAK_TFLOPS
     if few_launches and few_ms > 0:
-        # H's split planes (4 d^2 bytes) dominate these launches; per active
-        # column they add the compressed x planes (2 d bytes) and the packed
-        # update (16.25 d bytes), or x in fp32 (4 d) and the update (33 d).
+        # Iterations with at most 8 active columns. Launched one per iteration
+        # they stream H's split planes (4 d^2 bytes) from HBM each time; per
+        # active column they add the compressed x planes (2 d bytes) and the
+        # packed update (16.25 d bytes), or x in fp32 (4 d) and the update
+        # (33 d). Run as one cooperative launch per block of iterations they
+        # keep H's planes in registers: then the figure below is the rate a
+        # streaming kernel would need to match them (it can exceed the peak).
+        persistent = sum(i.get("persistent_launches", 0) for i in infos)
         per_col = (2.0 + 16.25) * d if sparse else (4.0 + 33.0) * d
         few_bytes = 4.0 * d * d * few_launches + per_col * few_rows
         few_gbs = few_bytes / (few_ms * 1e-3) / 1e9
+        if persistent:
+            name = ("k_few_persistent<sparse>" if sparse else "k_few_persistent<bf16x3>") + \
+                   (": at most 8 active columns, every iteration between two checks in one "
+                    "cooperative launch with H's planes in registers and a grid barrier per "
+                    "iteration")
+            bound = "latency"
+        else:
+            name = ("k_product_skinny_sparse" if sparse else "k_product_skinny") + \
+                   ("<fused>: the same product when at most 8 columns are active, H's planes "
+                    "streamed once per launch")
+            bound = "hbm"
         out["few_column_kernel"] = {
-            "kernel": ("k_product_skinny_sparse" if sparse else "k_product_skinny") +
-                      "<fused>: the same product when at most 8 columns are active, H's planes "
-                      "streamed once per launch",
-            "bound": "hbm", "achieved": few_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": few_gbs / HBM_PEAK_GBS, "traffic": few_traffic,
+            "kernel": name, "bound": bound, "achieved": few_gbs, "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": few_gbs / HBM_PEAK_GBS,
+            "traffic": None if persistent else few_traffic,
             "avg_launch_us": few_ms * 1e3 / few_launches, "launches": few_launches,
+            "cooperative_launches": persistent,
             "bytes_per_launch": few_bytes / few_launches}
     if all_launches and all_ms > 0:
         out["all_iteration_products"] = {

@@ -358,6 +358,16 @@ typedef struct {
                              (v_smfmac_f32_16x16x64_bf16), skipping the pruned
                              entries; the same products are formed, summed in
                              another order. 0: dense products always. */
+  int32_t cooperative;    /* 1 (default): when at most 8 columns are still active
+                             and d <= 4096, the iterations between two checks
+                             run as one cooperative launch (hipLaunchCooperativeKernel)
+                             that keeps H's split planes in registers and meets
+                             at a grid barrier between iterations; the same
+                             products and updates, bit for bit, as one launch
+                             per iteration. 0: one launch per iteration (for
+                             callers whose streams cannot take cooperative
+                             launches). Falls back to per-iteration launches
+                             by itself when the device refuses them. */
 } optima_solver_opts;
 
 typedef struct {
@@ -383,6 +393,10 @@ typedef struct {
                                  active columns with split planes: H streamed once per launch) */
   int64_t few_row_products;   /* columns multiplied by those launches */
   double few_product_ms;      /* their device time (included in timed_product_ms) */
+  int64_t persistent_launches; /* blocks of few-column iterations (the iterations between two
+                                  checks) that ran as one cooperative launch keeping H's planes
+                                  in registers (d <= 4096); each counts all of its iterations in
+                                  few_launches */
 } optima_solve_info;
 
 void optima_solver_opts_default(optima_solver_opts* opts);

@@ -54,7 +54,8 @@ class _Opts(ctypes.Structure):
                 ("beta_necessary", ctypes.c_float), ("beta_artificial", ctypes.c_float),
                 ("step_safety", ctypes.c_float), ("restarts", ctypes.c_int32),
                 ("precision", ctypes.c_int32), ("method", ctypes.c_int32),
-                ("col_scale", ctypes.c_void_p), ("sparse", ctypes.c_int32)]
+                ("col_scale", ctypes.c_void_p), ("sparse", ctypes.c_int32),
+                ("cooperative", ctypes.c_int32)]
 
 
 class _Stats(ctypes.Structure):
@@ -68,7 +69,7 @@ class _Info(ctypes.Structure):
                 ("timed_launches", ctypes.c_int64), ("timed_row_products", ctypes.c_int64),
                 ("timed_product_ms", ctypes.c_double), ("sparse_products", ctypes.c_int64),
                 ("few_launches", ctypes.c_int64), ("few_row_products", ctypes.c_int64),
-                ("few_product_ms", ctypes.c_double)]
+                ("few_product_ms", ctypes.c_double), ("persistent_launches", ctypes.c_int64)]
 
 
 def _sig(name, res, args):
@@ -81,7 +82,7 @@ def _sig(name, res, args):
 _status_string = _sig("optima_status_string", ctypes.c_char_p, [_i32])
 _abi_version = _sig("optima_abi_version", _i32, [])
 # The structs above mirror include/optima.h at this ABI version.
-ABI_VERSION = 10
+ABI_VERSION = 11
 if _abi_version() != ABI_VERSION:
     raise ImportError(f"{_LIB_PATH} has ABI version {_abi_version()}, the binding expects "
                       f"{ABI_VERSION}: rebuild the library")
@@ -179,6 +180,7 @@ class SolverOpts:
     method: int = 0
     col_scale: "torch.Tensor | None" = None  # [d] float32 device scaling D, or None
     sparse: int = 0
+    cooperative: int = 0
 
     @classmethod
     def default(cls, **overrides) -> "SolverOpts":

@@ -58,7 +58,7 @@ const char* optima_status_string(optima_status status) {
   }
 }
 
-int optima_abi_version(void) { return 10; }
+int optima_abi_version(void) { return 11; }
 
 size_t optima_hessian_workspace_bytes(int64_t n_tok, int64_t d, int dtype) {
   if (n_tok < 0 || d < 1 || d > kMaxDim) return 0;
@@ -225,6 +225,7 @@ void optima_solver_opts_default(optima_solver_opts* o) {
   o->method = OPTIMA_METHOD_RAPDHG;
   o->col_scale = nullptr;
   o->sparse = 1;
+  o->cooperative = 1;
 }
 
 size_t optima_qp_workspace_bytes(int64_t d, int64_t n_cols) {
@@ -255,6 +256,7 @@ optima_status optima_qp_solve_batched(const float* H, int64_t d, const float* la
   const optima_solver_opts& o = *opts;
   if (o.max_iters < 0 || o.check_every < 1) return OPTIMA_E_INVAL;
   if (o.sparse != 0 && o.sparse != 1) return OPTIMA_E_INVAL;
+  if (o.cooperative != 0 && o.cooperative != 1) return OPTIMA_E_INVAL;
   if (o.precision != OPTIMA_PREC_FP32 && o.precision != OPTIMA_PREC_BF16X3)
     return OPTIMA_E_UNSUPPORTED;
   if (!(o.eps_rel >= 0.f) || !(o.eps_abs >= 0.f) || !(o.step_safety >= 0.f) ||

@@ -206,9 +206,32 @@ __device__ inline PackedIn load_packed(const ProductArgs& p, int j, int n) {
   return in;
 }
 
+// Stores that other workgroups of the same cooperative launch read: relaxed
+// agent-scope atomics (sc1), which the L2s of all XCDs see without the cache
+// write-back and invalidation that a release/acquire fence costs.
+__device__ inline void store_u32_agent(void* q, uint32_t v) {
+  __hip_atomic_store(reinterpret_cast<uint32_t*>(q), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void store_f4_agent(float* q, float4 v) {
+  uint64_t* w = reinterpret_cast<uint64_t*>(q);
+  __hip_atomic_store(w, (uint64_t(__float_as_uint(v.y)) << 32) | __float_as_uint(v.x),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(w + 1, (uint64_t(__float_as_uint(v.w)) << 32) | __float_as_uint(v.z),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Loads of what other workgroups of the launch wrote (the same scope).
+__device__ inline uint4 load_u4_agent(const void* q) {
+  const uint64_t* w = reinterpret_cast<const uint64_t*>(q);
+  const uint64_t a = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t b = __hip_atomic_load(w + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_uint4(uint32_t(a), uint32_t(a >> 32), uint32_t(b), uint32_t(b >> 32));
+}
+
 // Consumes y = (H x)[j][n..n+3] for column j (n a multiple of 4); the
-// iteration products of a sparse solve update the packed vectors.
-template <int MODE>
+// iteration products of a sparse solve update the packed vectors. COHERENT:
+// the planes of the next x are stored with agent-scope atomics (the
+// cooperative few-column launch, where every workgroup reads them).
+template <int MODE, bool COHERENT = false>
 __device__ inline void finish_packed(const ProductArgs& p, int j, int n, float4 y4,
                                      const RowCoef& c, const PackedIn& in) {
   const int g = n >> 2;
@@ -239,7 +262,16 @@ __device__ inline void finish_packed(const ProductArgs& p, int j, int n, float4 
     st2(p.XA + o, make_float2(xa[0], xa[1]));
     st2(p.HA + o, make_float2(ha[0], ha[1]));
     st2(p.Xout + o, make_float2(xn[0], xn[1]));
-    store_pair_planes(p.XoutP + size_t(j) * p.dp, g, xn[0], xn[1]);
+    if (COHERENT) {
+      const uint32_t ha_ = bf16_rne_bits(xn[0]), hb_ = bf16_rne_bits(xn[1]);
+      const uint32_t la_ = bf16_rne_bits(xn[0] - bf16_bits_value(ha_));
+      const uint32_t lb_ = bf16_rne_bits(xn[1] - bf16_bits_value(hb_));
+      uint16_t* blk = p.XoutP + size_t(j) * p.dp + (g >> 4) * 64 + (g & 15) * 2;
+      store_u32_agent(blk, ha_ | (hb_ << 16));
+      store_u32_agent(blk + 32, la_ | (lb_ << 16));
+    } else {
+      store_pair_planes(p.XoutP + size_t(j) * p.dp, g, xn[0], xn[1]);
+    }
   }
 }
 
@@ -270,7 +302,9 @@ __device__ inline Dense4In load_dense4(const ProductArgs& p, int j, int n) {
 }
 
 // The dense update of columns n..n+3 of column j from y = (H x)[j][n..n+3].
-template <int MODE, int PREC>
+// COHERENT: the next x is stored with agent-scope atomics (the cooperative
+// few-column launch, where every workgroup reads it).
+template <int MODE, int PREC, bool COHERENT = false>
 __device__ inline void finish_dense4(const ProductArgs& p, int j, int n, float4 y4,
                                      const RowCoef& c, const Dense4In& in) {
   const size_t o = size_t(j) * p.dp + n;
@@ -298,7 +332,10 @@ __device__ inline void finish_dense4(const ProductArgs& p, int j, int n, float4 
     }
     st4(p.XA + o, make_float4(xa[0], xa[1], xa[2], xa[3]));
     st4(p.HA + o, make_float4(ha[0], ha[1], ha[2], ha[3]));
-    st4(p.Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
+    if (COHERENT)
+      store_f4_agent(p.Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
+    else
+      st4(p.Xout + o, make_float4(xn[0], xn[1], xn[2], xn[3]));
     if (PREC == kPrecBf16x3) store_split4(p.XoutP + size_t(j) * p.dp * 2, n, xn);
   }
 }
@@ -736,6 +773,228 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny_sparse(Pro
       y[e] = a;
     }
     finish_packed<MODE>(p, jv, nv, make_float4(y[0], y[1], y[2], y[3]), cv, pin);
+  }
+}
+
+// All iterations of a block (the iterations between two checks) with at most
+// kSkinnyRows active columns in one cooperative launch. Each workgroup owns
+// the 16 rows of H that the few-column kernels give it, and keeps their
+// split planes in registers for the whole block (16 rows x 4 dp bytes over
+// 512 lanes: 128 registers a lane at dp = 4096), so H is read from HBM once
+// per block instead of once per iteration. An iteration is the few-column
+// product (the same instructions and summation order as
+// k_product_skinny[_sparse]) and its update epilogue; the workgroups then
+// meet at a grid barrier before the next iteration reads the x just written.
+// The barrier's arrival counter and generation live in the solver workspace;
+// a wait that exceeds kBarrierPolls sets a flag that the host turns into an
+// error, so every wave always reaches the end of the kernel.
+constexpr int kPersistMaxDp = 4096;
+constexpr int kPersistBatch = 4;  // steps whose x loads are in flight together
+constexpr unsigned kBarrierPolls = 1u << 20;
+constexpr int kDirectScopeSc1 = 16;  // cache-policy bits of an agent-scope (sc1) buffer access
+
+struct PersistArgs {
+  ProductArgs p;      // rows, n_rows, dp, d, HA, HW0, XA, mask, kbase, Lp, Bp, Aidx, slot, out1
+  float* X[2];        // x of the iterations, ping-pong
+  uint16_t* XP[2];    // their split (or compressed) planes
+  uint32_t x_bytes;   // bytes of each X[] and XP[] buffer the launch may address (< 2^31)
+  int cur;            // index of the first iteration's x
+  int n_iter;         // iterations of the block; the last one stores H x in out1
+  unsigned* arrivals; // zero at the launch; barrier k completes at k * gridDim.x arrivals
+  int* timeout;       // set to 1 when a barrier wait gives up
+};
+
+// Grid barrier k (k = 1, 2, ...) of the cooperative launch. Everything that
+// crosses workgroups (the next x) is written and read with agent-scope
+// accesses, so the barrier only has to order them: each thread's stores are
+// complete (vmcnt) before its workgroup arrives, and a workgroup leaves once
+// the arrival count reaches k * gridDim.x. A wait that runs out of polls
+// raises the time-out flag; from then on every barrier of the launch returns
+// at once, so the launch ends quickly and the host reports the error.
+__device__ inline void grid_barrier(unsigned* arrivals, unsigned k, int* timeout) {
+  wait_vmcnt<0>();
+  __syncthreads();
+  if (threadIdx.x == 0 &&
+      __hip_atomic_load(timeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+    const unsigned target = k * gridDim.x;
+    unsigned seen =
+        __hip_atomic_fetch_add(arrivals, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+    unsigned polls = 0;
+    while (seen < target) {
+      if (++polls >= kBarrierPolls ||
+          __hip_atomic_load(timeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+        __hip_atomic_store(timeout, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      seen = __hip_atomic_load(arrivals, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  __syncthreads();
+}
+
+// Raw buffer over `bytes` from `base`; loads through it with the sc1 policy
+// are agent-scope (see store_u32_agent), 16 bytes at a time.
+__device__ inline __amdgpu_buffer_rsrc_t agent_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), 0x00020000);
+}
+__device__ inline uint4 load16_agent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, int(off), 0, kDirectScopeSc1);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+template <int PREC>
+__global__ void __launch_bounds__(64 * kSkinnyWaves) k_few_persistent(PersistArgs a) {
+  constexpr bool kSparse = PREC == kPrecSparse;
+  constexpr int kStepCols = kSparse ? 64 : 32;         // contraction columns per step
+  constexpr int kMaxSteps = kPersistMaxDp / kStepCols / kSkinnyWaves;  // per wave
+  constexpr int kHVec = kSparse ? 4 : 2;               // 16-byte H pieces per step
+  __shared__ float red[kSkinnyWaves][kSkinnyHRows][kSkinnyHRows + 1];
+  ProductArgs p = a.p;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * kSkinnyHRows;
+  const int nr = p.n_rows;
+  const int r = lane & 15, g = lane >> 4;
+  const bool has_x = r < nr;
+  const int jx = p.rows ? p.rows[has_x ? r : 0] : (has_x ? r : 0);
+  const int t = threadIdx.x;
+  const bool upd = t < 4 * nr;
+  const int jv = upd ? (p.rows ? p.rows[t >> 2] : (t >> 2)) : 0;
+  const int nv = n0 + 4 * (t & 3);
+  const int steps = p.dp / kStepCols;
+  const int s0 = steps * wave / kSkinnyWaves, s1 = steps * (wave + 1) / kSkinnyWaves;
+
+  // This lane's pieces of H row n0 + r for the wave's steps.
+  const char* hrow = reinterpret_cast<const char*>(p.Bp) + size_t(n0 + r) * p.dp * 4 + 16 * g;
+  uint4 hreg[kMaxSteps][kHVec];
+#pragma unroll
+  for (int k = 0; k < kMaxSteps; ++k)
+#pragma unroll
+    for (int v = 0; v < kHVec; ++v)
+      hreg[k][v] = s0 + k < s1 ? *reinterpret_cast<const uint4*>(
+                                     hrow + size_t(s0 + k) * (kStepCols * 4) + 64 * v)
+                               : make_uint4(0u, 0u, 0u, 0u);
+
+  const float L = *p.Lp;
+  int cur = a.cur;
+  p.Xin = a.X[cur];
+  PackedIn pin{};
+  Dense4In din{};
+  if (upd) {
+    if constexpr (kSparse) pin = load_packed<kFused>(p, jv, nv);
+    else din = load_dense4<kFused>(p, jv, nv);
+  }
+  for (int i = 0; i < a.n_iter; ++i) {
+    const bool last = i == a.n_iter - 1;
+    p.s = i;
+    p.Xin = a.X[cur];
+    p.Xout = a.X[cur ^ 1];
+    p.XoutP = a.XP[cur ^ 1];
+    const RowCoef cv = upd ? row_coef<kFused>(p, jv, L) : RowCoef{};
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (kSparse) {
+      const __amdgpu_buffer_rsrc_t xr = agent_rsrc(a.XP[cur], a.x_bytes);
+      const uint32_t arow = uint32_t(jx) * uint32_t(p.dp) * 2u + 16u * g;
+      const char* irow = reinterpret_cast<const char*>(p.Aidx) + size_t(jx) * (p.dp / 8) + 2 * g;
+#pragma unroll
+      for (int b = 0; b < kMaxSteps; b += kPersistBatch) {
+        uint4 ah[kPersistBatch], al[kPersistBatch];
+        int ix[kPersistBatch];
+#pragma unroll
+        for (int k = 0; k < kPersistBatch; ++k) {
+          if (s0 + b + k < s1) {
+            const uint32_t q = arow + uint32_t(s0 + b + k) * 128u;
+            ah[k] = load16_agent(xr, q);
+            al[k] = load16_agent(xr, q + 64u);
+            ix[k] = *reinterpret_cast<const uint16_t*>(irow + size_t(s0 + b + k) * 8);
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < kPersistBatch; ++k) {
+          if (s0 + b + k < s1) {
+            bf16x8 xh = __builtin_bit_cast(bf16x8, ah[k]), xl = __builtin_bit_cast(bf16x8, al[k]);
+            if (!has_x) xh = xl = bf16x8{};
+            const bf16x16 bh = sp_b_pair(__builtin_bit_cast(bf16x8, hreg[b + k][0]),
+                                         __builtin_bit_cast(bf16x8, hreg[b + k][2]));
+            const bf16x16 bl = sp_b_pair(__builtin_bit_cast(bf16x8, hreg[b + k][1]),
+                                         __builtin_bit_cast(bf16x8, hreg[b + k][3]));
+            acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(xh, bh, acc, ix[k], 0, 0);
+            acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(xh, bl, acc, ix[k], 0, 0);
+            acc = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(xl, bh, acc, ix[k], 0, 0);
+          }
+        }
+      }
+    } else {
+      const __amdgpu_buffer_rsrc_t xr = agent_rsrc(a.X[cur], a.x_bytes);
+      const uint32_t xrow = uint32_t(jx) * uint32_t(p.dp) * 4u + 32u * g;
+#pragma unroll
+      for (int b = 0; b < kMaxSteps; b += kPersistBatch) {
+        uint4 x0[kPersistBatch], x1[kPersistBatch];
+#pragma unroll
+        for (int k = 0; k < kPersistBatch; ++k) {
+          if (s0 + b + k < s1) {
+            const uint32_t q = xrow + uint32_t(s0 + b + k) * 128u;
+            x0[k] = load16_agent(xr, q);
+            x1[k] = load16_agent(xr, q + 16u);
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < kPersistBatch; ++k) {
+          if (s0 + b + k < s1) {
+            bf16x8 xh, xl;
+            split8(make_float4(__uint_as_float(x0[k].x), __uint_as_float(x0[k].y),
+                               __uint_as_float(x0[k].z), __uint_as_float(x0[k].w)),
+                   make_float4(__uint_as_float(x1[k].x), __uint_as_float(x1[k].y),
+                               __uint_as_float(x1[k].z), __uint_as_float(x1[k].w)),
+                   xh, xl);
+            if (!has_x) xh = xl = bf16x8{};
+            const bf16x8 bh = __builtin_bit_cast(bf16x8, hreg[b + k][0]);
+            const bf16x8 bl = __builtin_bit_cast(bf16x8, hreg[b + k][1]);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xh, bh, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xh, bl, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xl, bh, acc, 0, 0, 0);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) red[wave][4 * g + e][r] = acc[e];
+    __syncthreads();
+    if (upd) {
+      const int v = t >> 2, q = t & 3;
+      float y[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float sum = red[0][v][4 * q + e];
+#pragma unroll
+        for (int w = 1; w < kSkinnyWaves; ++w) sum += red[w][v][4 * q + e];
+        y[e] = sum;
+      }
+      const float4 y4 = make_float4(y[0], y[1], y[2], y[3]);
+      if constexpr (kSparse) {
+        if (last)
+          finish_packed<kStore>(p, jv, nv, y4, cv, pin);
+        else
+          finish_packed<kFused, true>(p, jv, nv, y4, cv, pin);
+      } else {
+        if (last)
+          finish_dense4<kStore, kPrecBf16x3>(p, jv, nv, y4, cv, din);
+        else
+          finish_dense4<kFused, kPrecBf16x3, true>(p, jv, nv, y4, cv, din);
+      }
+    }
+    if (!last) {
+      // The next iteration's update inputs are this thread's own stores of
+      // this iteration: their loads go out before the barrier.
+      cur ^= 1;
+      p.Xin = a.X[cur];
+      if (upd) {
+        if constexpr (kSparse) pin = load_packed<kFused>(p, jv, nv);
+        else din = load_dense4<kFused>(p, jv, nv);
+      }
+      grid_barrier(a.arrivals, unsigned(i + 1), a.timeout);
+    }
   }
 }
 
@@ -1456,6 +1715,7 @@ struct Layout {
   uint16_t* XIDX2;           // index words of the pruned part of w0
   uint8_t* SLOT;             // slot codes of the packed vectors, dp / 4 per column
   int *rows0, *rows1, *n_active, *flags;
+  unsigned* bar;             // grid barrier of k_few_persistent: arrivals
   ColState st;
 };
 
@@ -1494,6 +1754,7 @@ Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
   l.st.f_start = c.take<double>(n_cols);
   l.n_active = c.take<int>(4);
   l.flags = c.take<int>(4);
+  l.bar = c.take<unsigned>(4);
   l.L = c.take<float>(4);
   if (bytes) *bytes = c.bytes();
   return l;
@@ -1569,6 +1830,58 @@ bool few_column_path(int prec, int n_rows, int dp) {
   if (n_rows > kSkinnyRows) return false;
   if (prec == kPrecSparse) return true;
   return prec == kPrecBf16x3 && dp % (32 * kSkinnyWaves) == 0;
+}
+
+// Whether a block of few-column iterations can run as one cooperative launch
+// of k_few_persistent on the current device: cooperative launches are
+// supported and all dp / 16 workgroups fit on the device at once. Queried
+// once per device and precision.
+bool persistent_fits(int prec, int dp) {
+  static std::atomic<int> cache[64][2];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
+  const int slot = prec == kPrecSparse ? 0 : 1;
+  int blocks_per_cu = cache[dev][slot].load(std::memory_order_relaxed);
+  if (blocks_per_cu == 0) {
+    int coop = 0, n = 0;
+    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess)
+      coop = 0;
+    hipError_t e = prec == kPrecSparse
+                       ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                             &n, k_few_persistent<kPrecSparse>, 64 * kSkinnyWaves, 0)
+                       : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                             &n, k_few_persistent<kPrecBf16x3>, 64 * kSkinnyWaves, 0);
+    if (e != hipSuccess) (void)hipGetLastError();
+    blocks_per_cu = coop && e == hipSuccess && n > 0 ? n : -1;
+    cache[dev][slot].store(blocks_per_cu, std::memory_order_relaxed);
+  }
+  if (blocks_per_cu < 0) return false;
+  return int64_t(dp / kSkinnyHRows) <= int64_t(blocks_per_cu) * device_cu_count();
+}
+
+bool persistent_path(int prec, int n_rows, int dp) {
+  if (!few_column_path(prec, n_rows, dp) || dp > kPersistMaxDp) return false;
+  if (prec != kPrecSparse && (prec != kPrecBf16x3 || dp % (32 * kSkinnyWaves) != 0)) return false;
+  return persistent_fits(prec, dp);
+}
+
+// One cooperative launch for the n iterations of a block; false (nothing
+// launched) when the runtime refuses the cooperative launch.
+bool launch_persistent(const PersistArgs& a, int prec, hipStream_t s) {
+  PersistArgs arg = a;
+  void* params[] = {&arg};
+  const dim3 grid(unsigned(a.p.dp / kSkinnyHRows)), block(64 * kSkinnyWaves);
+  const hipError_t e =
+      prec == kPrecSparse
+          ? hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&k_few_persistent<kPrecSparse>),
+                                       grid, block, params, 0, s)
+          : hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&k_few_persistent<kPrecBf16x3>),
+                                       grid, block, params, 0, s);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return true;
 }
 
 template <int MODE, int PREC>
@@ -1737,6 +2050,8 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   optima_solve_info inf{};
 
   OPTIMA_HIP_TRY(hipMemsetAsync(l.flags, 0, 4 * sizeof(int), s));
+  OPTIMA_HIP_TRY(hipMemsetAsync(l.bar, 0, 4 * sizeof(unsigned), s));
+  OPTIMA_HIP_TRY(hipMemsetAsync(l.n_active, 0, 4 * sizeof(int), s));
   OPTIMA_HIP_TRY(hipMemsetAsync(l.st.done, 0, size_t(nc) * sizeof(int), s));
   const float* Hm = H;
   const bool split = o.precision == kPrecBf16x3;
@@ -1940,21 +2255,45 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     p.HW0 = l.HW0;
     p.XA = l.XA;
     if (info) OPTIMA_HIP_TRY(hipEventRecord(ev[0], s));
-    for (int i = 0; i + 1 < n; ++i) {
+    bool persisted = false;
+    if (o.cooperative && persistent_path(iprec, n_act, dp) &&
+        size_t(nc) * size_t(dp) * 4 < (size_t(1) << 31)) {
+      PersistArgs pa{};
+      pa.p = p;
+      pa.p.out1 = l.HX;
+      pa.X[0] = xbuf[0];
+      pa.X[1] = xbuf[1];
+      pa.XP[0] = xpl[0];
+      pa.XP[1] = xpl[1];
+      pa.x_bytes = uint32_t(size_t(nc) * size_t(dp) * 4);
+      pa.cur = cur;
+      pa.n_iter = n;
+      pa.arrivals = l.bar;
+      pa.timeout = l.n_active + 1;
+      OPTIMA_HIP_TRY(hipMemsetAsync(l.bar, 0, sizeof(unsigned), s));
+      persisted = launch_persistent(pa, iprec, s);
+      if (persisted) {
+        cur ^= (n - 1) & 1;
+        inf.persistent_launches += 1;
+      }
+    }
+    if (!persisted) {
+      for (int i = 0; i + 1 < n; ++i) {
+        p.A = xbuf[cur];
+        p.Ap = xpl[cur];
+        p.Xin = xbuf[cur];
+        p.Xout = xbuf[cur ^ 1];
+        p.XoutP = xpl[cur ^ 1];
+        p.s = i;
+        if (auto e = launch_product<kFused>(p, l, iprec, s)) return e;
+        cur ^= 1;
+      }
       p.A = xbuf[cur];
       p.Ap = xpl[cur];
-      p.Xin = xbuf[cur];
-      p.Xout = xbuf[cur ^ 1];
-      p.XoutP = xpl[cur ^ 1];
-      p.s = i;
-      if (auto e = launch_product<kFused>(p, l, iprec, s)) return e;
-      cur ^= 1;
+      p.out1 = l.HX;
+      p.s = n - 1;
+      if (auto e = launch_product<kStore>(p, l, iprec, s)) return e;
     }
-    p.A = xbuf[cur];
-    p.Ap = xpl[cur];
-    p.out1 = l.HX;
-    p.s = n - 1;
-    if (auto e = launch_product<kStore>(p, l, iprec, s)) return e;
     if (info) OPTIMA_HIP_TRY(hipEventRecord(ev[1], s));
     inf.gemm_calls += n;
     inf.row_products += int64_t(n) * n_act;
@@ -1979,7 +2318,10 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
                        l.n_active);
     OPTIMA_LAUNCH_CHECK();
     std::swap(rows, rows_next);
-    OPTIMA_HIP_TRY(read_back(&n_act, l.n_active, sizeof(int), s));
+    int act_timeout[2] = {0, 0};
+    OPTIMA_HIP_TRY(read_back(act_timeout, l.n_active, 2 * sizeof(int), s));
+    n_act = act_timeout[0];
+    if (act_timeout[1]) return OPTIMA_E_HIP;  // a grid barrier wait gave up
     if (info) {
       float ms = 0.f;
       OPTIMA_HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));

@@ -54,6 +54,7 @@ def test_default_options_follow_table_8():
     assert o.precision == L.PREC_BF16X3
     assert o.method == L.METHOD_RAPDHG
     assert o.sparse == 1
+    assert o.cooperative == 1
 
 
 def test_workspace_queries():
