@@ -58,9 +58,9 @@ SPECTRAL_BLOCK = 16
 
 # HBM traffic of the product kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (profiles/), valid only for the kernel sources they were taken on.
-TRAFFIC = {"sources_sha1": "83031e9020184cd01698e8f93ad9f1123919a061",
-           "bytes_per_launch": 276962 * 1024,       # k_product_sparse<fused|store>
-           "few_bytes_per_launch": 67072 * 1024}    # k_product_skinny_sparse<fused|store>
+TRAFFIC = {"sources_sha1": "c7c5d2562071c2206de5083e26e12f8d736d6881",
+           "bytes_per_launch": 277964 * 1024,       # k_product_sparse<fused>
+           "few_bytes_per_launch": 67082 * 1024}    # k_product_skinny_sparse<fused>
 
 # Per-configuration legs after the headline: (config, untimed fixed-batch
 # iterations, timed steps). The fixed-batch leg gives the iteration rate at
@@ -551,6 +551,10 @@ def main() -> int:
                     help="also run the layer loop of Algorithm 1 on a chain of four 4096 x 4096 "
                          "layers (forward propagation of the pruned activations, skip rule, "
                          "layer-wise error ratios)")
+    ap.add_argument("--no-cooperative", action="store_true",
+                    help="run the few-column iterations one launch per iteration instead of one "
+                         "cooperative launch per block (rocprofv3 counter collection ends the "
+                         "process with a crash after a cooperative launch)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="first run one 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -577,6 +581,8 @@ def main() -> int:
         del src, dst
     # Table 8: tol 0.01 / 0.01, 100000 iterations
     opts = L.SolverOpts.default()
+    if args.no_cooperative:
+        opts.cooperative = 0
     if args.precision is not None:
         opts.precision = {"fp32": L.PREC_FP32, "bf16x3": L.PREC_BF16X3}[args.precision]
     prec = opts.precision
