@@ -346,6 +346,9 @@ __device__ inline void gemm_tile_mainloop(f4 (&acc)[Cfg::MB][Cfg::NB], const Ope
 // buffered stages fit the LDS: per 64-column stage the stored A rows
 // (256 x 128 B), their index words (256 x 8 B) and the split planes of B
 // (128 x 256 B), 66 KiB, all fetched once per workgroup by direct loads.
+// The index words come stage-major (one stage's words of consecutive tile
+// rows are contiguous): with 8 bytes per row in a row-major array each
+// stage's 2 KiB would touch 256 cache lines, as many as the A rows.
 // That is 64 algorithmic flops per loaded byte, twice the dense bf16x3
 // 128 x 128 tile's 32.
 struct SpTile {
@@ -367,6 +370,7 @@ struct SpOperands {
   const char* a[SpTile::kLoadsA];  // A segment of this thread's direct loads at stage 0
   const char* b[SpTile::kLoadsB];  // B segment of this thread's direct loads at stage 0
   const char* ai;                  // its 4 bytes of index words at stage 0
+  int64_t ai_stage;                // bytes from one stage's index words to the next
 };
 
 // Tile rows fetched by this thread's direct loads and the byte offset of the
@@ -409,7 +413,7 @@ __device__ inline void sp_issue_stage(const SpOperands& src, int s, char* buf) {
                                                   (i * SpTile::kWaves + wave) * 1024),
         16, 0, 0);
   __builtin_amdgcn_global_load_lds(
-      (const __attribute__((address_space(1))) void*)(src.ai + size_t(s) * 8),
+      (const __attribute__((address_space(1))) void*)(src.ai + s * src.ai_stage),
       (__attribute__((address_space(3))) void*)(buf + SpTile::kIdxOff + wave * 256), 4, 0, 0);
 }
 

@@ -63,6 +63,9 @@ struct ProductArgs {
   const uint16_t* Ap;  // kPrecBf16x3: split planes of A (same rows as A);
                        // kPrecSparse: their 2:4-compressed form
   const uint16_t* Aidx;  // kPrecSparse: index words of the compressed rows
+  const uint16_t* AidxS;  // the same for rows 0..n_rows-1 of this product, stage-major
+                          // (k_idx_stage_major): the 2:4 tile kernel reads these
+  int idx_pitch;          // rows per stage of AidxS
   const uint16_t* Bp;  // kPrecBf16x3, kPrecSparse: split planes of H
   uint16_t* XoutP;     // kFused: split (or compressed) planes of the next x
   const uint8_t* slot; // kPrecSparse: stored positions and keep flags per group (slot_code)
@@ -547,8 +550,9 @@ __global__ void __launch_bounds__(SpTile::kThreads) k_product_sparse(ProductArgs
   for (int i = 0; i < SpTile::kLoadsB; ++i)
     src.b[i] = reinterpret_cast<const char*>(p.Bp) + size_t(n0 + sp_b_row(i)) * p.dp * 4 +
                size_t(s0) * SpTile::kBRowBytes + sp_b_seg_bytes(i);
-  src.ai = reinterpret_cast<const char*>(p.Aidx) + size_t(col_of(sp_idx_row())) * (p.dp / 8) +
-           size_t(s0) * 8 + sp_idx_bytes();
+  src.ai = reinterpret_cast<const char*>(p.AidxS) +
+           (size_t(s0) * size_t(p.idx_pitch) + size_t(m0 + sp_idx_row())) * 8 + sp_idx_bytes();
+  src.ai_stage = int64_t(p.idx_pitch) * 8;
   f4 acc[SpTile::MB][SpTile::NB];
   gemm_sparse_mainloop(acc, src, s1 - s0, lds0, lds1);
 
@@ -1699,6 +1703,22 @@ __global__ void __launch_bounds__(1024) k_compact(const int* rows_in, int n_in, 
   if (threadIdx.x == 0) *n_out = carry;
 }
 
+// Stage-major copy of the index words that the 2:4 tile product reads for
+// rows 0..n_pad-1: entry (s, r), at out + 4 (s pitch + r), holds the 8 bytes
+// of stage s of column rows[min(r, n_rows - 1)] (the tile kernel's padded
+// rows repeat the last row). One thread per entry, r fastest.
+__global__ void __launch_bounds__(kThreads) k_idx_stage_major(const uint16_t* idx, const int* rows,
+                                                              int n_rows, int n_pad, int stages,
+                                                              int pitch, uint16_t* out) {
+  const int64_t e = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (e >= int64_t(stages) * n_pad) return;
+  const int st = int(e / n_pad), r = int(e - int64_t(st) * n_pad);
+  const int rr = r < n_rows ? r : n_rows - 1;
+  const int j = rows ? rows[rr] : rr;
+  *reinterpret_cast<uint2*>(out + (size_t(st) * pitch + r) * 4) =
+      *reinterpret_cast<const uint2*>(idx + (size_t(j) * stages + st) * 4);
+}
+
 // Split-K limits: at most kMaxSplits ranges, and at most kMaxSplitTiles
 // (tile, range) pairs, which bounds the partial-sum buffer to 128 MiB.
 constexpr int kMaxSplits = 16;
@@ -1713,6 +1733,8 @@ struct Layout {
   uint16_t *XP0, *XP1, *HP;  // split planes for kPrecBf16x3
   uint16_t* XIDX;            // index words of the 2:4-compressed x planes
   uint16_t* XIDX2;           // index words of the pruned part of w0
+  uint16_t* XIDXS;           // stage-major copy for one product's rows (k_idx_stage_major)
+  int idx_pitch;             // its rows per stage: n_cols rounded up to the 2:4 tile
   uint8_t* SLOT;             // slot codes of the packed vectors, dp / 4 per column
   int *rows0, *rows1, *n_active, *flags;
   unsigned* bar;             // grid barrier of k_few_persistent: arrivals
@@ -1740,6 +1762,8 @@ Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
   l.HP = c.take<uint16_t>(2 * size_t(l.dp) * size_t(l.dp));
   l.XIDX = c.take<uint16_t>(size_t(n_cols) * size_t(l.dp / 16));
   l.XIDX2 = c.take<uint16_t>(size_t(n_cols) * size_t(l.dp / 16));
+  l.idx_pitch = int(round_up(n_cols, SpTile::BM));
+  l.XIDXS = c.take<uint16_t>(size_t(l.idx_pitch) * size_t(l.dp / 16));
   l.SLOT = c.take<uint8_t>(size_t(n_cols) * size_t(l.dp / 4));
   l.rows0 = c.take<int>(n_cols);
   l.rows1 = c.take<int>(n_cols);
@@ -1946,6 +1970,24 @@ optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t 
   return OPTIMA_OK;
 }
 
+// Before a run of 2:4 tile products over rows 0..n_rows-1 (column rows[r],
+// or r without a list): their index words from `idx` in the stage-major
+// order that k_product_sparse reads.
+optima_status stage_major_idx(const uint16_t* idx, const int* rows, int n_rows, const Layout& l,
+                              ProductArgs& p, hipStream_t s) {
+  p.AidxS = l.XIDXS;
+  p.idx_pitch = l.idx_pitch;
+  if (n_rows <= 0) return OPTIMA_OK;
+  const int stages = int(l.dp / SpTile::kKPerStage);
+  const int n_pad = int(round_up(n_rows, SpTile::BM));
+  const int64_t entries = int64_t(stages) * n_pad;
+  hipLaunchKernelGGL(k_idx_stage_major, dim3(unsigned(ceil_div(entries, kThreads))),
+                     dim3(kThreads), 0, s, idx, rows, n_rows, n_pad, stages, l.idx_pitch,
+                     l.XIDXS);
+  OPTIMA_LAUNCH_CHECK();
+  return OPTIMA_OK;
+}
+
 template <int MODE>
 optima_status launch_product(const ProductArgs& p, const Layout& l, int prec, hipStream_t s) {
   if (prec == kPrecSparse) return launch_product<MODE, kPrecSparse>(p, l, s);
@@ -2128,11 +2170,13 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     p.Aidx = l.XIDX;
     p.out1 = l.HX;
     p.out2 = l.HA;
+    if (auto e = stage_major_idx(l.XIDX, nullptr, nc, l, p, s)) return e;
     if (auto e = launch_product<kPlain2>(p, l, kPrecSparse, s)) return e;
     p.Ap = l.XP1;
     p.Aidx = l.XIDX2;
     p.out1 = l.HW0;
     p.out2 = l.HX;
+    if (auto e = stage_major_idx(l.XIDX2, nullptr, nc, l, p, s)) return e;
     if (auto e = launch_product<kPlainAdd>(p, l, kPrecSparse, s)) return e;
     p.Aidx = l.XIDX;
   } else {
@@ -2254,6 +2298,8 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
     p.HA = l.HA;
     p.HW0 = l.HW0;
     p.XA = l.XA;
+    if (iprec == kPrecSparse && !few_column_path(iprec, n_act, dp))
+      if (auto e = stage_major_idx(l.XIDX, rows, n_act, l, p, s)) return e;
     if (info) OPTIMA_HIP_TRY(hipEventRecord(ev[0], s));
     bool persisted = false;
     if (o.cooperative && persistent_path(iprec, n_act, dp) &&
