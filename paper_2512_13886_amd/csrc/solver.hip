@@ -789,13 +789,20 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_product_skinny_sparse(Pro
 // product (the same instructions and summation order as
 // k_product_skinny[_sparse]) and its update epilogue; the workgroups then
 // meet at a grid barrier before the next iteration reads the x just written.
-// The barrier's arrival counter and generation live in the solver workspace;
-// a wait that exceeds kBarrierPolls sets a flag that the host turns into an
-// error, so every wave always reaches the end of the kernel.
+// The barrier's arrival counters live in the solver workspace; a wait that
+// exceeds kBarrierPolls sets a flag that the host turns into an error, so
+// every wave always reaches the end of the kernel.
 constexpr int kPersistMaxDp = 4096;
 constexpr int kPersistBatch = 4;  // steps whose x loads are in flight together
 constexpr unsigned kBarrierPolls = 1u << 20;
 constexpr int kDirectScopeSc1 = 16;  // cache-policy bits of an agent-scope (sc1) buffer access
+// Arrival counters of the grid barrier: kBarGroups group counters and one
+// top counter, kBarStride words (128 bytes) apart. Four groups measured
+// fastest: one counter for all 256 workgroups made every arrival wait its
+// turn at one address (4.0 us a barrier against 2.4 us).
+constexpr int kBarGroups = 4;
+constexpr int kBarStride = 32;
+constexpr int kBarWords = (kBarGroups + 1) * kBarStride;
 
 struct PersistArgs {
   ProductArgs p;      // rows, n_rows, dp, d, HA, HW0, XA, mask, kbase, Lp, Bp, Aidx, slot, out1
@@ -804,25 +811,45 @@ struct PersistArgs {
   uint32_t x_bytes;   // bytes of each X[] and XP[] buffer the launch may address (< 2^31)
   int cur;            // index of the first iteration's x
   int n_iter;         // iterations of the block; the last one stores H x in out1
-  unsigned* arrivals; // zero at the launch; barrier k completes at k * gridDim.x arrivals
+  unsigned* arrivals; // kBarWords words, zero at the launch (grid_arrive)
   int* timeout;       // set to 1 when a barrier wait gives up
 };
 
-// Grid barrier k (k = 1, 2, ...) of the cooperative launch. Everything that
-// crosses workgroups (the next x) is written and read with agent-scope
+// Grid barrier k (k = 1, 2, ...) of the cooperative launch, in two halves so
+// that loads the next iteration needs can go out between them. Everything
+// that crosses workgroups (the next x) is written and read with agent-scope
 // accesses, so the barrier only has to order them: each thread's stores are
-// complete (vmcnt) before its workgroup arrives, and a workgroup leaves once
-// the arrival count reaches k * gridDim.x. A wait that runs out of polls
-// raises the time-out flag; from then on every barrier of the launch returns
-// at once, so the launch ends quickly and the host reports the error.
-__device__ inline void grid_barrier(unsigned* arrivals, unsigned k, int* timeout) {
+// complete (vmcnt) before its workgroup arrives.
+//
+// Arrival: workgroup b adds 1 to the counter of group b % G (G = min(4,
+// gridDim.x)); the counters only grow, so group g is complete for barrier k
+// at k times its size, and the workgroup whose add completes it adds 1 to
+// the top counter. Every workgroup reaches barrier k before any leaves it,
+// so no add of barrier k + 1 can be counted early. A workgroup leaves once
+// the top counter reaches k G. A wait that runs out of polls raises the
+// time-out flag; from then on every barrier of the launch returns at once,
+// so the launch ends quickly and the host reports the error.
+__device__ inline void grid_arrive(unsigned* bar, unsigned k, int* timeout) {
   wait_vmcnt<0>();
   __syncthreads();
   if (threadIdx.x == 0 &&
       __hip_atomic_load(timeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-    const unsigned target = k * gridDim.x;
-    unsigned seen =
-        __hip_atomic_fetch_add(arrivals, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+    const unsigned G = min(unsigned(kBarGroups), gridDim.x);
+    const unsigned grp = blockIdx.x % G;
+    const unsigned size = gridDim.x / G + (grp < gridDim.x % G ? 1u : 0u);
+    const unsigned old = __hip_atomic_fetch_add(bar + grp * kBarStride, 1u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+    if (old + 1u == k * size)
+      __hip_atomic_fetch_add(bar + kBarGroups * kBarStride, 1u, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+__device__ inline void grid_wait(const unsigned* bar, unsigned k, int* timeout) {
+  if (threadIdx.x == 0 &&
+      __hip_atomic_load(timeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+    const unsigned* top = bar + kBarGroups * kBarStride;
+    const unsigned target = k * min(unsigned(kBarGroups), gridDim.x);
+    unsigned seen = __hip_atomic_load(top, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     unsigned polls = 0;
     while (seen < target) {
       if (++polls >= kBarrierPolls ||
@@ -831,7 +858,7 @@ __device__ inline void grid_barrier(unsigned* arrivals, unsigned k, int* timeout
         break;
       }
       __builtin_amdgcn_s_sleep(1);
-      seen = __hip_atomic_load(arrivals, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      seen = __hip_atomic_load(top, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
   __syncthreads();
@@ -990,14 +1017,15 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_few_persistent(PersistArg
     }
     if (!last) {
       // The next iteration's update inputs are this thread's own stores of
-      // this iteration: their loads go out before the barrier.
+      // this iteration: their loads go out while the barrier waits.
       cur ^= 1;
       p.Xin = a.X[cur];
+      grid_arrive(a.arrivals, unsigned(i + 1), a.timeout);
       if (upd) {
         if constexpr (kSparse) pin = load_packed<kFused>(p, jv, nv);
         else din = load_dense4<kFused>(p, jv, nv);
       }
-      grid_barrier(a.arrivals, unsigned(i + 1), a.timeout);
+      grid_wait(a.arrivals, unsigned(i + 1), a.timeout);
     }
   }
 }
@@ -1737,7 +1765,7 @@ struct Layout {
   int idx_pitch;             // its rows per stage: n_cols rounded up to the 2:4 tile
   uint8_t* SLOT;             // slot codes of the packed vectors, dp / 4 per column
   int *rows0, *rows1, *n_active, *flags;
-  unsigned* bar;             // grid barrier of k_few_persistent: arrivals
+  unsigned* bar;             // grid barrier of k_few_persistent: arrival counters
   ColState st;
 };
 
@@ -1778,7 +1806,7 @@ Layout carve(void* ws, int64_t d, int64_t n_cols, size_t* bytes) {
   l.st.f_start = c.take<double>(n_cols);
   l.n_active = c.take<int>(4);
   l.flags = c.take<int>(4);
-  l.bar = c.take<unsigned>(4);
+  l.bar = c.take<unsigned>(kBarWords);
   l.L = c.take<float>(4);
   if (bytes) *bytes = c.bytes();
   return l;
@@ -2092,7 +2120,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   optima_solve_info inf{};
 
   OPTIMA_HIP_TRY(hipMemsetAsync(l.flags, 0, 4 * sizeof(int), s));
-  OPTIMA_HIP_TRY(hipMemsetAsync(l.bar, 0, 4 * sizeof(unsigned), s));
+  OPTIMA_HIP_TRY(hipMemsetAsync(l.bar, 0, kBarWords * sizeof(unsigned), s));
   OPTIMA_HIP_TRY(hipMemsetAsync(l.n_active, 0, 4 * sizeof(int), s));
   OPTIMA_HIP_TRY(hipMemsetAsync(l.st.done, 0, size_t(nc) * sizeof(int), s));
   const float* Hm = H;
@@ -2316,7 +2344,7 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
       pa.n_iter = n;
       pa.arrivals = l.bar;
       pa.timeout = l.n_active + 1;
-      OPTIMA_HIP_TRY(hipMemsetAsync(l.bar, 0, sizeof(unsigned), s));
+      OPTIMA_HIP_TRY(hipMemsetAsync(l.bar, 0, kBarWords * sizeof(unsigned), s));
       persisted = launch_persistent(pa, iprec, s);
       if (persisted) {
         cur ^= (n - 1) & 1;
