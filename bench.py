@@ -527,6 +527,66 @@ def chain_leg(L, torch, dev, opts) -> dict:
             "tokens": int(Xd.shape[0]), "columns": sum(r.d_out for r in reps)}
 
 
+def read_phase_stamps(L):
+    """Stamps of the instrumented library since the last call: tile-product
+    rows (start, end of main loop, end, block | mode << 32 | rows << 40) and
+    the cooperative launch's [4][256][6] per-iteration stamps."""
+    import ctypes
+    fn = ctypes.CDLL(L.library_path()).optima_phase_stamps
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    tile = np.zeros((1 << 16, 4), np.uint64)
+    coop = np.zeros((4, 256, 6), np.uint64)
+    n = fn(tile.ctypes.data, tile.shape[0], coop.ctypes.data)
+    if n < 0:
+        raise RuntimeError("optima_phase_stamps failed")
+    return tile[:n].astype(np.int64), coop.astype(np.int64)
+
+
+def summarize_phase_stamps(tile, coop) -> dict:
+    """Per-launch phases of the 2:4 tile product over more than 8 active
+    columns (fused update launches) and per-iteration phases of the last
+    cooperative launch, in microseconds (the stamps count at 100 MHz)."""
+    us = 0.01
+    out = {}
+    if len(tile):
+        order = np.argsort(tile[:, 0])
+        t = tile[order]
+        mode = (t[:, 3] >> 32) & 0xff
+        rows = t[:, 3] >> 40
+        starts = np.where(np.diff(t[:, 0]) > 2000)[0] + 1  # launches start >20 us apart
+        groups = np.split(np.arange(len(t)), starts)
+        spans, loops, loop_max, epis, epi_max, gaps = [], [], [], [], [], []
+        prev_end = None
+        for g in groups:
+            begin, end = t[g, 0].min(), t[g, 2].max()
+            if mode[g[0]] == 3 and rows[g[0]] > 8:
+                spans.append((end - begin) * us)
+                loops.append(((t[g, 1] - t[g, 0]) * us).mean())
+                loop_max.append(((t[g, 1] - t[g, 0]) * us).max())
+                epis.append(((t[g, 2] - t[g, 1]) * us).mean())
+                epi_max.append(((t[g, 2] - t[g, 1]) * us).max())
+                if prev_end is not None:
+                    gaps.append((begin - prev_end) * us)
+            prev_end = end
+        if spans:
+            out["tile_fused"] = {
+                "launches": len(spans), "span_us": float(np.mean(spans)),
+                "main_loop_us": float(np.mean(loops)), "main_loop_max_us": float(np.mean(loop_max)),
+                "epilogue_us": float(np.mean(epis)), "epilogue_max_us": float(np.mean(epi_max)),
+                "gap_before_us_median": float(np.median(gaps)) if gaps else None}
+    n_iter = int(coop[0, 0, 5])
+    if n_iter > 1:
+        c = coop[:, :n_iter - 1, :5] * us
+        d = np.diff(c, axis=2)
+        per = np.diff(c[:, :, 0], axis=1)
+        out["cooperative"] = {
+            "iterations": n_iter, "product_us": float(d[:, :, 0].mean()),
+            "reduction_us": float(d[:, :, 1].mean()), "update_us": float(d[:, :, 2].mean()),
+            "barrier_us": float(d[:, :, 3].mean()), "iteration_us": float(per.mean())}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -557,6 +617,10 @@ def main() -> int:
                          "process with a crash after a cooperative launch)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="first run one 256 MiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--phase-stamps", action="store_true",
+                    help="load the instrumented library (paper_2512_13886_amd/build.py phases) and "
+                         "report the phases of the timed steps' sparse iteration products from its "
+                         "clock stamps (the stamps add a little time to every product)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -565,6 +629,13 @@ def main() -> int:
             "Run it with --gpus 1.")
         return 2
 
+    if args.phase_stamps:
+        lib = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2512_13886_amd",
+                           "liboptima_phases.so")
+        if not os.path.exists(lib):
+            log(f"--phase-stamps needs {lib}: run python paper_2512_13886_amd/build.py phases")
+            return 1
+        os.environ["OPTIMA_LIBRARY"] = lib
     import torch
     import paper_2512_13886_amd as L
     from paper_2512_13886_amd.pipeline import spectral_step_size
@@ -604,10 +675,15 @@ def main() -> int:
         log(f"warmup step {w + 1}/{args.warmup} done")
 
     torch.cuda.synchronize()
+    if args.phase_stamps:
+        read_phase_stamps(L)  # drop the warm-up steps' stamps
     t0 = time.perf_counter()
     recs = [run.step() for _ in range(args.steps)]
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    phases = summarize_phase_stamps(*read_phase_stamps(L)) if args.phase_stamps else None
+    if phases:
+        log(f"phase stamps: {json.dumps(phases)}")
 
     ms_step = wall * 1000.0 / args.steps
     hess_ms = np.mean([e[0].elapsed_time(e[1]) for e, _ in recs])
@@ -844,6 +920,8 @@ def main() -> int:
         "roofline": roofline,
     }
     out.update(extras)
+    if phases is not None:
+        out["phase_stamps"] = phases
     if cpu is not None:
         out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)

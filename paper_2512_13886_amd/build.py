@@ -1,7 +1,8 @@
 """Builds liboptima.so (the gfx950 HIP library) in the package directory.
 
-Usage: python paper_2512_13886_amd/build.py   (or build() from Python). It runs as a
-plain script: importing the package would load the library it builds.
+Usage: python paper_2512_13886_amd/build.py [sanitized | phases]   (or build()
+from Python). It runs as a plain script: importing the package would load the
+library it builds.
 Every HIP source under csrc/ is compiled with hipcc for gfx950 only and linked
 into one shared library next to this file.
 """
@@ -94,6 +95,33 @@ def build_sanitized(verbose: bool = True) -> str:
     return SAN_LIB
 
 
+# Instrumented variant: the same kernels with clock stamps of the sparse
+# iteration products' phases (OPTIMA_PHASE_STAMPS in solver.hip), read by
+# `bench.py --phase-stamps`. It is never the library the package loads unless
+# OPTIMA_LIBRARY names it.
+PHASES_BUILD = os.path.join(BUILD, "phases")
+PHASES_LIB = os.path.join(PKG, "liboptima_phases.so")
+
+
+def build_phases(verbose: bool = True) -> str:
+    """liboptima_phases.so: the library with phase stamps compiled in."""
+    if not os.path.exists(HIPCC):
+        raise RuntimeError(f"hipcc not found at {HIPCC}")
+    os.makedirs(PHASES_BUILD, exist_ok=True)
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(lambda f: _compile(f, PHASES_BUILD, ["-DOPTIMA_PHASE_STAMPS"]), srcs))
+    tmp = PHASES_LIB + ".tmp"
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stderr}")
+    shutil.move(tmp, PHASES_LIB)
+    if verbose:
+        print(f"built {PHASES_LIB}")
+    return PHASES_LIB
+
+
 def asan_runtime() -> str:
     """Path of the clang ASan runtime that the sanitized build links against."""
     r = subprocess.run([os.path.join(os.path.dirname(HIPCC), "..", "lib", "llvm", "bin", "clang"),
@@ -111,5 +139,7 @@ def asan_runtime() -> str:
 if __name__ == "__main__":
     if len(sys.argv) > 1 and sys.argv[1] == "sanitized":
         build_sanitized()
+    elif len(sys.argv) > 1 and sys.argv[1] == "phases":
+        build_phases()
     else:
         build()

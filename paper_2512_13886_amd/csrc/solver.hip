@@ -514,6 +514,40 @@ __global__ void __launch_bounds__(WideTile::kThreads) k_product_wide(ProductArgs
   }
 }
 
+#ifdef OPTIMA_PHASE_STAMPS
+// Instrumented builds only (build.py phases): clock stamps (the 100 MHz
+// counter of wall_clock64) of the phases of the two kernels that run the
+// iteration products of a sparse solve, read back by optima_phase_stamps.
+// Each workgroup of k_product_sparse records its start, the end of its main
+// loop and its end; four workgroups of k_few_persistent record each
+// iteration's start, the end of its product, of the reduction, of the update
+// and of the barrier. Thread 0 writes them with ordinary stores.
+constexpr int kTileStampSlots = 1 << 16;
+constexpr int kCoopStampBlocks = 4, kCoopStampIters = 256;
+__device__ uint64_t g_tile_stamps[kTileStampSlots][4];
+__device__ unsigned g_tile_stamp_count;
+__device__ uint64_t g_coop_stamps[kCoopStampBlocks][kCoopStampIters][6];
+
+__device__ inline void tile_stamp(uint64_t t0, uint64_t t1, int mode, int n_rows) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint64_t t2 = wall_clock64();
+    const unsigned slot = atomicAdd(&g_tile_stamp_count, 1u);
+    if (slot < unsigned(kTileStampSlots)) {
+      g_tile_stamps[slot][0] = t0;
+      g_tile_stamps[slot][1] = t1;
+      g_tile_stamps[slot][2] = t2;
+      g_tile_stamps[slot][3] = uint64_t(blockIdx.x) | (uint64_t(mode) << 32) |
+                               (uint64_t(n_rows) << 40);
+    }
+  }
+}
+__device__ inline int coop_stamp_block() {
+  const unsigned b = blockIdx.x, n = gridDim.x;
+  return b == 0 ? 0 : b == n / 3 ? 1 : b == 2 * n / 3 ? 2 : b == n - 1 ? 3 : -1;
+}
+#endif
+
 // The iteration products with x 2:4-compressed (kPrecSparse): 256 x 128
 // tiles of 8 waves on the sparse MFMA, one workgroup per CU (132 KiB of
 // LDS). Split ranges, partial sums and the epilogue work as in k_product,
@@ -554,7 +588,13 @@ __global__ void __launch_bounds__(SpTile::kThreads) k_product_sparse(ProductArgs
            (size_t(s0) * size_t(p.idx_pitch) + size_t(m0 + sp_idx_row())) * 8 + sp_idx_bytes();
   src.ai_stage = int64_t(p.idx_pitch) * 8;
   f4 acc[SpTile::MB][SpTile::NB];
+#ifdef OPTIMA_PHASE_STAMPS
+  const uint64_t stamp0 = wall_clock64();
+#endif
   gemm_sparse_mainloop(acc, src, s1 - s0, lds0, lds1);
+#ifdef OPTIMA_PHASE_STAMPS
+  const uint64_t stamp1 = wall_clock64();
+#endif
 
   sp_stage_tile(acc, lds0, lds1);
   __syncthreads();
@@ -576,6 +616,9 @@ __global__ void __launch_bounds__(SpTile::kThreads) k_product_sparse(ProductArgs
     const int j = p.rows ? p.rows[rg] : rg;
     epilogue4<MODE, kPrecSparse>(p, j, n, y, row_coef<MODE>(p, j, L));
   }
+#ifdef OPTIMA_PHASE_STAMPS
+  tile_stamp(stamp0, stamp1, MODE, p.n_rows);
+#endif
 }
 
 // The iteration products when at most kSkinnyRows columns are still active
@@ -916,8 +959,15 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_few_persistent(PersistArg
     if constexpr (kSparse) pin = load_packed<kFused>(p, jv, nv);
     else din = load_dense4<kFused>(p, jv, nv);
   }
+#ifdef OPTIMA_PHASE_STAMPS
+  const int stamp_b = coop_stamp_block();
+  uint64_t st[6];
+#endif
   for (int i = 0; i < a.n_iter; ++i) {
     const bool last = i == a.n_iter - 1;
+#ifdef OPTIMA_PHASE_STAMPS
+    st[0] = wall_clock64();
+#endif
     p.s = i;
     p.Xin = a.X[cur];
     p.Xout = a.X[cur ^ 1];
@@ -989,9 +1039,15 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_few_persistent(PersistArg
         }
       }
     }
+#ifdef OPTIMA_PHASE_STAMPS
+    st[1] = wall_clock64();
+#endif
 #pragma unroll
     for (int e = 0; e < 4; ++e) red[wave][4 * g + e][r] = acc[e];
     __syncthreads();
+#ifdef OPTIMA_PHASE_STAMPS
+    st[2] = wall_clock64();
+#endif
     if (upd) {
       const int v = t >> 2, q = t & 3;
       float y[4];
@@ -1020,12 +1076,22 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_few_persistent(PersistArg
       // this iteration: their loads go out while the barrier waits.
       cur ^= 1;
       p.Xin = a.X[cur];
+#ifdef OPTIMA_PHASE_STAMPS
+      st[3] = wall_clock64();
+#endif
       grid_arrive(a.arrivals, unsigned(i + 1), a.timeout);
       if (upd) {
         if constexpr (kSparse) pin = load_packed<kFused>(p, jv, nv);
         else din = load_dense4<kFused>(p, jv, nv);
       }
       grid_wait(a.arrivals, unsigned(i + 1), a.timeout);
+#ifdef OPTIMA_PHASE_STAMPS
+      st[4] = wall_clock64();
+      if (stamp_b >= 0 && threadIdx.x == 0 && i < kCoopStampIters) {
+        for (int e = 0; e < 5; ++e) g_coop_stamps[stamp_b][i][e] = st[e];
+        g_coop_stamps[stamp_b][i][5] = uint64_t(a.n_iter);
+      }
+#endif
     }
   }
 }
@@ -2411,5 +2477,24 @@ optima_status qp_solve(const float* H, int64_t d, const float* lambda_max, const
   if (info) *info = inf;
   return OPTIMA_OK;
 }
+
+#ifdef OPTIMA_PHASE_STAMPS
+// Copies the stamps into host memory (tile: up to max_tile rows of 4
+// uint64; coop: 4 x 256 x 6 uint64), clears the tile count and returns the
+// number of tile stamps recorded since the last call (< 0: HIP error).
+extern "C" int optima_phase_stamps(uint64_t* tile, int max_tile, uint64_t* coop) {
+  unsigned n = 0;
+  if (hipDeviceSynchronize() != hipSuccess) return -1;
+  if (hipMemcpyFromSymbol(&n, HIP_SYMBOL(g_tile_stamp_count), sizeof(n)) != hipSuccess) return -1;
+  const size_t rows = std::min<size_t>(std::min<size_t>(n, kTileStampSlots), size_t(std::max(max_tile, 0)));
+  if (rows && hipMemcpyFromSymbol(tile, HIP_SYMBOL(g_tile_stamps), rows * 4 * sizeof(uint64_t)) != hipSuccess)
+    return -1;
+  if (coop && hipMemcpyFromSymbol(coop, HIP_SYMBOL(g_coop_stamps), sizeof(g_coop_stamps)) != hipSuccess)
+    return -1;
+  const unsigned zero = 0;
+  if (hipMemcpyToSymbol(HIP_SYMBOL(g_tile_stamp_count), &zero, sizeof(zero)) != hipSuccess) return -1;
+  return int(std::min<size_t>(n, kTileStampSlots));
+}
+#endif
 
 }  // namespace optima

@@ -36,6 +36,14 @@ def test_every_declared_symbol_is_exported(lib):
     assert not missing, missing
 
 
+def test_product_library_has_no_phase_stamps(lib):
+    # The clock stamps exist only in the instrumented build (build.py phases);
+    # the library the package loads must not carry them.
+    import paper_2512_13886_amd as L
+    if os.path.basename(L.library_path()) == "liboptima.so":
+        assert not hasattr(lib, "optima_phase_stamps")
+
+
 def test_status_strings_and_version():
     import paper_2512_13886_amd as L
     assert L.optima_abi_version() >= 1
