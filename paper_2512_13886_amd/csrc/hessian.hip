@@ -416,14 +416,16 @@ __device__ inline void grouped_tri_tile(int idx, int nt, int* ti, int* tj) {
 }
 
 // X: [n_rows][d] bf16 with n_rows >= stages * 64. The work units are the
-// (split, tile) pairs of the triangle of d / 256 blocks, split-major, tiles
-// in grouped_tri_tile order; split sp covers stages
-// [stages sp / splits, stages (sp + 1) / splits). The dispatcher sends
-// workgroup b to XCD b % 8, so XCD x runs workgroups x, x + 8, ... in that
-// order; it takes the x-th eighth of the units as one contiguous range.
-// Its 32 resident workgroups then share one token range and few feature
-// blocks, which its L2 fetches once for all of them. The grid is 8 times
-// the longest range; workgroups beyond their XCD's range exit at once.
+// (split, tile) pairs of the triangle of d / 256 blocks; split sp covers
+// stages [stages sp / splits, stages (sp + 1) / splits). The dispatcher
+// sends workgroup b to XCD b % 8, so XCD x runs workgroups x, x + 8, ... in
+// that order. XCD x owns the x-th eighth of the tiles in grouped_tri_tile
+// order (a few feature blocks) for every split, and runs them split by
+// split. Its 32 resident workgroups then share one or two token ranges and
+// few blocks, which its L2 fetches once for all of them; and all eight XCDs
+// move through the tokens together, so the device-wide cache serves one
+// XCD's misses to the others. The grid is 8 times the largest XCD share;
+// workgroups beyond their XCD's share exit at once.
 // Writes (first) or adds the tile's partial sum into part[sp] ([d][d] fp32).
 template <int WAVES>
 __global__ void __launch_bounds__(64 * WAVES) k_syrk_direct(const uint16_t* X, int64_t d,
@@ -435,14 +437,12 @@ __global__ void __launch_bounds__(64 * WAVES) k_syrk_direct(const uint16_t* X, i
   __shared__ __attribute__((aligned(1024))) char lds1[kBufBytes];
   const int nt = int(d / kBlock);
   const int n_tiles = nt * (nt + 1) / 2;
-  const int64_t units = int64_t(n_tiles) * splits;
   const int x = blockIdx.x & 7, l = blockIdx.x >> 3;
-  const int64_t u0 = units * x / 8, u1 = units * (x + 1) / 8;
-  if (u0 + l >= u1) return;
-  const int64_t u = u0 + l;
-  const int sp = int(u / n_tiles);
+  const int t0 = int(int64_t(n_tiles) * x / 8), tx = int(int64_t(n_tiles) * (x + 1) / 8) - t0;
+  if (int64_t(l) >= int64_t(tx) * splits) return;
+  const int sp = l / tx;
   int ti, tj;
-  grouped_tri_tile(int(u - int64_t(sp) * n_tiles), nt, &ti, &tj);
+  grouped_tri_tile(t0 + l % tx, nt, &ti, &tj);
   const int s0 = int(int64_t(stages) * sp / splits);
   const int s1 = int(int64_t(stages) * (sp + 1) / splits);
   const int n = s1 - s0;
@@ -519,9 +519,11 @@ struct DirectPlan {
   size_t part_elems;
 };
 
-// Grid of k_syrk_direct for `units` (split, tile) pairs: 8 times the
-// longest per-XCD range.
-unsigned direct_grid(int64_t units) { return unsigned(8 * ceil_div(units, int64_t(8))); }
+// Grid of k_syrk_direct over `tiles` tiles and `splits` splits: 8 times the
+// largest XCD share (ceil(tiles / 8) tiles, every split).
+unsigned direct_grid(int64_t tiles, int splits) {
+  return unsigned(8 * ceil_div(tiles, int64_t(8)) * splits);
+}
 
 bool direct_ok(int64_t d, int dtype) {
   return dtype == OPTIMA_DTYPE_BF16 && d % dt::kBlock == 0;
@@ -535,13 +537,14 @@ DirectPlan direct_plan(int64_t n_tok, int64_t d) {
   p.tail_rows = int(n_tok % dt::kRows);
   // Splits along the tokens: the fewest rounds of workgroups per CU relative
   // to the work, with 1% per split for the partial sums; at most 4 GiB of
-  // partials.
+  // partials. Each XCD (an eighth of the CUs) runs the largest eighth of the
+  // tiles for every split.
   int best = 1;
   double best_cost = 1e30;
   const int max_s = std::max(1, std::min(dt::kMaxSplits, p.full_stages));
   for (int S = 1; S <= max_s; ++S) {
     if (S > 1 && double(S) * double(d) * double(d) * 4.0 > double(int64_t(1) << 32)) break;
-    const double rounds = double(ceil_div(p.tiles * S, dt::kCus));
+    const double rounds = double(ceil_div(ceil_div(p.tiles, int64_t(8)) * S, dt::kCus / 8));
     const double c = rounds / S * (1.0 + 0.01 * S);
     if (c < best_cost - 1e-12) {
       best = S;
@@ -598,7 +601,7 @@ optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_
     const uint16_t* Xb = static_cast<const uint16_t*>(X);
     int splits = p.splits;
     if (p.full_stages > 0) {
-      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(direct_grid(p.tiles * splits)),
+      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(direct_grid(p.tiles, splits)),
                          dim3(64 * kDirectWaves), 0, s, Xb, d, p.full_stages, splits, part, 1);
       OPTIMA_LAUNCH_CHECK();
     } else {
@@ -608,7 +611,7 @@ optima_status hessian_accumulate(const void* X, int dtype, int64_t n_tok, int64_
       hipLaunchKernelGGL(k_tail_rows, dim3(256), dim3(kThreads), 0, s, Xb, d,
                          int64_t(p.full_stages) * dt::kRows, p.tail_rows, tail);
       OPTIMA_LAUNCH_CHECK();
-      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(direct_grid(p.tiles)),
+      hipLaunchKernelGGL(k_syrk_direct<kDirectWaves>, dim3(direct_grid(p.tiles, 1)),
                          dim3(64 * kDirectWaves), 0, s, tail, d, 1, 1, part,
                          p.full_stages > 0 ? 0 : 1);
       OPTIMA_LAUNCH_CHECK();
