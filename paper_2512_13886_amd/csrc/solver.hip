@@ -839,6 +839,7 @@ constexpr int kPersistMaxDp = 4096;
 constexpr int kPersistBatch = 4;  // steps whose x loads are in flight together
 constexpr unsigned kBarrierPolls = 1u << 20;
 constexpr int kDirectScopeSc1 = 16;  // cache-policy bits of an agent-scope (sc1) buffer access
+constexpr int kXsPitch = 2 * kPersistMaxDp + 16;  // LDS bytes per staged x row (sparse)
 // Arrival counters of the grid barrier: kBarGroups group counters and one
 // top counter, kBarStride words (128 bytes) apart. Four groups measured
 // fastest: one counter for all 256 workgroups made every arrival wait its
@@ -925,6 +926,13 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_few_persistent(PersistArg
   constexpr int kMaxSteps = kPersistMaxDp / kStepCols / kSkinnyWaves;  // per wave
   constexpr int kHVec = kSparse ? 4 : 2;               // 16-byte H pieces per step
   __shared__ float red[kSkinnyWaves][kSkinnyHRows][kSkinnyHRows + 1];
+  // Sparse: the compressed planes of the active x rows, staged once per
+  // iteration (rows kXsPitch bytes apart, which keeps the fragment reads of
+  // 16 rows on distinct banks).
+  __shared__ __attribute__((aligned(16))) char xs[kSparse ? kSkinnyRows * kXsPitch : 16];
+  // Sparse: the active rows' index words (dp / 8 bytes each), constant for
+  // the launch, copied once.
+  __shared__ __attribute__((aligned(16))) uint32_t ids[kSparse ? kSkinnyRows * kPersistMaxDp / 32 : 4];
   ProductArgs p = a.p;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * kSkinnyHRows;
@@ -950,6 +958,16 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_few_persistent(PersistArg
                                      hrow + size_t(s0 + k) * (kStepCols * 4) + 64 * v)
                                : make_uint4(0u, 0u, 0u, 0u);
 
+  if constexpr (kSparse) {
+    const int words = p.dp / 32;  // 4-byte words of one row's index words
+    for (int e = threadIdx.x; e < nr * words; e += blockDim.x) {
+      const int k = e / words, w = e - k * words;
+      const int jk = p.rows ? p.rows[k] : k;
+      ids[k * (kPersistMaxDp / 32) + w] =
+          reinterpret_cast<const uint32_t*>(p.Aidx)[size_t(jk) * words + w];
+    }
+    __syncthreads();
+  }
   const float L = *p.Lp;
   int cur = a.cur;
   p.Xin = a.X[cur];
@@ -975,9 +993,23 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_few_persistent(PersistArg
     const RowCoef cv = upd ? row_coef<kFused>(p, jv, L) : RowCoef{};
     f4 acc = {0.f, 0.f, 0.f, 0.f};
     if constexpr (kSparse) {
-      const __amdgpu_buffer_rsrc_t xr = agent_rsrc(a.XP[cur], a.x_bytes);
-      const uint32_t arow = uint32_t(jx) * uint32_t(p.dp) * 2u + 16u * g;
-      const char* irow = reinterpret_cast<const char*>(p.Aidx) + size_t(jx) * (p.dp / 8) + 2 * g;
+      // The active rows' planes (dp * 2 bytes each) into LDS by agent-scope
+      // direct loads, all in flight at once: wave w fetches the w-th KiB of
+      // every row, lanes past the row's end fetch its last 16 bytes again.
+      const int row_bytes = p.dp * 2;
+      const int off = min(wave * 1024 + lane * 16, row_bytes - 16);
+      const char* xplanes = reinterpret_cast<const char*>(a.XP[cur]);
+      for (int k = 0; k < nr; ++k) {
+        const int jk = p.rows ? p.rows[k] : k;
+        __builtin_amdgcn_global_load_lds(
+            (const __attribute__((address_space(1))) void*)(xplanes + size_t(jk) * row_bytes + off),
+            (__attribute__((address_space(3))) void*)(xs + k * kXsPitch + wave * 1024), 16, 0,
+            kDirectScopeSc1);
+      }
+      wait_vmcnt<0>();
+      __syncthreads();
+      const char* xrow = xs + (has_x ? r : 0) * kXsPitch + 16 * g;
+      const char* irow = reinterpret_cast<const char*>(ids) + (has_x ? r : 0) * (kPersistMaxDp / 8) + 2 * g;
 #pragma unroll
       for (int b = 0; b < kMaxSteps; b += kPersistBatch) {
         uint4 ah[kPersistBatch], al[kPersistBatch];
@@ -985,10 +1017,10 @@ __global__ void __launch_bounds__(64 * kSkinnyWaves) k_few_persistent(PersistArg
 #pragma unroll
         for (int k = 0; k < kPersistBatch; ++k) {
           if (s0 + b + k < s1) {
-            const uint32_t q = arow + uint32_t(s0 + b + k) * 128u;
-            ah[k] = load16_agent(xr, q);
-            al[k] = load16_agent(xr, q + 64u);
-            ix[k] = *reinterpret_cast<const uint16_t*>(irow + size_t(s0 + b + k) * 8);
+            const char* q = xrow + (s0 + b + k) * 128;
+            ah[k] = *reinterpret_cast<const uint4*>(q);
+            al[k] = *reinterpret_cast<const uint4*>(q + 64);
+            ix[k] = *reinterpret_cast<const uint16_t*>(irow + (s0 + b + k) * 8);
           }
         }
 #pragma unroll
