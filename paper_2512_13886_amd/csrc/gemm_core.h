@@ -488,11 +488,17 @@ __device__ inline void sp_stage_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Stages per iteration of the sparse main loop's unrolled body. The compiler
+// lets part of a stage's MFMAs run past the next stage barrier (they then
+// overlap the wait for the slowest wave), but not past the loop's back edge:
+// bodies of 8 stages instead of 2 made the loop about 7 % faster.
+constexpr int kSpUnroll = 8;
+
 // n stages (of 64 K values) of the sparse product, starting at the stage the
 // operand addresses point to; lds0 / lds1 are distinct __shared__ arrays of
 // SpTile::kBufBytes. The loads of stage s + 1 run during the compute of
-// stage s. (An L2 prefetch touch of stage s + 2 was measured to cost more in
-// load requests than it saved in latency.)
+// stage s; stage s is in lds0 when s is even. (An L2 prefetch touch of stage
+// s + 2 was measured to cost more in load requests than it saved in latency.)
 __device__ inline void gemm_sparse_mainloop(f4 (&acc)[SpTile::MB][SpTile::NB],
                                             const SpOperands& src, int n, char* lds0,
                                             char* lds1) {
@@ -503,7 +509,22 @@ __device__ inline void gemm_sparse_mainloop(f4 (&acc)[SpTile::MB][SpTile::NB],
   if (n <= 0) return;
   sp_issue_stage(src, 0, lds0);
   int s = 0;
-  for (; s + 1 < n; s += 2) {
+  for (; s + kSpUnroll <= n; s += kSpUnroll) {
+#pragma unroll
+    for (int u = 0; u < kSpUnroll; u += 2) {
+      sp_stage_barrier();
+      sp_issue_stage(src, s + u + 1, lds1);
+      sp_compute_stage(acc, lds0);
+      sp_stage_barrier();
+      if (u + 2 < kSpUnroll) {
+        sp_issue_stage(src, s + u + 2, lds0);
+      } else if (s + kSpUnroll < n) {
+        sp_issue_stage(src, s + kSpUnroll, lds0);
+      }
+      sp_compute_stage(acc, lds1);
+    }
+  }
+  for (; s + 1 < n; s += 2) {  // the stages left over, two at a time
     sp_stage_barrier();
     sp_issue_stage(src, s + 1, lds1);
     sp_compute_stage(acc, lds0);
