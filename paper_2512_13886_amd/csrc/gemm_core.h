@@ -125,12 +125,6 @@ struct TileCfg {
 
 // The 128 x 128 tile with 4 waves of 64 x 64 and two 128-byte stage buffers.
 using Tile128 = TileCfg<128, 128, 2, 2, 2>;
-// The 128 x 128 tile with 8 waves: two K groups of 4 waves of 64 x 64 over
-// 256-byte stages (two waves per SIMD with one workgroup per CU).
-using Tile128K2 = TileCfg<128, 128, 2, 2, 2, 2, 256>;
-// The 256 x 128 tile with 8 waves of 64 x 64 (4 x 2) and two 128-byte stage
-// buffers: a quarter fewer operand bytes per flop than the 128 x 128 tile.
-using Tile256 = TileCfg<256, 128, 4, 2, 2>;
 
 // Rows of the tile that this thread's direct loads fetch: A round i covers
 // A tile row load_row<Cfg>(i), B round i covers B tile row load_row<Cfg>(i);
@@ -246,6 +240,22 @@ __device__ inline void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
 }
 
+// Barrier of a ring of LDS stage buffers fed by direct loads: this wave's
+// loads other than its N most recent have landed and its LDS reads are
+// complete, then all waves meet. It is a bare s_barrier: the workgroup fence
+// of __syncthreads makes the compiler wait for every direct load in flight
+// (they write LDS), which would leave only the newest stage loading during
+// each compute. The empty asm statements keep the compiler from moving
+// memory accesses across.
+template <int N>
+__device__ inline void ring_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70);  // vmcnt(N) lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // src.a[i] / src.b[i]: address of the 16-byte segment this thread fetches in
 // A / B tile row load_row<Cfg>(i) at the first stage (row start +
 // load_seg_bytes<Cfg>(i)); stage s adds s * Cfg::SRB. All addresses must be
@@ -285,16 +295,13 @@ __device__ inline void gemm_tile_mainloop(f4 (&acc)[Cfg::MB][Cfg::NB], const Ope
     issue_stage<Cfg>(src, cl(1), lds1);
     int s = 0;
     for (; s + 2 < n; s += 3) {
-      wait_vmcnt<Cfg::kLoads>();  // stage s landed, stage s + 1 may still fly
-      __syncthreads();
+      ring_barrier<Cfg::kLoads>();  // stage s landed, stage s + 1 may still fly
       issue_stage<Cfg>(src, s + 2, lds2);
       compute_stage<Cfg, T>(acc, lds0);
-      wait_vmcnt<Cfg::kLoads>();
-      __syncthreads();
+      ring_barrier<Cfg::kLoads>();
       issue_stage<Cfg>(src, cl(s + 3), lds0);
       compute_stage<Cfg, T>(acc, lds1);
-      wait_vmcnt<Cfg::kLoads>();
-      __syncthreads();
+      ring_barrier<Cfg::kLoads>();
       issue_stage<Cfg>(src, cl(s + 4), lds1);
       compute_stage<Cfg, T>(acc, lds2);
     }

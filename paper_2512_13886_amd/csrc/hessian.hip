@@ -257,11 +257,13 @@ __global__ void __launch_bounds__(1024) k_damp(float* H, int64_t d, float rel, f
 //
 // Workgroup: one 256 x 256 output tile (ti, tj), ti >= tj, over a contiguous
 // range of 64-token stages; 8 waves in a 4 x 2 grid, each wave owning 64 x
-// 128 outputs (4 x 8 blocks of 16 x 16). Stage buffer: block A holds
-// X[t][256 ti + 0..255] and block B X[t][256 tj + 0..255] for the stage's 64
-// tokens, one 512-byte row per token, written by direct loads (one wave load
-// = 1 KiB = 2 token rows). Within a row the 16-byte segment g sits at
-// physical segment g ^ swz(row), which keeps both the loads' writes and the
+// 128 outputs (4 x 8 blocks of 16 x 16). The stages stream through a ring of
+// four LDS buffers of 32 tokens each, so that while one buffer is read the
+// loads of the next three are in flight. Buffer: block A holds
+// X[t][256 ti + 0..255] and block B X[t][256 tj + 0..255] for its 32 tokens,
+// one 512-byte row per token, written by direct loads (one wave load = 1 KiB
+// = 2 token rows). Within a row the 16-byte segment g sits at physical
+// segment g ^ swz(row), which keeps both the loads' writes and the
 // transposing reads free of bank conflicts.
 //
 // Operands: ds_read_b64_tr_b16 treats the eight-byte reads of each 16-lane
@@ -273,11 +275,13 @@ __global__ void __launch_bounds__(1024) k_damp(float* H, int64_t d, float rel, f
 // that a 16x16x32 bf16 MFMA takes from lane (g, i), for both operands. The
 // output block (lane, e) is then H[f_a + 4 g + e][f_b + i] as in the NT core.
 namespace dt {
-constexpr int kRows = 64;                   // tokens per stage
+constexpr int kRows = 64;                   // tokens per stage (unit of the token splits)
+constexpr int kBufRows = 32;                // tokens per ring buffer (one MFMA K step)
+constexpr int kRing = 4;                    // ring buffers
 constexpr int kBlock = 256;                 // features per operand block (tile side)
 constexpr int kRowBytes = 2 * kBlock;       // 512
-constexpr int kBlockBytes = kRows * kRowBytes;
-constexpr int kBufBytes = 2 * kBlockBytes;  // 64 KiB per stage buffer
+constexpr int kBlockBytes = kBufRows * kRowBytes;
+constexpr int kBufBytes = 2 * kBlockBytes;  // 32 KiB per ring buffer
 constexpr int kMaxSplits = 64;
 constexpr int kCus = 256;                   // MI355X compute units (sizing only)
 
@@ -292,6 +296,7 @@ struct Cfg {
   static constexpr int WGN = 2, WGM = WAVES / WGN;
   static constexpr int kMB = kBlock / WGM / 16, kNB = kBlock / WGN / 16;
   static constexpr int kLoads = kBlockBytes / 1024 / WAVES;  // wave loads per block per thread
+  static constexpr int kBufLoads = 2 * kLoads;                // per buffer (blocks A and B)
 };
 
 // Physical XOR of the 16-byte segment index for token row r of a stage:
@@ -306,7 +311,7 @@ __device__ inline uint2 tr_read(const char* p) {
   return __builtin_bit_cast(uint2, v);
 }
 
-// Direct loads of one stage. Round i of this thread fetches token row
+// Direct loads of one ring buffer. Round i of this thread fetches token row
 // row0 + 2 WAVES i (row0 = 2 wave + lane / 32) at physical segment lane % 32;
 // `a` / `b` point at that row's A / B block for round 0 without the segment
 // offset, seg[i & 1] is the logical segment's byte offset for the round.
@@ -327,18 +332,18 @@ __device__ inline void issue(const char* a, const char* b, int64_t round_bytes, 
         16, 0, 0);
 }
 
-// Operand fragments of K step kk (32 tokens) of the stage in `buf`.
+// Operand fragments of the 32 tokens in ring buffer `buf`.
 template <typename C>
-__device__ inline void read_frags(const char* buf, int kk, uint4 (&a)[C::kMB], uint4 (&b)[C::kNB]) {
+__device__ inline void read_frags(const char* buf, uint4 (&a)[C::kMB], uint4 (&b)[C::kNB]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int g = lane >> 4, j = lane & 15;
-  // Token row 32 kk + 8 g + 4 h + j / 4 has (row & 3) = j / 4 and bit 3 of
-  // the row equal to g & 1, so its swizzle depends on the lane only.
+  // Token row 8 g + 4 h + j / 4 has (row & 3) = j / 4 and bit 3 of the row
+  // equal to g & 1, so its swizzle depends on the lane only.
   const int sw = 2 * ((j >> 2) | ((g & 1) << 2));
   const int intra = 8 * (j & 1);
   const int seg_lane = (j & 3) >> 1;
-  const char* A0 = buf + (32 * kk + 8 * g + (j >> 2)) * kRowBytes;
+  const char* A0 = buf + (8 * g + (j >> 2)) * kRowBytes;
   const char* A1 = A0 + 4 * kRowBytes;
 #pragma unroll
   for (int mi = 0; mi < C::kMB; ++mi) {
@@ -369,17 +374,25 @@ __device__ inline void mfma_step(f4 (&acc)[C::kMB][C::kNB], const uint4 (&a)[C::
 template <typename C>
 __device__ inline void compute(f4 (&acc)[C::kMB][C::kNB], const char* buf) {
   constexpr int kReads = 2 * (C::kMB + C::kNB), kMfma = C::kMB * C::kNB;
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
-    uint4 a[C::kMB], b[C::kNB];
-    read_frags<C>(buf, kk, a, b);
-    mfma_step<C>(acc, a, b);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x020, 2 * C::kLoads, 0);
+  uint4 a[C::kMB], b[C::kNB];
+  read_frags<C>(buf, a, b);
+  mfma_step<C>(acc, a, b);
+  __builtin_amdgcn_sched_group_barrier(0x020, C::kBufLoads, 0);
   __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
   __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
-  __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
-  __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
+}
+
+// One step of the ring: buffer `cur` holds the next 32 tokens once this
+// wave's loads other than the two most recent buffers' have landed and every
+// wave has arrived (so every wave is also done reading `nxt`, read one step
+// earlier); then the loads of the buffer three ahead go to `nxt` and `cur` is
+// consumed.
+template <typename C>
+__device__ inline void ring_step(f4 (&acc)[C::kMB][C::kNB], const char* a, const char* b,
+                                 int64_t round_bytes, const int (&seg)[2], char* cur, char* nxt) {
+  ring_barrier<2 * C::kBufLoads>();
+  issue<C>(a, b, round_bytes, seg, nxt);
+  compute<C>(acc, cur);
 }
 
 }  // namespace dt
@@ -435,6 +448,9 @@ __global__ void __launch_bounds__(64 * WAVES) k_syrk_direct(const uint16_t* X, i
   using C = Cfg<WAVES>;
   __shared__ __attribute__((aligned(1024))) char lds0[kBufBytes];
   __shared__ __attribute__((aligned(1024))) char lds1[kBufBytes];
+  __shared__ __attribute__((aligned(1024))) char lds2[kBufBytes];
+  __shared__ __attribute__((aligned(1024))) char lds3[kBufBytes];
+  static_assert(kRing == 4 && kRows == 2 * kBufRows, "the loop below is written for this ring");
   const int nt = int(d / kBlock);
   const int n_tiles = nt * (nt + 1) / 2;
   const int x = blockIdx.x & 7, l = blockIdx.x >> 3;
@@ -454,7 +470,7 @@ __global__ void __launch_bounds__(64 * WAVES) k_syrk_direct(const uint16_t* X, i
   const char* a = xb + int64_t(ti) * kBlock * 2;
   const char* b = xb + int64_t(tj) * kBlock * 2;
   const int64_t round_bytes = 2 * WAVES * row_bytes;
-  const int64_t stage_bytes = kRows * row_bytes;
+  const int64_t buf_bytes = kBufRows * row_bytes;
 
   f4 acc[C::kMB][C::kNB];
 #pragma unroll
@@ -462,23 +478,24 @@ __global__ void __launch_bounds__(64 * WAVES) k_syrk_direct(const uint16_t* X, i
 #pragma unroll
     for (int ni = 0; ni < C::kNB; ++ni) acc[mi][ni] = f4{0.f, 0.f, 0.f, 0.f};
   if (n > 0) {
-    auto cl = [n](int q) { return q < n ? q : n - 1; };
+    // nb = 2 n buffers of 32 tokens. Loads past the last buffer repeat it
+    // (into buffers nobody reads again) so that every step waits for the
+    // same count; they are drained before the epilogue.
+    const int nb = 2 * n;
+    auto at = [nb, buf_bytes](const char* p, int q) { return p + (q < nb ? q : nb - 1) * buf_bytes; };
     issue<C>(a, b, round_bytes, seg, lds0);
+    issue<C>(at(a, 1), at(b, 1), round_bytes, seg, lds1);
+    issue<C>(at(a, 2), at(b, 2), round_bytes, seg, lds2);
     int q = 0;
-    for (; q + 1 < n; q += 2) {
-      wait_vmcnt<0>();
-      __syncthreads();
-      issue<C>(a + (q + 1) * stage_bytes, b + (q + 1) * stage_bytes, round_bytes, seg, lds1);
-      compute<C>(acc, lds0);
-      wait_vmcnt<0>();
-      __syncthreads();
-      issue<C>(a + cl(q + 2) * stage_bytes, b + cl(q + 2) * stage_bytes, round_bytes, seg, lds0);
-      compute<C>(acc, lds1);
+    for (; q + 4 <= nb; q += 4) {
+      ring_step<C>(acc, at(a, q + 3), at(b, q + 3), round_bytes, seg, lds0, lds3);
+      ring_step<C>(acc, at(a, q + 4), at(b, q + 4), round_bytes, seg, lds1, lds0);
+      ring_step<C>(acc, at(a, q + 5), at(b, q + 5), round_bytes, seg, lds2, lds1);
+      ring_step<C>(acc, at(a, q + 6), at(b, q + 6), round_bytes, seg, lds3, lds2);
     }
-    if (q < n) {
-      wait_vmcnt<0>();
-      __syncthreads();
-      compute<C>(acc, lds0);
+    if (q < nb) {
+      ring_step<C>(acc, at(a, q + 3), at(b, q + 3), round_bytes, seg, lds0, lds3);
+      ring_step<C>(acc, at(a, q + 4), at(b, q + 4), round_bytes, seg, lds1, lds0);
     }
     wait_vmcnt<0>();
     __syncthreads();

@@ -436,28 +436,67 @@ __global__ void __launch_bounds__(ProductTile::kThreads) k_product(ProductArgs p
 }
 
 // The dense products on 256 x 128 tiles of 8 waves, one workgroup per CU,
-// for long contractions (d >= kWideMinDim): a quarter fewer operand bytes per
-// flop than the 128 x 128 tile, whose loads from L2 bound it there. The 128
-// KiB accumulator tile is staged for the epilogue through the two 64 KiB
-// buffers in the layout of the sparse tile (same 4 x 2 waves of 64 x 64).
-// Split ranges, partial sums and the epilogue work as in k_product, with
-// partial rows padded to the 256-row tile.
-using WideTile = Tile256;
-constexpr int kWideStageBytes = 65536;
-constexpr int kWideMinDim = 8192;
+// for long contractions or large batches (wide_tile_path): a quarter fewer
+// operand bytes per flop than the 128 x 128 tile, whose loads from L2 bound
+// it there. Three
+// 48 KiB stage buffers keep two stages loading during each stage's MFMAs.
+// The 128 KiB accumulator tile is staged for the epilogue through them (see
+// wide_stage_row). Split ranges, partial sums and the epilogue work as in
+// k_product, with partial rows padded to the 256-row tile.
+using WideTile = TileCfg<256, 128, 4, 2, 3>;
+constexpr int kWideMinDim = 8192;    // with batches of at least kWideMinRows columns
 constexpr int kWideMinRows = 256;
+constexpr int kWideMidDim = 4096;    // with batches of at least kWideMidRows columns
+constexpr int kWideMidRows = 8192;
+
+// Where the wide tile beats the 128 x 128 tile, whose two workgroups per CU
+// overlap one's update epilogue with the other's main loop. At d = 4096 the
+// two tie at 4096 columns, the wide tile is 8 % faster at 14336 and 8 %
+// slower at 1024.
+inline bool wide_tile_path(int64_t dp, int64_t n_rows) {
+  return (dp >= kWideMinDim && n_rows >= kWideMinRows) ||
+         (dp >= kWideMidDim && n_rows >= kWideMidRows);
+}
+
+// Epilogue staging of the wide tile's 256 x 128 fp32 accumulators: tile rows
+// 32 q .. 32 q + 31 take 16 KiB region q, the (q / 3)-th 16 KiB of buffer
+// q % 3, 512 bytes per row; 16-byte column chunk c of row r sits at physical
+// chunk c ^ (r & 31), which keeps the MFMA-layout writes and the row-chunk
+// reads free of bank conflicts.
+__device__ inline char* wide_stage_row(char* lds0, char* lds1, char* lds2, int r) {
+  const int q = r >> 5;
+  char* buf = q % 3 == 0 ? lds0 : (q % 3 == 1 ? lds1 : lds2);
+  return buf + (q / 3) * 16384 + (r & 31) * 512;
+}
+__device__ inline void wide_stage_tile(const f4 (&acc)[WideTile::MB][WideTile::NB], char* lds0,
+                                       char* lds1, char* lds2) {
+  static_assert(WideTile::BM == 256 && WideTile::BN == 128, "staging covers 256 x 128 tiles");
+  static_assert(WideTile::kBufBytes >= 3 * 16384, "three 16 KiB regions per stage buffer");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WideTile::WGN, wn = wave % WideTile::WGN;
+#pragma unroll
+  for (int mi = 0; mi < WideTile::MB; ++mi)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = wm * WideTile::MB * 16 + mi * 16 + 4 * (lane >> 4) + e;
+      char* row = wide_stage_row(lds0, lds1, lds2, r);
+#pragma unroll
+      for (int ni = 0; ni < WideTile::NB; ++ni) {
+        const int col = wn * WideTile::NB * 16 + ni * 16 + (lane & 15);
+        *reinterpret_cast<float*>(row + ((col >> 2) ^ (r & 31)) * 16 + (col & 3) * 4) =
+            acc[mi][ni][e];
+      }
+    }
+}
 
 template <int MODE, int PREC>
 __global__ void __launch_bounds__(WideTile::kThreads) k_product_wide(ProductArgs p, int splits,
                                                                      float* part) {
   using Cfg = WideTile;
-  static_assert(Cfg::MB == SpTile::MB && Cfg::NB == SpTile::NB && Cfg::WGN == SpTile::WGN &&
-                    Cfg::kThreads == SpTile::kThreads && Cfg::BM == SpTile::BM &&
-                    Cfg::BN == SpTile::BN,
-                "accumulator layout of the sparse tile");
-  static_assert(Cfg::kBufBytes <= kWideStageBytes, "stage buffers");
-  __shared__ __attribute__((aligned(1024))) char lds0[kWideStageBytes];
-  __shared__ __attribute__((aligned(1024))) char lds1[kWideStageBytes];
+  static_assert(Cfg::NBUF == 3, "three stage buffers");
+  __shared__ __attribute__((aligned(1024))) char lds0[Cfg::kBufBytes];
+  __shared__ __attribute__((aligned(1024))) char lds1[Cfg::kBufBytes];
+  __shared__ __attribute__((aligned(1024))) char lds2[Cfg::kBufBytes];
   const int tiles_m = (p.n_rows + Cfg::BM - 1) / Cfg::BM;
   const int tiles_n = p.dp / Cfg::BN;
   const int n_tiles = tiles_m * tiles_n;
@@ -488,11 +527,11 @@ __global__ void __launch_bounds__(WideTile::kThreads) k_product_wide(ProductArgs
     src.b[i] = b_base + size_t(n0 + load_row<Cfg>(i)) * p.dp * 4 + k_off + load_seg_bytes<Cfg>(i);
   f4 acc[Cfg::MB][Cfg::NB];
   if (PREC == kPrecBf16x3)
-    gemm_tile_mainloop<Cfg, Bf16x3Tag>(acc, src, s1 - s0, lds0, lds1, nullptr);
+    gemm_tile_mainloop<Cfg, Bf16x3Tag>(acc, src, s1 - s0, lds0, lds1, lds2);
   else
-    gemm_tile_mainloop<Cfg, float>(acc, src, s1 - s0, lds0, lds1, nullptr);
+    gemm_tile_mainloop<Cfg, float>(acc, src, s1 - s0, lds0, lds1, lds2);
 
-  sp_stage_tile(acc, lds0, lds1);
+  wide_stage_tile(acc, lds0, lds1, lds2);
   __syncthreads();
   const float L = (MODE == kFused || MODE == kStore) ? *p.Lp : 0.f;
   float* P = part + size_t(sp) * size_t(tiles_m) * Cfg::BM * size_t(p.dp);
@@ -503,7 +542,8 @@ __global__ void __launch_bounds__(WideTile::kThreads) k_product_wide(ProductArgs
     const int r = c >> 5, ch = c & 31;
     const int rg = m0 + r;
     if (rg >= p.n_rows) continue;
-    const float4 y = sp_staged_chunk(lds0, lds1, r, ch);
+    const float4 y = *reinterpret_cast<const float4*>(wide_stage_row(lds0, lds1, lds2, r) +
+                                                       ((ch ^ (r & 31)) * 16));
     const int n = n0 + 4 * ch;
     if (splits > 1) {
       st4(P + size_t(rg) * p.dp + n, y);
@@ -2053,7 +2093,7 @@ optima_status launch_product(const ProductArgs& p, const Layout& l, hipStream_t 
     }
   }
   if constexpr (PREC == kPrecBf16x3) {
-    if (p.dp >= kWideMinDim && p.n_rows >= kWideMinRows) {
+    if (wide_tile_path(p.dp, p.n_rows)) {
       const int tiles_m = int(ceil_div(p.n_rows, WideTile::BM));
       const int tiles_n = p.dp / WideTile::BN;
       const int rows_pad = tiles_m * WideTile::BM;

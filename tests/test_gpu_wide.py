@@ -1,11 +1,13 @@
-"""GPU parity of the dense products on the 256 x 128 tile (d >= 8192).
+"""GPU parity of the dense products on the 256 x 128 tile.
 
-Long contractions (d >= 8192, at least 256 active columns) run the dense
-bf16x3 products on 256 x 128 tiles. d = 8192 with 300 columns gives two row
-tiles, the second ragged, and a split of the contraction into two ranges
-(partial sums plus the split epilogue), so every piece of that path runs.
+Long contractions (d >= 8192, at least 256 active columns) and large batches
+(d >= 4096, at least 8192 active columns) run the dense bf16x3 products on
+256 x 128 tiles. d = 8192 with 300 columns gives two row tiles, the second
+ragged, and a split of the contraction into two ranges (partial sums plus the
+split epilogue), so every piece of that path runs. d = 4096 with 8492 columns
+gives 34 row tiles, the last with 44 rows, and no split.
 
-H = B B^T / r + I with B an 8192 x 512 Gaussian matrix: symmetric positive
+H = B B^T / r + I with B a d x 512 Gaussian matrix: symmetric positive
 definite and cheap to form on the host.
 """
 import numpy as np
@@ -17,7 +19,9 @@ from gpu_util import dev, to_dev, gpu_solve, rel_fro, f32_exact, log
 
 pytestmark = pytest.mark.gpu
 
-D, N_COLS, RANK = 8192, 300, 512
+RANK = 512
+# (d, columns, seed)
+SHAPES = {"long": (8192, 300, 81), "batch": (4096, 8492, 82)}
 
 
 @pytest.fixture(scope="module")
@@ -26,9 +30,18 @@ def L():
     return lib_mod
 
 
-@pytest.fixture(scope="module")
-def problem(L):
-    rng = np.random.default_rng(81)
+_PROBLEMS = {}
+
+
+def _problem(L, shape):
+    if shape not in _PROBLEMS:
+        _PROBLEMS[shape] = _make_problem(L, shape)
+    return _PROBLEMS[shape]
+
+
+def _make_problem(L, shape):
+    D, N_COLS, seed = SHAPES[shape]
+    rng = np.random.default_rng(seed)
     B = rng.standard_normal((D, RANK))
     H = f32_exact(B @ B.T / RANK + np.eye(D))
     W0 = (rng.standard_normal((N_COLS, D)) * 0.02).astype(np.float32)
@@ -40,30 +53,44 @@ def problem(L):
     lm = torch.empty(1, dtype=torch.float32, device=dev())
     L.optima_spectral_lanczos(Hd, to_dev(rng.standard_normal(D).astype(np.float32)), lm)
     lam = float(lm.item())
-    log(f"wide: lambda_max {lam:.6e} (above 1: the identity term)")
+    log(f"wide {shape}: d {D}, {N_COLS} columns, lambda_max {lam:.6e} (above 1: the identity term)")
     assert lam > 1.0
     return H, Hd, lm, lam, W0, M
 
 
-def test_wide_trajectory_matches_oracle(L, problem):
+@pytest.fixture(scope="module")
+def problem(L):
+    return _problem(L, "long")
+
+
+@pytest.mark.parametrize("shape", ["long", "batch"])
+def test_wide_trajectory_matches_oracle(L, shape):
     # Ten iterations before any check: the iterates of the bf16x3 wide tile
-    # against the oracle's fp64 ones.
-    H, Hd, lm, lam, W0, M = problem
+    # against the oracle's fp64 ones. With fixed iterations the columns do not
+    # interact, so for the large batch the oracle runs a sample of 39 columns:
+    # 32 spread over the batch and the last 8, in the ragged last row tile.
+    H, Hd, lm, lam, W0, M = _problem(L, shape)
+    n_cols = W0.shape[0]
     T = 10
     Wg, st, info = gpu_solve(L, Hd, lm, W0, M,
                              L.SolverOpts.default(max_iters=T, fixed_iters=1, check_every=64,
                                                   precision=L.PREC_BF16X3))
-    r = oracle.rapdhg(H, W0, M, lam, oracle.SolverOptions(max_iters=T, fixed_iters=True))
+    cols = (np.arange(n_cols) if n_cols <= 512 else
+            np.unique(np.concatenate([np.linspace(0, n_cols - 1, 32).astype(int),
+                                      np.arange(n_cols - 8, n_cols)])))
+    r = oracle.rapdhg(H, W0[cols], M[cols], lam,
+                      oracle.SolverOptions(max_iters=T, fixed_iters=True))
     Wg = Wg.cpu().numpy()
     assert np.all(Wg[M == 0].view(np.uint32) == 0)
-    rel = rel_fro(Wg, r.W)
-    per_col = max(rel_fro(Wg[j], r.W[j]) for j in range(0, N_COLS, 37))
-    log(f"  T={T}: W rel_fro {rel:.3e}, worst sampled column {per_col:.3e}")
+    rel = rel_fro(Wg[cols], r.W)
+    per_col = max(rel_fro(Wg[j], r.W[i]) for i, j in enumerate(cols) if i % 7 == 0 or j >= n_cols - 8)
+    log(f"  T={T}: W rel_fro {rel:.3e} over {cols.size} columns, worst checked column {per_col:.3e}")
     assert rel <= 1e-5 and per_col <= 1e-5
 
 
 def test_wide_tight_reaches_closed_form_and_fp32(L, problem):
     H, Hd, lm, lam, W0, M = problem
+    D, N_COLS, _ = SHAPES["long"]
     opts = dict(max_iters=3000, fixed_iters=1)
     Wb, _, _ = gpu_solve(L, Hd, lm, W0, M, L.SolverOpts.default(precision=L.PREC_BF16X3, **opts))
     Wf, _, _ = gpu_solve(L, Hd, lm, W0, M, L.SolverOpts.default(precision=L.PREC_FP32, **opts))
