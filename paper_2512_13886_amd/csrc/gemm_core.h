@@ -430,38 +430,64 @@ __device__ inline void sp_issue_stage(const SpOperands& src, int s, char* buf) {
 // loads in flight.
 __device__ inline bf16x8 sp_a_frag(const char* buf, int r, int seg) {
   return *reinterpret_cast<const bf16x8*>(buf + r * SpTile::kARowBytes +
-                                          ((seg ^ (r % SpTile::kASegs)) * 16));
+                                          ((seg ^ (r & (SpTile::kASegs - 1))) * 16));
 }
 __device__ inline bf16x8 sp_b_frag16(const char* buf, int r, int seg) {
   return *reinterpret_cast<const bf16x8*>(buf + SpTile::BM * SpTile::kARowBytes +
                                           r * SpTile::kBRowBytes +
-                                          ((seg ^ (r % SpTile::kBSegs)) * 16));
+                                          ((seg ^ (r & (SpTile::kBSegs - 1))) * 16));
 }
 __device__ inline bf16x16 sp_b_pair(bf16x8 k0, bf16x8 k1) {
   return __builtin_shufflevector(k0, k1, 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
 }
 
+// Byte offsets within a stage buffer of this lane's fragment reads for the
+// first 16-row block of its A and B rows: the A hi and lo segments, the
+// index words and the four B segments (hi planes of K [0, 32) and [32, 64),
+// then the lo planes). Row block mi of A adds mi * 2048 and block ni of B
+// adds ni * 4096, which leaves the swizzles unchanged.
+struct SpFragOffsets {
+  uint32_t ah, al, ix, b0, b1, b2, b3;
+};
+__device__ inline SpFragOffsets sp_frag_offsets() {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ra = (wave / SpTile::WGN) * SpTile::MB * 16 + (lane & 15);
+  const int rb = (wave % SpTile::WGN) * SpTile::NB * 16 + (lane & 15);
+  const int g = lane >> 4, sa = ra & (SpTile::kASegs - 1), sb = rb & (SpTile::kBSegs - 1);
+  const uint32_t a0 = ra * SpTile::kARowBytes;
+  const uint32_t b = SpTile::BM * SpTile::kARowBytes + rb * SpTile::kBRowBytes;
+  return {a0 + ((g ^ sa) * 16u),        a0 + (((4 + g) ^ sa) * 16u),
+          uint32_t(SpTile::kIdxOff + ra * 8 + 2 * g),
+          b + ((g ^ sb) * 16u),         b + (((8 + g) ^ sb) * 16u),
+          b + (((4 + g) ^ sb) * 16u),   b + (((12 + g) ^ sb) * 16u)};
+}
+
 __device__ inline void sp_compute_stage(f4 (&acc)[SpTile::MB][SpTile::NB], const char* buf) {
   constexpr int MB = SpTile::MB, NB = SpTile::NB;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int ra = (wave / SpTile::WGN) * MB * 16 + (lane & 15);
-  const int rb = (wave % SpTile::WGN) * NB * 16 + (lane & 15);
-  const int g = lane >> 4;
+  // The empty asm statement makes the offsets opaque at every stage, so the
+  // compiler keeps these seven values in registers and folds each read's
+  // constant part (row block, buffer) into the read's offset field, instead
+  // of hoisting one address register per read out of the loop.
+  SpFragOffsets o = sp_frag_offsets();
+  asm volatile("" : "+v"(o.ah), "+v"(o.al), "+v"(o.ix), "+v"(o.b0), "+v"(o.b1), "+v"(o.b2),
+               "+v"(o.b3));
   bf16x8 ah[MB], al[MB];
   int ix[MB];
 #pragma unroll
   for (int mi = 0; mi < MB; ++mi) {
-    ah[mi] = sp_a_frag(buf, ra + mi * 16, g);
-    al[mi] = sp_a_frag(buf, ra + mi * 16, 4 + g);
-    ix[mi] = *reinterpret_cast<const uint16_t*>(buf + SpTile::kIdxOff + (ra + mi * 16) * 8 + 2 * g);
+    ah[mi] = *reinterpret_cast<const bf16x8*>(buf + o.ah + mi * 16 * SpTile::kARowBytes);
+    al[mi] = *reinterpret_cast<const bf16x8*>(buf + o.al + mi * 16 * SpTile::kARowBytes);
+    ix[mi] = *reinterpret_cast<const uint16_t*>(buf + o.ix + mi * 16 * 8);
   }
   // B row segments: hi planes of K [0, 32) at 0-3 and [32, 64) at 8-11, lo
   // planes at 4-7 and 12-15. Consecutive MFMAs use different accumulators.
 #pragma unroll
   for (int ni = 0; ni < NB; ++ni) {
-    const int r = rb + ni * 16;
-    const bf16x16 bh = sp_b_pair(sp_b_frag16(buf, r, g), sp_b_frag16(buf, r, 8 + g));
-    const bf16x16 bl = sp_b_pair(sp_b_frag16(buf, r, 4 + g), sp_b_frag16(buf, r, 12 + g));
+    const char* bb = buf + ni * 16 * SpTile::kBRowBytes;
+    const bf16x16 bh = sp_b_pair(*reinterpret_cast<const bf16x8*>(bb + o.b0),
+                                 *reinterpret_cast<const bf16x8*>(bb + o.b1));
+    const bf16x16 bl = sp_b_pair(*reinterpret_cast<const bf16x8*>(bb + o.b2),
+                                 *reinterpret_cast<const bf16x8*>(bb + o.b3));
 #pragma unroll
     for (int mi = 0; mi < MB; ++mi)
       acc[mi][ni] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(ah[mi],
