@@ -447,12 +447,12 @@ using WideTile = TileCfg<256, 128, 4, 2, 3>;
 constexpr int kWideMinDim = 8192;    // with batches of at least kWideMinRows columns
 constexpr int kWideMinRows = 256;
 constexpr int kWideMidDim = 4096;    // with batches of at least kWideMidRows columns
-constexpr int kWideMidRows = 8192;
+constexpr int kWideMidRows = 4096;
 
 // Where the wide tile beats the 128 x 128 tile, whose two workgroups per CU
 // overlap one's update epilogue with the other's main loop. At d = 4096 the
-// two tie at 4096 columns, the wide tile is 8 % faster at 14336 and 8 %
-// slower at 1024.
+// two tie at 4096 columns; the wide tile is 7 % faster over the 7600 to
+// 14336 columns of the gate/up solves and 8 % slower at 1024.
 inline bool wide_tile_path(int64_t dp, int64_t n_rows) {
   return (dp >= kWideMinDim && n_rows >= kWideMinRows) ||
          (dp >= kWideMidDim && n_rows >= kWideMidRows);
