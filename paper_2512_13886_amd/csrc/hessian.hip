@@ -569,7 +569,7 @@ DirectPlan direct_plan(int64_t n_tok, int64_t d) {
     }
   }
   p.splits = best;
-  p.part_elems = size_t(best) * size_t(d) * size_t(d);
+  p.part_elems = size_t(p.splits) * size_t(d) * size_t(d);  // one [d][d] partial per split
   return p;
 }
 
