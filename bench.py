@@ -58,9 +58,9 @@ SPECTRAL_BLOCK = 16
 
 # HBM traffic of the product kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (profiles/), valid only for the kernel sources they were taken on.
-TRAFFIC = {"sources_sha1": "fdef155a924b0a093fcb323f403de317096e076b",
-           "bytes_per_launch": 278760 * 1024,       # k_product_sparse<fused>
-           "few_bytes_per_launch": 67107 * 1024}    # k_product_skinny_sparse<fused>
+TRAFFIC = {"sources_sha1": "903c051551054bd90b3781d469138b49e2b9aa74",
+           "bytes_per_launch": 278758 * 1024,       # k_product_sparse<fused>
+           "few_bytes_per_launch": 67089 * 1024}    # k_product_skinny_sparse<fused>
 
 # Per-configuration legs after the headline: (config, untimed fixed-batch
 # iterations, timed steps). The fixed-batch leg gives the iteration rate at
