@@ -61,6 +61,10 @@ SPECTRAL_BLOCK = 16
 TRAFFIC = {"sources_sha1": "903c051551054bd90b3781d469138b49e2b9aa74",
            "bytes_per_launch": 278758 * 1024,       # k_product_sparse<fused>
            "few_bytes_per_launch": 67089 * 1024}    # k_product_skinny_sparse<fused>
+# The same for the Hessian's k_syrk_direct on the q_proj tokens (FETCH x 2 +
+# WRITE of its one launch), valid for the Hessian sources it was taken on.
+HESSIAN_TRAFFIC = {"sources_sha1": "725d9c628d1e3893728e22af672c5cb05c990997",
+                   "bytes_per_launch": (2 * 5889100 + 382983) * 1024}
 
 # Per-configuration legs after the headline: (config, untimed fixed-batch
 # iterations, timed steps). The fixed-batch leg gives the iteration rate at
@@ -73,12 +77,30 @@ def log(msg: str):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_sources_sha1() -> str:
+def kernel_sources_sha1(files=("gemm_core.h", "solver.hip")) -> str:
     h = hashlib.sha1()
-    for f in ("gemm_core.h", "solver.hip"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2512_13886_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
+
+
+HESSIAN_SOURCES = ("gemm_core.h", "hessian.hip")
+
+
+def hessian_roofline(n_tok: int, d: int, hess_ms: float) -> dict:
+    """The Hessian call (k_syrk_direct plus the fixed-order sum of its split
+    partials) against the dense bf16 MFMA peak, in useful flops (one
+    triangle, n_tok d^2), timed by the step's HIP events."""
+    achieved = float(n_tok) * d * d / (hess_ms * 1e-3) / 1e12
+    traffic = None
+    if HESSIAN_TRAFFIC.get("sources_sha1") == kernel_sources_sha1(HESSIAN_SOURCES):
+        traffic = HESSIAN_TRAFFIC["bytes_per_launch"]
+    return {"kernel": "k_syrk_direct (256 x 256 lower tiles, token rows in place, ring of four "
+                      "32-token LDS buffers, v_mfma_f32_16x16x32_bf16) + k_hess_reduce4",
+            "bound": "mfma", "achieved": achieved, "peak": BF16_MFMA_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": achieved / BF16_MFMA_PEAK_TFLOPS, "traffic": traffic,
+            "call_ms": hess_ms, "useful_flops": float(n_tok) * d * d}
 
 
 def cpu_baseline(cfg, X, W0, mask, H_dev: np.ndarray, lam_dev: float, sample_cols: int,
@@ -912,6 +934,7 @@ def main() -> int:
         "solve_only": {"solve_ms_median": solve_ms_median, "runs": args.steps,
                        "columns_per_s": C / (solve_ms_median * 1e-3)},
         "hessian_tflops": 2.0 * N * d * d / 2 / (hess_ms * 1e-3) / 1e12,
+        "hessian_roofline": hessian_roofline(N, d, hess_ms),
         "fixed_batch": fixed_batch,
         "configs": configs,
         "decoder_block": block,
