@@ -42,6 +42,10 @@ def _check_h(Hg: np.ndarray, Ho: np.ndarray, rel=1e-5, ent=2e-5):
     ("bf16_direct_tail_only", workloads.Q_PROJ, (50, 512)),
     ("bf16_direct_exact_stages", workloads.GPT2_FC, (640, 768)),
     ("bf16_direct_split", workloads.Q_PROJ, (8256, 1024)),
+    # one tile over 100 full stages in 32 token splits of 3 or 4 stages (6 or 8
+    # ring buffers: the unrolled body and its two-step remainder) plus a 37-row
+    # tail (two buffers: the remainder alone)
+    ("bf16_direct_ring_lengths", workloads.Q_PROJ, (6437, 256)),
 ])
 def test_hessian_parity_small(L, case):
     name, cfg, shape = case
