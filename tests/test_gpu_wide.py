@@ -5,7 +5,9 @@ Long contractions (d >= 8192, at least 256 active columns) and large batches
 256 x 128 tiles. d = 8192 with 300 columns gives two row tiles, the second
 ragged, and a split of the contraction into two ranges (partial sums plus the
 split epilogue), so every piece of that path runs. d = 4096 with 4396 columns
-gives 18 row tiles, the last with 44 rows, and no split.
+gives 18 row tiles, the last with 44 rows, and no split. d = 9216 with 256
+columns runs three ranges of 96 stages: the three-buffer loop ends without a
+remainder (the other shapes leave one or two stages).
 
 H = B B^T / r + I with B a d x 512 Gaussian matrix: symmetric positive
 definite and cheap to form on the host.
@@ -21,7 +23,7 @@ pytestmark = pytest.mark.gpu
 
 RANK = 512
 # (d, columns, seed)
-SHAPES = {"long": (8192, 300, 81), "batch": (4096, 4396, 82)}
+SHAPES = {"long": (8192, 300, 81), "batch": (4096, 4396, 82), "split3": (9216, 256, 83)}
 
 
 @pytest.fixture(scope="module")
@@ -63,19 +65,19 @@ def problem(L):
     return _problem(L, "long")
 
 
-@pytest.mark.parametrize("shape", ["long", "batch"])
+@pytest.mark.parametrize("shape", ["long", "batch", "split3"])
 def test_wide_trajectory_matches_oracle(L, shape):
     # Ten iterations before any check: the iterates of the bf16x3 wide tile
     # against the oracle's fp64 ones. With fixed iterations the columns do not
-    # interact, so for the large batch the oracle runs a sample of 39 columns:
-    # 32 spread over the batch and the last 8, in the ragged last row tile.
+    # interact, so past the first shape the oracle runs a sample of columns:
+    # 32 spread over the batch and the last 8 (in the ragged last row tile).
     H, Hd, lm, lam, W0, M = _problem(L, shape)
     n_cols = W0.shape[0]
     T = 10
     Wg, st, info = gpu_solve(L, Hd, lm, W0, M,
                              L.SolverOpts.default(max_iters=T, fixed_iters=1, check_every=64,
                                                   precision=L.PREC_BF16X3))
-    cols = (np.arange(n_cols) if n_cols <= 512 else
+    cols = (np.arange(n_cols) if shape == "long" else
             np.unique(np.concatenate([np.linspace(0, n_cols - 1, 32).astype(int),
                                       np.arange(n_cols - 8, n_cols)])))
     r = oracle.rapdhg(H, W0[cols], M[cols], lam,
