@@ -58,13 +58,13 @@ SPECTRAL_BLOCK = 16
 
 # HBM traffic of the product kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (profiles/), valid only for the kernel sources they were taken on.
-TRAFFIC = {"sources_sha1": "903c051551054bd90b3781d469138b49e2b9aa74",
+TRAFFIC = {"sources_sha1": "caba776757dbde68da49bb9b17ae5c4dba5b9493",
            "bytes_per_launch": 278758 * 1024,       # k_product_sparse<fused>
-           "few_bytes_per_launch": 67089 * 1024}    # k_product_skinny_sparse<fused>
+           "few_bytes_per_launch": 67098 * 1024}    # k_product_skinny_sparse<fused>
 # The same for the Hessian's k_syrk_direct on the q_proj tokens (FETCH x 2 +
 # WRITE of its one launch), valid for the Hessian sources it was taken on.
-HESSIAN_TRAFFIC = {"sources_sha1": "725d9c628d1e3893728e22af672c5cb05c990997",
-                   "bytes_per_launch": (2 * 5889100 + 382983) * 1024}
+HESSIAN_TRAFFIC = {"sources_sha1": "74556267ecb4153098e1288c059f918b0d8584d1",
+                   "bytes_per_launch": (2 * 5916560 + 382982) * 1024}
 
 # Per-configuration legs after the headline: (config, untimed fixed-batch
 # iterations, timed steps). The fixed-batch leg gives the iteration rate at
