@@ -232,6 +232,9 @@ struct SubState {
 // is overwritten. Run by all threads of a 256-thread workgroup; thread t owns
 // entry (t / 16, t % 16). A pivot not above kDropRel times the column's
 // original diagonal (or NaN) drops the direction: its column of L stays 0.
+// Step j updates the trailing block straight from column j of A,
+// A[i][k] -= A[i][j] A[k][j] / p (= L[i][j] L[k][j]), so that one barrier
+// per column suffices and the square root stays off the dependent chain.
 __device__ void chol_drop(double (*A)[kPitch], double (*L)[kPitch], double* diag0, int b) {
   const int t = threadIdx.x, i = t >> 4, k = t & 15;
   if (t < kMaxBlock) diag0[t] = A[t][t];
@@ -240,18 +243,24 @@ __device__ void chol_drop(double (*A)[kPitch], double (*L)[kPitch], double* diag
   for (int j = 0; j < b; ++j) {
     const double p = A[j][j];
     const bool keep = p > kDropRel * diag0[j];
-    if (keep && k == j && i >= j && i < b) L[i][j] = i == j ? sqrt(p) : A[i][j] / sqrt(p);
-    __syncthreads();
-    if (keep && i > j && k > j && i < b && k < b) A[i][k] -= L[i][j] * L[k][j];
+    if (keep) {
+      const double aij = A[i][j];
+      if (i > j && k > j && i < b && k < b) A[i][k] -= aij * (A[k][j] / p);
+      if (k == j && i >= j && i < b) L[i][j] = i == j ? sqrt(p) : aij / sqrt(p);
+    }
     __syncthreads();
   }
 }
 
 // X = L^-1 for a lower-triangular L whose zero diagonal entries mark dropped
 // directions (their rows and columns of X are 0). Thread c < 16 forms
-// column c by forward substitution with the column in registers.
+// column c by forward substitution with the column in registers; the 16
+// pivot reciprocals are formed first, in parallel.
 __device__ void inv_lower(double (*L)[kPitch], double (*X)[kPitch], int b) {
   const int c = threadIdx.x;
+  __shared__ double rpiv[kMaxBlock];
+  if (c < kMaxBlock) rpiv[c] = L[c][c] != 0.0 ? 1.0 / L[c][c] : 0.0;
+  __syncthreads();
   if (c < kMaxBlock) {
     double xc[kMaxBlock];
 #pragma unroll
@@ -259,8 +268,7 @@ __device__ void inv_lower(double (*L)[kPitch], double (*X)[kPitch], int b) {
       double s = i == c ? 1.0 : 0.0;
 #pragma unroll
       for (int k = 0; k < i; ++k) s -= k >= c ? L[i][k] * xc[k] : 0.0;
-      const double piv = L[i][i];
-      xc[i] = (i >= c && i < b && c < b && piv != 0.0) ? s / piv : 0.0;
+      xc[i] = (i >= c && i < b && c < b) ? s * rpiv[i] : 0.0;
     }
 #pragma unroll
     for (int i = 0; i < kMaxBlock; ++i) X[i][c] = xc[i];
