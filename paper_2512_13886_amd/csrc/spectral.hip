@@ -431,7 +431,8 @@ __global__ void __launch_bounds__(256) k_subspace_reduce(const double* part, int
   const int per = (nblk + kRedSegs - 1) / kRedSegs;
   const int k0 = sg * per, k1 = min(nblk, k0 + per);
   double a = 0.0;
-  for (int k = k0; k < k1; ++k) a += part[size_t(k) * kPart + e];
+#pragma unroll 8
+  for (int k = k0; k < k1; ++k) a += part[size_t(k) * kPart + e];  // eight loads in flight
   seg[sg][el] = a;
   __syncthreads();
   if (sg == 0) {
